@@ -1,0 +1,173 @@
+/*
+ * focus.h -- C ABI of the FOCUS scale-learning hot path for MI355X (gfx950).
+ *
+ * FOCUS (arXiv 2608.01847) learns FP4 block scales by gradient descent. For every linear layer of
+ * a block being calibrated, one step of the method
+ *   1. fake-quantises the weights with the learned scales (Sec. 3.2 Eq. 4, Sec. 3.3 Eq. 6-7,
+ *      Sec. 3.4 Eq. 8):  S_dq = Q_fmt(S_fp),  S_q = S_dq * c,  W_hat = Q_E2M1(W / S_q) * S_dq
+ *   2. fake-quantises the activations with dynamic absmax scales (Sec. 3.2, Sec. 4.1)
+ *   3. runs the reconstruction GEMM Y_hat = X_hat W_hat^T against the full-precision output Y_ref
+ *      with the loss L = sum((Y_hat - Y_ref)^2) / (M N)
+ *   4. back-propagates with the straight-through estimator (Sec. 3.2) to the scales S_fp and the
+ *      Coupled-Relaxation / Dual-Granularity coefficients c (Eq. 6-8).
+ * Only the FP4 codes and the dequantisation scales are exported (Fig. 3(d)).
+ *
+ * Conventions for every call:
+ *   - All tensor pointers are DEVICE pointers owned by the caller, row-major and contiguous. The
+ *     library allocates nothing; scratch memory comes from the caller's workspace `ws`.
+ *   - Blocks and sub-blocks run along K, the contiguous (input-feature / reduction) dimension.
+ *     MXFP4: block B = 32, one E8M0 scale byte per block. NVFP4: block B = 16, one E4M3 byte per
+ *     block plus one fp32 tensor scale alpha.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL is the null stream). Argument
+ *     checks happen on the host before anything is launched; a failed check returns an error and
+ *     launches nothing. No call synchronises except focus_check_flags.
+ *   - A workspace must be at least focus_workspace_size() bytes, 256-byte aligned, and zero-filled
+ *     once before its first use (its first 256 bytes hold the sticky domain-error flag that
+ *     focus_check_flags reads and clears). Calls that overlap on one workspace race.
+ *   - Sizes of 0 are valid no-ops. Each dimension must be below 2^31 and rows*K below 2^46.
+ *   - Tensor pointers must be 16-byte aligned (they are read and written with vector accesses);
+ *     a misaligned pointer is rejected with FOCUS_ERR_SHAPE.
+ *   - Results are deterministic: no atomics; every reduction has a fixed order.
+ */
+#ifndef FOCUS_H
+#define FOCUS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FOCUS_OK = 0,
+    FOCUS_ERR_NULL = 1,      /* a required pointer is NULL */
+    FOCUS_ERR_SHAPE = 2,     /* bad sizes (negative, too large, K not a multiple of the block size)
+                                or a tensor pointer that is not 16-byte aligned */
+    FOCUS_ERR_DTYPE = 3,     /* unknown dtype or unsupported dtype combination */
+    FOCUS_ERR_CONFIG = 4,    /* bad focus_qconfig (format, sub_block, ste_clip, reserved) */
+    FOCUS_ERR_WORKSPACE = 5, /* workspace NULL, misaligned or smaller than focus_workspace_size() */
+    FOCUS_ERR_DOMAIN = 6,    /* focus_check_flags: a kernel met a NaN scale or a c <= 0 / non-finite */
+    FOCUS_ERR_HIP = 7        /* the HIP runtime reported an error */
+} focus_status;
+
+typedef enum { FOCUS_MXFP4 = 0, FOCUS_NVFP4 = 1 } focus_format;
+typedef enum { FOCUS_F32 = 0, FOCUS_BF16 = 1 } focus_dtype;
+
+/* Quantisation configuration.
+ *   format    : focus_format.
+ *   sub_block : elements per coefficient c (Sec. 3.4 Eq. 8); one of 2, 4, 8, 16, 32 and a divisor
+ *               of the block size. sub_block == block size is Coupled-Relaxation Scaling with one
+ *               coefficient per block (Sec. 3.3 Eq. 6-7); the paper's default is 8.
+ *   ste_clip  : 1 -> the straight-through derivative of Q_E2M1 is the clamp's, m = [|u| <= 6];
+ *               0 -> m = 1 everywhere.
+ *   reserved  : must be 0. */
+typedef struct {
+    int32_t format;
+    int32_t sub_block;
+    int32_t ste_clip;
+    int32_t reserved;
+} focus_qconfig;
+
+typedef void *focus_stream; /* a hipStream_t */
+
+/* Which call a workspace is sized for (first argument of focus_workspace_size). */
+typedef enum {
+    FOCUS_CALL_SCALES_INIT = 0,
+    FOCUS_CALL_FAKEQUANT_FWD = 1,
+    FOCUS_CALL_FAKEQUANT_BWD = 2,
+    FOCUS_CALL_RECON_GEMM_FWD = 3,
+    FOCUS_CALL_RECON_GEMM_BWD = 4,
+    FOCUS_CALL_EXPORT_PACKED = 5
+} focus_call;
+
+/* Workspace bytes a call needs for the given sizes (M = tokens, N = rows / out features,
+ * K = in features; unused sizes are ignored). Host-only; returns 0 for invalid arguments. */
+size_t focus_workspace_size(int call, const focus_qconfig *q, int64_t M, int64_t N, int64_t K);
+
+/* Absmax initialisation of the learnable scales (Sec. 3.2 "initialized via absmax", Eq. 2-3).
+ *   W [N][K] (w_dtype) frozen weights.
+ *   MXFP4: s_fp[n][i] = fl32(max_{block i}|w| / 6)              ([N][K/32] fp32)
+ *   NVFP4: alpha = fl32(max|W| / 2688) (1 if W is all zero), written to *alpha_out (device fp32);
+ *          s_fp[n][i] = Delta_fp = fl32(max_{block i}|w| / fl32(alpha * 6))   ([N][K/16] fp32)
+ *   c [N][K/sub_block] fp32 is set to 1 (Sec. 3.3, Sec. 3.4). alpha_out may be NULL for MXFP4. */
+focus_status focus_scales_init(const focus_qconfig *q, const void *W, int w_dtype, int64_t N, int64_t K,
+                               float *s_fp, float *c, float *alpha_out,
+                               void *ws, size_t ws_bytes, focus_stream stream);
+
+/* Fake quantisation forward of one tensor X [rows][K] (x_dtype) into X_hat [rows][K] (xhat_dtype).
+ * Weight mode (s_fp != NULL; Eq. 4, 6-8, 1):
+ *   S_dq = Q_fmt(s_fp) per block (MXFP4: 2^E8M0(s_fp), rounded up; NVFP4: fl32(alpha * Q_E4M3(s_fp))),
+ *   S_q = fl32(S_dq * c) per sub-block (c == NULL means every c = 1), u = fl32(x / S_q),
+ *   code = Q_E2M1(u) (nearest, ties to even, saturating at 6), x_hat = fl32(q * S_dq).
+ *   NVFP4 needs `alpha` (device fp32 [1], the frozen tensor scale).
+ * Activation mode (s_fp == NULL, c and alpha must be NULL): scales recomputed from X by absmax
+ *   (Sec. 3.2 dynamic activation quantisation): MXFP4 S = 2^E8M0(fl32(amax/6)); NVFP4 alpha_x =
+ *   fl32(max|X| / 2688) over the whole X (1 if X is all zero), S = fl32(alpha_x * Q_E4M3(fl32(amax /
+ *   fl32(alpha_x * 6)))); alpha_x is written to *alpha_out_opt when it is non-NULL.
+ * Optional outputs: codes_opt [rows][K/2] packed FP4 codes (code = sign<<3 | magnitude index, the
+ *   even-k code in the low nibble); scale_bytes_opt [rows][K/B] (E8M0 byte e+127, or E4M3 byte).
+ * A zero dequantisation (or quantisation) scale quantises its block to signed zeros. */
+focus_status focus_fakequant_fwd(const focus_qconfig *q, const void *X, int x_dtype, int64_t rows, int64_t K,
+                                 const float *s_fp, const float *c, const float *alpha,
+                                 void *X_hat, int xhat_dtype, uint8_t *codes_opt,
+                                 uint8_t *scale_bytes_opt, float *alpha_out_opt,
+                                 void *ws, size_t ws_bytes, focus_stream stream);
+
+/* Straight-through backward of the weight fake quantisation (Sec. 3.2 STE through Eq. 6-8), given
+ * G = dL/dW_hat [N][K] fp32. With u = w / S_q and m the clamp mask:
+ *   grad_c[n][k]  = -(1/c^2) * sum_{j in sub-block k} G_j m_j w_j               ([N][K/sub_block])
+ *   grad_s[n][i]  = f * sum_{j in block i} G_j (q_j - m_j u_j)                   ([N][K/B])
+ * where f = 1 for MXFP4 (STE through Q_E8M0) and f = alpha for NVFP4 (Delta_fp, alpha frozen).
+ * Outputs are fp32 and overwritten. Blocks with a zero scale get zero gradients. */
+focus_status focus_fakequant_bwd(const focus_qconfig *q, const float *G, int64_t N, int64_t K,
+                                 const void *W, int w_dtype, const float *s_fp, const float *c,
+                                 const float *alpha, float *grad_s, float *grad_c,
+                                 void *ws, size_t ws_bytes, focus_stream stream);
+
+/* Reconstruction GEMM forward with the MSE epilogue.
+ *   X_hat [M][K], W_hat [N][K] in op_dtype (FOCUS_BF16: bf16 MFMA with fp32 accumulation;
+ *   FOCUS_F32: fp32), Y_hat = X_hat W_hat^T.
+ *   Y_ref == NULL: plain GEMM, Y_hat is written to dY [M][N] (op_dtype).
+ *   Y_ref != NULL ([M][N], op_dtype): D = Y_hat - Y_ref, dY = fl(2 D / (M N)) (op_dtype),
+ *     *loss_out (device double) = sum(D^2) / (M N) and, if col_sq_opt != NULL, col_sq_opt[n]
+ *     (device double [N]) = sum over tokens of D[t][n]^2. */
+focus_status focus_recon_gemm_fwd(const void *X_hat, const void *W_hat, int op_dtype,
+                                  int64_t M, int64_t N, int64_t K, const void *Y_ref, void *dY,
+                                  double *loss_out, double *col_sq_opt,
+                                  void *ws, size_t ws_bytes, focus_stream stream);
+
+/* Reconstruction GEMM backward with the fused straight-through epilogue.
+ *   G = dY^T X_hat ([N][K], the reduction runs over the M tokens, fp32 accumulation) is formed
+ *   tile by tile and reduced at once into grad_s [N][K/B] and grad_c [N][K/sub_block] exactly as
+ *   in focus_fakequant_bwd, from W [N][K] (w_dtype), s_fp, c (NULL = ones) and alpha (NVFP4).
+ *   dY [M][N] and X_hat [M][K] are in op_dtype. If G_out_opt != NULL the fp32 G is also written.
+ *   Long token ranges are split across workgroups; the per-split partial gradients are summed in a
+ *   fixed order. */
+focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const void *X_hat, int op_dtype,
+                                  int64_t M, int64_t N, int64_t K,
+                                  const void *W, int w_dtype, const float *s_fp, const float *c,
+                                  const float *alpha, float *grad_s, float *grad_c, float *G_out_opt,
+                                  void *ws, size_t ws_bytes, focus_stream stream);
+
+/* Export of the deployable tensor (Fig. 3(d): only FP4 codes and dequantisation scales are kept;
+ * the coefficients and S_q are discarded): packed [N][K/2] codes as in focus_fakequant_fwd and
+ * scale_bytes [N][K/B]. The NVFP4 tensor scale is the caller's frozen alpha. */
+focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dtype, int64_t N, int64_t K,
+                                 const float *s_fp, const float *c, const float *alpha,
+                                 uint8_t *packed, uint8_t *scale_bytes,
+                                 void *ws, size_t ws_bytes, focus_stream stream);
+
+/* Synchronises `stream`, reads and clears the workspace's sticky domain flag. Returns
+ * FOCUS_ERR_DOMAIN if any call on this workspace met a NaN scale or a coefficient c that is
+ * <= 0 or not finite since the last check (outputs of such blocks are unspecified), FOCUS_OK
+ * otherwise, FOCUS_ERR_HIP on a runtime error. */
+focus_status focus_check_flags(void *ws, focus_stream stream);
+
+/* Static description of a status code. */
+const char *focus_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FOCUS_H */

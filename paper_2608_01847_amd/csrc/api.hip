@@ -1,0 +1,229 @@
+// extern "C" entry points of libfocus: host-side argument checks, workspace layout and dispatch.
+// Every check runs before anything is launched; a failed check launches nothing.
+#include "../../include/focus.h"
+#include "focus_device.h"
+#include "gemm_common.h"
+#include "internal.h"
+
+#include <initializer_list>
+
+using namespace focus;
+
+namespace {
+
+constexpr int64_t kMaxDim = (int64_t(1) << 31) - 1;
+constexpr int64_t kMaxElems = int64_t(1) << 46;
+
+focus_status check_q(const focus_qconfig *q) {
+    if (!q) return FOCUS_ERR_NULL;
+    if (q->format != FOCUS_MXFP4 && q->format != FOCUS_NVFP4) return FOCUS_ERR_CONFIG;
+    const int B = block_of(q->format), sb = q->sub_block;
+    if (!(sb == 2 || sb == 4 || sb == 8 || sb == 16 || sb == 32) || B % sb != 0) return FOCUS_ERR_CONFIG;
+    if (q->ste_clip != 0 && q->ste_clip != 1) return FOCUS_ERR_CONFIG;
+    if (q->reserved != 0) return FOCUS_ERR_CONFIG;
+    return FOCUS_OK;
+}
+
+bool dtype_ok(int d) { return d == FOCUS_F32 || d == FOCUS_BF16; }
+
+focus_status check_rows_k(int64_t rows, int64_t K, int B) {
+    if (rows < 0 || K < 0 || rows > kMaxDim || K > kMaxDim) return FOCUS_ERR_SHAPE;
+    if (K % B != 0) return FOCUS_ERR_SHAPE;
+    if (rows > 0 && K > 0 && rows > kMaxElems / K) return FOCUS_ERR_SHAPE;
+    return FOCUS_OK;
+}
+
+focus_status check_ws(const void *ws, size_t bytes, size_t need) {
+    if (!ws || (reinterpret_cast<uintptr_t>(ws) % 256) != 0 || bytes < need) return FOCUS_ERR_WORKSPACE;
+    return FOCUS_OK;
+}
+
+// tensors are read and written with 16-byte vector accesses
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool all_aligned(std::initializer_list<const void *> ps) {
+    for (const void *p : ps)
+        if (p && !aligned16(p)) return false;
+    return true;
+}
+
+uint32_t *flag_of(void *ws) { return reinterpret_cast<uint32_t *>(ws); }
+float *partials_of(void *ws) { return reinterpret_cast<float *>(reinterpret_cast<char *>(ws) + kWsHeader); }
+
+focus_status hip_status(hipError_t e) { return e == hipSuccess ? FOCUS_OK : FOCUS_ERR_HIP; }
+
+size_t fwd_ws(int64_t M, int64_t N, int64_t K) {
+    return std::max(plan_fwd(kF32, M, N, K).ws_bytes, plan_fwd(kBF16, M, N, K).ws_bytes);
+}
+
+size_t bwd_ws(int fmt, int sb, int64_t M, int64_t N, int64_t K) {
+    size_t m = 0;
+    for (int dt : {kF32, kBF16})
+        for (bool g : {false, true}) m = std::max(m, plan_bwd(dt, fmt, sb, M, N, K, g).ws_bytes);
+    return m;
+}
+
+#define FOCUS_TRY(x)                  \
+    do {                              \
+        focus_status s_ = (x);        \
+        if (s_ != FOCUS_OK) return s_; \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+size_t focus_workspace_size(int call, const focus_qconfig *q, int64_t M, int64_t N, int64_t K) {
+    if (check_q(q) != FOCUS_OK) return 0;
+    const int B = block_of(q->format);
+    switch (call) {
+        case FOCUS_CALL_SCALES_INIT:
+        case FOCUS_CALL_FAKEQUANT_FWD:
+            return kWsHeader + kAbsmaxParts * sizeof(float);
+        case FOCUS_CALL_FAKEQUANT_BWD:
+        case FOCUS_CALL_EXPORT_PACKED:
+            return kWsHeader;
+        case FOCUS_CALL_RECON_GEMM_FWD:
+            if (M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return 0;
+            return fwd_ws(M, N, K);
+        case FOCUS_CALL_RECON_GEMM_BWD:
+            if (check_rows_k(N, K, B) != FOCUS_OK || M < 0 || M > kMaxDim) return 0;
+            return bwd_ws(q->format, q->sub_block, M, N, K);
+        default:
+            return 0;
+    }
+}
+
+focus_status focus_scales_init(const focus_qconfig *q, const void *W, int w_dtype, int64_t N, int64_t K,
+                               float *s_fp, float *c, float *alpha_out, void *ws, size_t ws_bytes,
+                               focus_stream stream) {
+    FOCUS_TRY(check_q(q));
+    if (!W || !s_fp || !c) return FOCUS_ERR_NULL;
+    if (q->format == FOCUS_NVFP4 && !alpha_out) return FOCUS_ERR_NULL;
+    if (!dtype_ok(w_dtype)) return FOCUS_ERR_DTYPE;
+    FOCUS_TRY(check_rows_k(N, K, block_of(q->format)));
+    if (!all_aligned({W})) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_SCALES_INIT, q, 0, N, K)));
+    if (N == 0 || K == 0) return FOCUS_OK;
+    return hip_status(launch_scales_init(q->format, w_dtype, W, N, K, s_fp, c, q->sub_block, alpha_out,
+                                         partials_of(ws), (hipStream_t)stream));
+}
+
+focus_status focus_fakequant_fwd(const focus_qconfig *q, const void *X, int x_dtype, int64_t rows, int64_t K,
+                                 const float *s_fp, const float *c, const float *alpha, void *X_hat,
+                                 int xhat_dtype, uint8_t *codes_opt, uint8_t *scale_bytes_opt,
+                                 float *alpha_out_opt, void *ws, size_t ws_bytes, focus_stream stream) {
+    FOCUS_TRY(check_q(q));
+    if (!X || !X_hat) return FOCUS_ERR_NULL;
+    const bool weight_mode = s_fp != nullptr;
+    if (weight_mode && q->format == FOCUS_NVFP4 && !alpha) return FOCUS_ERR_NULL;
+    if (!weight_mode && (c || alpha)) return FOCUS_ERR_CONFIG;
+    if (!dtype_ok(x_dtype) || !dtype_ok(xhat_dtype)) return FOCUS_ERR_DTYPE;
+    FOCUS_TRY(check_rows_k(rows, K, block_of(q->format)));
+    if (!all_aligned({X, X_hat, codes_opt})) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_FAKEQUANT_FWD, q, 0, rows, K)));
+    if (rows == 0 || K == 0) return FOCUS_OK;
+    hipStream_t st = (hipStream_t)stream;
+    if (weight_mode)
+        return hip_status(launch_fq_weight(q->format, x_dtype, xhat_dtype, X, rows, K, s_fp, c, q->sub_block,
+                                           alpha, X_hat, codes_opt, scale_bytes_opt, flag_of(ws), st));
+    return hip_status(launch_fq_act(q->format, x_dtype, xhat_dtype, X, rows, K, X_hat, codes_opt,
+                                    scale_bytes_opt, alpha_out_opt, partials_of(ws), flag_of(ws), st));
+}
+
+focus_status focus_fakequant_bwd(const focus_qconfig *q, const float *G, int64_t N, int64_t K, const void *W,
+                                 int w_dtype, const float *s_fp, const float *c, const float *alpha,
+                                 float *grad_s, float *grad_c, void *ws, size_t ws_bytes, focus_stream stream) {
+    FOCUS_TRY(check_q(q));
+    if (!G || !W || !s_fp || !grad_s || !grad_c) return FOCUS_ERR_NULL;
+    if (q->format == FOCUS_NVFP4 && !alpha) return FOCUS_ERR_NULL;
+    if (!dtype_ok(w_dtype)) return FOCUS_ERR_DTYPE;
+    FOCUS_TRY(check_rows_k(N, K, block_of(q->format)));
+    if (!all_aligned({G, W})) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_FAKEQUANT_BWD, q, 0, N, K)));
+    if (N == 0 || K == 0) return FOCUS_OK;
+    return hip_status(launch_fq_bwd(q->format, w_dtype, G, N, K, W, s_fp, c, q->sub_block, alpha, q->ste_clip,
+                                    grad_s, grad_c, flag_of(ws), (hipStream_t)stream));
+}
+
+focus_status focus_recon_gemm_fwd(const void *X_hat, const void *W_hat, int op_dtype, int64_t M, int64_t N,
+                                  int64_t K, const void *Y_ref, void *dY, double *loss_out, double *col_sq_opt,
+                                  void *ws, size_t ws_bytes, focus_stream stream) {
+    if (!X_hat || !W_hat || !dY) return FOCUS_ERR_NULL;
+    if (Y_ref && !loss_out) return FOCUS_ERR_NULL;
+    if (!dtype_ok(op_dtype)) return FOCUS_ERR_DTYPE;
+    if (M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return FOCUS_ERR_SHAPE;
+    if (K % 16 != 0) return FOCUS_ERR_SHAPE;
+    if ((M > 0 && K > kMaxElems / M) || (N > 0 && K > kMaxElems / N) || (M > 0 && N > kMaxElems / M))
+        return FOCUS_ERR_SHAPE;
+    if (!all_aligned({X_hat, W_hat, Y_ref, dY})) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, fwd_ws(M, N, K)));
+    if (M == 0 || N == 0) return FOCUS_OK;
+    const FwdPlan p = plan_fwd(op_dtype, M, N, K);
+    return hip_status(launch_recon_fwd(p, op_dtype, X_hat, W_hat, M, N, K, Y_ref, dY, loss_out, col_sq_opt, ws,
+                                       (hipStream_t)stream));
+}
+
+focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const void *X_hat, int op_dtype,
+                                  int64_t M, int64_t N, int64_t K, const void *W, int w_dtype,
+                                  const float *s_fp, const float *c, const float *alpha, float *grad_s,
+                                  float *grad_c, float *G_out_opt, void *ws, size_t ws_bytes,
+                                  focus_stream stream) {
+    FOCUS_TRY(check_q(q));
+    if (!dY || !X_hat || !W || !s_fp || !grad_s || !grad_c) return FOCUS_ERR_NULL;
+    if (q->format == FOCUS_NVFP4 && !alpha) return FOCUS_ERR_NULL;
+    if (!dtype_ok(op_dtype) || !dtype_ok(w_dtype)) return FOCUS_ERR_DTYPE;
+    FOCUS_TRY(check_rows_k(N, K, block_of(q->format)));
+    if (M < 0 || M > kMaxDim || (M > 0 && K > kMaxElems / M) || (M > 0 && N > kMaxElems / M))
+        return FOCUS_ERR_SHAPE;
+    if (!all_aligned({dY, X_hat, W, G_out_opt})) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, bwd_ws(q->format, q->sub_block, M, N, K)));
+    if (N == 0 || K == 0) return FOCUS_OK;
+    const BwdPlan p = plan_bwd(op_dtype, q->format, q->sub_block, M, N, K, G_out_opt != nullptr);
+    return hip_status(launch_recon_bwd(p, op_dtype, q->format, q->sub_block, q->ste_clip, dY, X_hat, M, N, K, W,
+                                       w_dtype, s_fp, c, alpha, grad_s, grad_c, G_out_opt, ws, flag_of(ws),
+                                       (hipStream_t)stream));
+}
+
+focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dtype, int64_t N, int64_t K,
+                                 const float *s_fp, const float *c, const float *alpha, uint8_t *packed,
+                                 uint8_t *scale_bytes, void *ws, size_t ws_bytes, focus_stream stream) {
+    FOCUS_TRY(check_q(q));
+    if (!W || !s_fp || !packed || !scale_bytes) return FOCUS_ERR_NULL;
+    if (q->format == FOCUS_NVFP4 && !alpha) return FOCUS_ERR_NULL;
+    if (!dtype_ok(w_dtype)) return FOCUS_ERR_DTYPE;
+    FOCUS_TRY(check_rows_k(N, K, block_of(q->format)));
+    if (!all_aligned({W, packed})) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_EXPORT_PACKED, q, 0, N, K)));
+    if (N == 0 || K == 0) return FOCUS_OK;
+    return hip_status(launch_fq_weight(q->format, w_dtype, w_dtype, W, N, K, s_fp, c, q->sub_block, alpha,
+                                       nullptr, packed, scale_bytes, flag_of(ws), (hipStream_t)stream));
+}
+
+focus_status focus_check_flags(void *ws, focus_stream stream) {
+    if (!ws) return FOCUS_ERR_WORKSPACE;
+    if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return FOCUS_ERR_HIP;
+    uint32_t flag = 0;
+    if (hipMemcpy(&flag, ws, sizeof(flag), hipMemcpyDeviceToHost) != hipSuccess) return FOCUS_ERR_HIP;
+    if (flag) {
+        const uint32_t zero = 0;
+        if (hipMemcpy(ws, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return FOCUS_ERR_HIP;
+        return FOCUS_ERR_DOMAIN;
+    }
+    return FOCUS_OK;
+}
+
+const char *focus_status_string(int status) {
+    switch (status) {
+        case FOCUS_OK: return "ok";
+        case FOCUS_ERR_NULL: return "a required pointer is NULL";
+        case FOCUS_ERR_SHAPE: return "invalid sizes (negative, too large, or K not a multiple of the block size)";
+        case FOCUS_ERR_DTYPE: return "unknown or unsupported dtype";
+        case FOCUS_ERR_CONFIG: return "invalid quantisation configuration or argument combination";
+        case FOCUS_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+        case FOCUS_ERR_DOMAIN: return "a kernel met a NaN scale or a coefficient c <= 0 or not finite";
+        case FOCUS_ERR_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+}  // extern "C"

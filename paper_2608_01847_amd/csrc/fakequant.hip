@@ -1,0 +1,385 @@
+// Streaming fake-quantisation kernels of the FOCUS step for gfx950 (HBM-bound).
+//
+// Work unit: a "chunk" of 8 consecutive elements along K, one per thread per loop trip (one
+// 16-byte bf16 or 32-byte fp32 vector load). K is a multiple of the block size (16 or 32), so a
+// block is 2 or 4 adjacent lanes and its absmax / gradient sums are formed with quad shuffles,
+// never with atomics. Grids are capped and grid-stride; every lane of a block runs the same trips.
+#include "focus_device.h"
+#include "internal.h"
+
+namespace focus {
+
+// xor-shuffle within groups of `width` lanes (width <= 4 here); every lane of the group is active
+__device__ __forceinline__ float shfl_xor_f(float v, int mask) { return __shfl_xor(v, mask, 64); }
+
+__device__ __forceinline__ float group_max(float v, int lanes) {
+    if (lanes >= 2) v = fmaxf(v, shfl_xor_f(v, 1));
+    if (lanes >= 4) v = fmaxf(v, shfl_xor_f(v, 2));
+    return v;
+}
+
+__device__ __forceinline__ float group_sum(float v, int lanes) {
+    // fixed pairing order: (l ^ 1) then (l ^ 2); every lane ends with the same bits
+    if (lanes >= 2) v = v + shfl_xor_f(v, 1);
+    if (lanes >= 4) v = v + shfl_xor_f(v, 2);
+    return v;
+}
+
+// ------------------------------------------------------------------------------------------------
+// K1 / K7: weight fake quantisation with learned scales (Eq. 4, 6-8) and export (Fig. 3(d)).
+template <int FMT, int IN, int OUT>
+__global__ void __launch_bounds__(256)
+fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
+                 const float *__restrict__ s_fp, const float *__restrict__ c, int sb_log2,
+                 const float *__restrict__ alpha_ptr, int ste_clip, void *__restrict__ w_hat,
+                 uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes, uint32_t *flag) {
+    constexpr int B = block_of(FMT);
+    const float alpha = FMT == kFmtNV ? *alpha_ptr : 1.0f;
+    const int sb = 1 << sb_log2;
+    const int64_t nb = K / B, ns = K >> sb_log2;
+    bool bad = false;
+    for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
+        const uint32_t r = t / cpr, j = t - r * cpr;
+        const int64_t row = row0 + r, k0 = (int64_t)j * 8;
+        const int64_t e0 = row * K + k0;
+        float v[8];
+        load8(W, IN, e0, v);
+        uint32_t byte;
+        const float sdq = weight_sdq(FMT, s_fp[row * nb + k0 / B], alpha, byte, bad);
+        float cv[4] = {1.0f, 1.0f, 1.0f, 1.0f};
+        const int ncoef = sb >= 8 ? 1 : 8 >> sb_log2;
+        if (c) {
+            for (int i = 0; i < ncoef; i++) {
+                cv[i] = c[row * ns + (k0 >> sb_log2) + i];
+                bad |= bad_coeff(cv[i]);
+            }
+        }
+        float out[8];
+        uint32_t packed = 0;
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            const float ci = sb >= 8 ? cv[0] : cv[i >> sb_log2];
+            const float sq = sdq * ci;
+            Quantized z = quantize_element(v[i], sq, sdq, true);
+            out[i] = z.xhat;
+            packed |= z.code << (4 * i);
+        }
+        if (w_hat) store8(w_hat, OUT, e0, out);
+        if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+        if (scale_bytes && (k0 % B) == 0) scale_bytes[row * nb + k0 / B] = (uint8_t)byte;
+    }
+    if (bad) raise_domain_flag(flag);
+    (void)ste_clip;
+}
+
+// ------------------------------------------------------------------------------------------------
+// K2 (MXFP4): dynamic activation fake quantisation, one pass. Block of 32 = 4 lanes.
+// S = 2^e with e = E8M0_up(fl32(amax / 6)); u = x / S is computed as x * 2^-e, which is the same
+// correctly rounded value because 2^-e is exact for every e in [-127, 127].
+template <int IN, int OUT>
+__global__ void __launch_bounds__(256)
+fq_act_mx_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
+                 void *__restrict__ x_hat, uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes,
+                 uint32_t *flag) {
+    const int64_t nb = K / 32;
+    bool bad = false;
+    for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
+        const uint32_t r = t / cpr, j = t - r * cpr;
+        const int64_t row = row0 + r, k0 = (int64_t)j * 8;
+        const int64_t e0 = row * K + k0;
+        float v[8];
+        load8(X, IN, e0, v);
+        float amax = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; i++) amax = fmaxf(amax, __builtin_fabsf(v[i]));
+        amax = group_max(amax, 4);
+        const int e = e8m0_ceil_exp(amax / 6.0f, bad);
+        const float S = exp2i(e), inv = exp2i(-e);
+        float out[8];
+        uint32_t packed = 0;
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            const uint32_t sign = __float_as_uint(v[i]) & 0x80000000u;
+            const uint32_t idx = e2m1_index(__builtin_fabsf(v[i] * inv));
+            const float q = __uint_as_float(e2m1_magnitude_bits(idx) | sign);
+            out[i] = q * S;
+            packed |= ((sign >> 28) | idx) << (4 * i);
+        }
+        if (x_hat) store8(x_hat, OUT, e0, out);
+        if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+        if (scale_bytes && (k0 % 32) == 0) scale_bytes[row * nb + k0 / 32] = (uint8_t)(e + 127);
+    }
+    if (bad) raise_domain_flag(flag);
+}
+
+// ------------------------------------------------------------------------------------------------
+// Absmax of a whole tensor, pass 1: one partial maximum per workgroup (max is order-free, so the
+// result is exact and deterministic).
+template <int IN>
+__global__ void __launch_bounds__(256)
+absmax_partial_kernel(const void *__restrict__ X, uint64_t nchunks, float *__restrict__ partial) {
+    float m = 0.0f;
+    for (uint64_t t = (uint64_t)blockIdx.x * 256u + threadIdx.x; t < nchunks; t += (uint64_t)gridDim.x * 256u) {
+        float v[8];
+        load8(X, IN, (int64_t)t * 8, v);
+#pragma unroll
+        for (int i = 0; i < 8; i++) m = fmaxf(m, __builtin_fabsf(v[i]));
+    }
+    __shared__ float red[256];
+    red[threadIdx.x] = m;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + s]);
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partial[blockIdx.x] = red[0];
+}
+
+// pass 2 helper: every workgroup folds the partials into the tensor scale
+// alpha = fl32(max|X| / (6 * 448)) (Eq. 2), or 1 for an all-zero tensor
+__device__ float tensor_alpha_from_partials(const float *__restrict__ partial, int npart) {
+    __shared__ float red[256];
+    float m = 0.0f;
+    for (int i = threadIdx.x; i < npart; i += 256) m = fmaxf(m, partial[i]);
+    red[threadIdx.x] = m;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + s]);
+        __syncthreads();
+    }
+    const float A = red[0];
+    return A > 0.0f ? A / 2688.0f : 1.0f;
+}
+
+// K2 (NVFP4) pass 2: block of 16 = 2 lanes; Delta = Q_E4M3(fl32(amax / fl32(alpha * 6))),
+// S = fl32(alpha * Delta), u = fl32(x / S) (a true division: S is not a power of two).
+template <int IN, int OUT>
+__global__ void __launch_bounds__(256)
+fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
+                 const float *__restrict__ partial, int npart, void *__restrict__ x_hat,
+                 uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes,
+                 float *__restrict__ alpha_out, uint32_t *flag) {
+    const float alpha = tensor_alpha_from_partials(partial, npart);
+    if (alpha_out && blockIdx.x == 0 && threadIdx.x == 0) *alpha_out = alpha;
+    const float alpha6 = alpha * 6.0f;
+    const int64_t nb = K / 16;
+    bool bad = false;
+    for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
+        const uint32_t r = t / cpr, j = t - r * cpr;
+        const int64_t row = row0 + r, k0 = (int64_t)j * 8;
+        const int64_t e0 = row * K + k0;
+        float v[8];
+        load8(X, IN, e0, v);
+        float amax = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; i++) amax = fmaxf(amax, __builtin_fabsf(v[i]));
+        amax = group_max(amax, 2);
+        const uint32_t byte = e4m3_code(amax / alpha6, bad);
+        const float S = alpha * e4m3_value(byte);
+        float out[8];
+        uint32_t packed = 0;
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            Quantized z = quantize_element(v[i], S, S, true);
+            out[i] = z.xhat;
+            packed |= z.code << (4 * i);
+        }
+        if (x_hat) store8(x_hat, OUT, e0, out);
+        if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+        if (scale_bytes && (k0 % 16) == 0) scale_bytes[row * nb + k0 / 16] = (uint8_t)byte;
+    }
+    if (bad) raise_domain_flag(flag);
+}
+
+// ------------------------------------------------------------------------------------------------
+// K8: absmax initialisation (Sec. 3.2). MXFP4: s = fl32(amax / 6). NVFP4: Delta_fp =
+// fl32(amax / fl32(alpha * 6)) with alpha from the partial maxima; c = 1.
+template <int FMT, int IN>
+__global__ void __launch_bounds__(256)
+scales_init_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
+                   const float *__restrict__ partial, int npart, float *__restrict__ s_fp,
+                   float *__restrict__ c, int sb_log2, float *__restrict__ alpha_out) {
+    constexpr int B = block_of(FMT);
+    float alpha = 1.0f;
+    if (FMT == kFmtNV) {
+        alpha = tensor_alpha_from_partials(partial, npart);
+        if (alpha_out && blockIdx.x == 0 && threadIdx.x == 0) *alpha_out = alpha;
+    } else if (alpha_out && blockIdx.x == 0 && threadIdx.x == 0) {
+        *alpha_out = 1.0f;
+    }
+    const int sb = 1 << sb_log2;
+    const int64_t nb = K / B, ns = K >> sb_log2;
+    for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
+        const uint32_t r = t / cpr, j = t - r * cpr;
+        const int64_t row = row0 + r, k0 = (int64_t)j * 8;
+        float v[8];
+        load8(W, IN, row * K + k0, v);
+        float amax = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; i++) amax = fmaxf(amax, __builtin_fabsf(v[i]));
+        amax = group_max(amax, B / 8);
+        if ((k0 % B) == 0) s_fp[row * nb + k0 / B] = FMT == kFmtMX ? amax / 6.0f : amax / (alpha * 6.0f);
+        if (sb >= 8) {
+            if ((k0 % sb) == 0) c[row * ns + (k0 >> sb_log2)] = 1.0f;
+        } else {
+            for (int i = 0; i < (8 >> sb_log2); i++) c[row * ns + (k0 >> sb_log2) + i] = 1.0f;
+        }
+    }
+}
+
+// ------------------------------------------------------------------------------------------------
+// K3: straight-through backward from a given G = dL/dW_hat (fp32).
+//   grad_c = -(1/c^2) sum_sub G m w ;  grad_s = f * sum_block G (q - m u)
+template <int FMT, int WDT>
+__global__ void __launch_bounds__(256)
+fq_bwd_kernel(const float *__restrict__ G, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
+              const void *__restrict__ W, const float *__restrict__ s_fp, const float *__restrict__ c,
+              int sb_log2, const float *__restrict__ alpha_ptr, int ste_clip,
+              float *__restrict__ grad_s, float *__restrict__ grad_c, uint32_t *flag) {
+    constexpr int B = block_of(FMT);
+    const float alpha = FMT == kFmtNV ? *alpha_ptr : 1.0f;
+    const int sb = 1 << sb_log2;
+    const int64_t nb = K / B, ns = K >> sb_log2;
+    bool bad = false;
+    for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
+        const uint32_t r = t / cpr, j = t - r * cpr;
+        const int64_t row = row0 + r, k0 = (int64_t)j * 8;
+        const int64_t e0 = row * K + k0;
+        float w[8], g[8];
+        load8(W, WDT, e0, w);
+        load8(G, kF32, e0, g);
+        uint32_t byte;
+        const float sdq = weight_sdq(FMT, s_fp[row * nb + k0 / B], alpha, byte, bad);
+        float cv[4] = {1.0f, 1.0f, 1.0f, 1.0f};
+        const int ncoef = sb >= 8 ? 1 : 8 >> sb_log2;
+        if (c) {
+            for (int i = 0; i < ncoef; i++) {
+                cv[i] = c[row * ns + (k0 >> sb_log2) + i];
+                bad |= bad_coeff(cv[i]);
+            }
+        }
+        float tc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        float ts = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            const int ci = sb >= 8 ? 0 : (i >> sb_log2);
+            const float sq = sdq * cv[ci];
+            Quantized z = quantize_element(w[i], sq, sdq, ste_clip != 0);
+            const float mw = z.m ? w[i] : 0.0f;
+            const float mu = z.m ? z.u : 0.0f;
+            tc[ci] += g[i] * mw;
+            ts += g[i] * (z.q - mu);
+        }
+        if (sb >= 8) {
+            const float s = group_sum(tc[0], sb / 8);
+            if ((k0 % sb) == 0) grad_c[row * ns + (k0 >> sb_log2)] = -s / (cv[0] * cv[0]);
+        } else {
+            for (int i = 0; i < ncoef; i++)
+                grad_c[row * ns + (k0 >> sb_log2) + i] = -tc[i] / (cv[i] * cv[i]);
+        }
+        const float s = group_sum(ts, B / 8);
+        if ((k0 % B) == 0) grad_s[row * nb + k0 / B] = FMT == kFmtNV ? s * alpha : s;
+    }
+    if (bad) raise_domain_flag(flag);
+}
+
+// ================================================================================================
+// Host launchers
+// ================================================================================================
+
+// The chunk index of one launch stays below 2^31; longer tensors are launched in row ranges.
+template <typename F>
+static hipError_t for_row_ranges(int64_t rows, int64_t K, F &&launch) {
+    const int64_t cpr = K / 8;
+    const int64_t max_rows = std::max<int64_t>(1, (int64_t(1) << 30) / cpr);
+    for (int64_t r0 = 0; r0 < rows; r0 += max_rows) {
+        const int64_t nr = std::min(max_rows, rows - r0);
+        const uint32_t nchunks = (uint32_t)(nr * cpr);
+        const uint32_t grid = (uint32_t)std::min<int64_t>((nchunks + 255) / 256, kStreamGridCap);
+        launch(r0, nchunks, (uint32_t)cpr, grid);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+static int log2i(int v) {
+    int l = 0;
+    while ((1 << l) < v) l++;
+    return l;
+}
+
+hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64_t rows, int64_t K,
+                            const float *s_fp, const float *c, int sb, const float *alpha, void *w_hat,
+                            uint8_t *codes, uint8_t *scale_bytes, uint32_t *flag, hipStream_t st) {
+    const int sbl = log2i(sb);
+    return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
+#define FQW(F, I, O) fq_weight_kernel<F, I, O><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, s_fp, c, sbl, alpha, 1, w_hat, codes, scale_bytes, flag)
+        if (fmt == kFmtMX) {
+            if (in_dt == kBF16) { if (out_dt == kBF16) FQW(kFmtMX, kBF16, kBF16); else FQW(kFmtMX, kBF16, kF32); }
+            else { if (out_dt == kBF16) FQW(kFmtMX, kF32, kBF16); else FQW(kFmtMX, kF32, kF32); }
+        } else {
+            if (in_dt == kBF16) { if (out_dt == kBF16) FQW(kFmtNV, kBF16, kBF16); else FQW(kFmtNV, kBF16, kF32); }
+            else { if (out_dt == kBF16) FQW(kFmtNV, kF32, kBF16); else FQW(kFmtNV, kF32, kF32); }
+        }
+#undef FQW
+    });
+}
+
+static hipError_t launch_absmax(int in_dt, const void *X, int64_t n, float *partial, hipStream_t st) {
+    const uint64_t nchunks = (uint64_t)n / 8;
+    if (in_dt == kBF16) absmax_partial_kernel<kBF16><<<kAbsmaxParts, 256, 0, st>>>(X, nchunks, partial);
+    else absmax_partial_kernel<kF32><<<kAbsmaxParts, 256, 0, st>>>(X, nchunks, partial);
+    return hipGetLastError();
+}
+
+hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t rows, int64_t K,
+                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, float *alpha_out,
+                         float *partial, uint32_t *flag, hipStream_t st) {
+    if (fmt == kFmtMX) {
+        return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
+#define FQA(I, O) fq_act_mx_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, x_hat, codes, scale_bytes, flag)
+            if (in_dt == kBF16) { if (out_dt == kBF16) FQA(kBF16, kBF16); else FQA(kBF16, kF32); }
+            else { if (out_dt == kBF16) FQA(kF32, kBF16); else FQA(kF32, kF32); }
+#undef FQA
+        });
+    }
+    hipError_t e = launch_absmax(in_dt, X, rows * K, partial, st);
+    if (e != hipSuccess) return e;
+    return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
+#define FQN(I, O) fq_act_nv_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, partial, kAbsmaxParts, x_hat, codes, scale_bytes, r0 == 0 ? alpha_out : nullptr, flag)
+        if (in_dt == kBF16) { if (out_dt == kBF16) FQN(kBF16, kBF16); else FQN(kBF16, kF32); }
+        else { if (out_dt == kBF16) FQN(kF32, kBF16); else FQN(kF32, kF32); }
+#undef FQN
+    });
+}
+
+hipError_t launch_scales_init(int fmt, int in_dt, const void *W, int64_t rows, int64_t K, float *s_fp,
+                              float *c, int sb, float *alpha_out, float *partial, hipStream_t st) {
+    const int sbl = log2i(sb);
+    if (fmt == kFmtNV) {
+        hipError_t e = launch_absmax(in_dt, W, rows * K, partial, st);
+        if (e != hipSuccess) return e;
+    }
+    return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
+        float *ao = r0 == 0 ? alpha_out : nullptr;
+#define SI(F, I) scales_init_kernel<F, I><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, partial, kAbsmaxParts, s_fp, c, sbl, ao)
+        if (fmt == kFmtMX) { if (in_dt == kBF16) SI(kFmtMX, kBF16); else SI(kFmtMX, kF32); }
+        else { if (in_dt == kBF16) SI(kFmtNV, kBF16); else SI(kFmtNV, kF32); }
+#undef SI
+    });
+}
+
+hipError_t launch_fq_bwd(int fmt, int w_dt, const float *G, int64_t rows, int64_t K, const void *W,
+                         const float *s_fp, const float *c, int sb, const float *alpha, int ste_clip,
+                         float *grad_s, float *grad_c, uint32_t *flag, hipStream_t st) {
+    const int sbl = log2i(sb);
+    return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
+#define FQB(F, WD) fq_bwd_kernel<F, WD><<<grid, 256, 0, st>>>(G, n, cpr, r0, K, W, s_fp, c, sbl, alpha, ste_clip, grad_s, grad_c, flag)
+        if (fmt == kFmtMX) { if (w_dt == kBF16) FQB(kFmtMX, kBF16); else FQB(kFmtMX, kF32); }
+        else { if (w_dt == kBF16) FQB(kFmtNV, kBF16); else FQB(kFmtNV, kF32); }
+#undef FQB
+    });
+}
+
+}  // namespace focus

@@ -1,0 +1,182 @@
+// Device-side FP4 / scale codecs and small helpers shared by the FOCUS kernels (gfx950).
+//
+// The element format is E2M1 (Sec. 3.1, Eq. 1): magnitudes {0, .5, 1, 1.5, 2, 3, 4, 6}; a code is
+// sign << 3 | magnitude index. Scales are E8M0 (MXFP4, Eq. 3, rounded up to a power of two) or
+// OCP E4M3FN (NVFP4, Eq. 2). All decisions are taken on fp32 values produced by single, correctly
+// rounded fp32 operations; the library is built with -ffp-contract=off so none is fused.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace focus {
+
+constexpr int kFmtMX = 0;
+constexpr int kFmtNV = 1;
+constexpr int kF32 = 0;
+constexpr int kBF16 = 1;
+
+__host__ __device__ constexpr int block_of(int fmt) { return fmt == kFmtMX ? 32 : 16; }
+
+// ---- E2M1 --------------------------------------------------------------------------------------
+// Nearest magnitude index of a = |u| with ties to the even index and saturation at 6: the grid's
+// midpoints are 0.25, 0.75, 1.25, 1.75, 2.5, 3.5 and 5; a midpoint goes to the even neighbour, so
+// the comparison is strict where the lower neighbour has an even index and inclusive otherwise.
+// A NaN compares false everywhere and maps to index 0.
+__device__ __forceinline__ uint32_t e2m1_index(float a) {
+    return (uint32_t)(a > 0.25f) + (uint32_t)(a >= 0.75f) + (uint32_t)(a > 1.25f) +
+           (uint32_t)(a >= 1.75f) + (uint32_t)(a > 2.5f) + (uint32_t)(a >= 3.5f) +
+           (uint32_t)(a > 5.0f);
+}
+
+// fp32 bit pattern of the magnitude with index idx: for idx >= 2 it is (1 + (idx & 1) / 2) *
+// 2^((idx >> 1) - 1); index 1 is 0.5 and index 0 is 0.
+__device__ __forceinline__ uint32_t e2m1_magnitude_bits(uint32_t idx) {
+    uint32_t hi = (((idx >> 1) + 126u) << 23) | ((idx & 1u) << 22);
+    return idx >= 2u ? hi : (idx ? 0x3F000000u : 0u);
+}
+
+// ---- E8M0 (scale rounded up to a power of two) ---------------------------------------------------
+// Smallest e in [-127, 127] with 2^e >= s. Non-positive s (and -0) -> -127; +inf -> 127;
+// NaN sets *nan_seen and gives -127.
+__device__ __forceinline__ int e8m0_ceil_exp(float s, bool &nan_seen) {
+    uint32_t b = __float_as_uint(s);
+    if ((b & 0x7FFFFFFFu) > 0x7F800000u) {
+        nan_seen = true;
+        return -127;
+    }
+    if ((int32_t)b <= 0) return -127;
+    uint32_t E = b >> 23, man = b & 0x7FFFFFu;
+    if (E == 0u) return man > 0x400000u ? -126 : -127;  // subnormal s < 2^-126; 2^-127 is man 0x400000
+    int e = (int)E - 127 + (man != 0u);
+    return e > 127 ? 127 : e;
+}
+
+// 2^e as fp32 for e in [-127, 127]; 2^-127 is the subnormal 0x00400000.
+__device__ __forceinline__ float exp2i(int e) {
+    return e >= -126 ? __uint_as_float((uint32_t)(e + 127) << 23) : __uint_as_float(0x00400000u);
+}
+
+// ---- E4M3 (OCP E4M3FN: bias 7, max 448, subnormals m * 2^-9, no infinities) -----------------------
+// Round to nearest, ties to even, saturating at 448; x <= 0 -> 0; NaN sets *nan_seen.
+__device__ __forceinline__ uint32_t e4m3_code(float x, bool &nan_seen) {
+    uint32_t b = __float_as_uint(x);
+    if ((b & 0x7FFFFFFFu) > 0x7F800000u) {
+        nan_seen = true;
+        return 0u;
+    }
+    if ((int32_t)b <= 0) return 0u;
+    if (x >= 448.0f) return 0x7Eu;
+    if (x >= 0.015625f) {  // normal E4M3 range: keep 3 mantissa bits with round-half-even
+        uint32_t r = b + 0x7FFFFu + ((b >> 20) & 1u);
+        uint32_t code = (((r >> 23) - 120u) << 3) | ((r >> 20) & 7u);
+        return code > 0x7Eu ? 0x7Eu : code;
+    }
+    // subnormal range: the nearest multiple of 2^-9, ties to even (x * 512 is exact)
+    return (uint32_t)__builtin_rintf(x * 512.0f);
+}
+
+__device__ __forceinline__ float e4m3_value(uint32_t code) {
+    uint32_t E = code >> 3, M = code & 7u;
+    return E == 0u ? (float)M * 0.001953125f : __uint_as_float(((E + 120u) << 23) | (M << 20));
+}
+
+// ---- bf16 ---------------------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// round to nearest even (NaN kept quiet)
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    uint32_t b = __float_as_uint(f);
+    if ((b & 0x7FFFFFFFu) > 0x7F800000u) return (b >> 16) | 0x40u;
+    return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+}
+
+// ---- 8-element vector I/O ---------------------------------------------------------------------
+// Loads 8 consecutive values of a bf16 or fp32 row as fp32 (16- or 32-byte vector loads).
+__device__ __forceinline__ void load8(const void *base, int dtype, int64_t idx, float v[8]) {
+    if (dtype == kBF16) {
+        uint4 p = *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(base) + idx);
+        uint32_t w[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            v[2 * i] = __uint_as_float(w[i] << 16);
+            v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+        }
+    } else {
+        const float4 *p = reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(base) + idx);
+        float4 a = p[0], b = p[1];
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    }
+}
+
+__device__ __forceinline__ void store8(void *base, int dtype, int64_t idx, const float v[8]) {
+    if (dtype == kBF16) {
+        uint4 p;
+        p.x = f32_to_bf16_bits(v[0]) | (f32_to_bf16_bits(v[1]) << 16);
+        p.y = f32_to_bf16_bits(v[2]) | (f32_to_bf16_bits(v[3]) << 16);
+        p.z = f32_to_bf16_bits(v[4]) | (f32_to_bf16_bits(v[5]) << 16);
+        p.w = f32_to_bf16_bits(v[6]) | (f32_to_bf16_bits(v[7]) << 16);
+        *reinterpret_cast<uint4 *>(reinterpret_cast<uint16_t *>(base) + idx) = p;
+    } else {
+        float4 *p = reinterpret_cast<float4 *>(reinterpret_cast<float *>(base) + idx);
+        p[0] = make_float4(v[0], v[1], v[2], v[3]);
+        p[1] = make_float4(v[4], v[5], v[6], v[7]);
+    }
+}
+
+// ---- the per-element quantiser shared by every weight / activation kernel ----------------------
+// Quantises x with the quantisation scale sq and dequantisation scale sdq (Eq. 7 / Eq. 8):
+// u = fl32(x / sq), q = Q_E2M1(u), x_hat = fl32(q * sdq). Returns the 4-bit code; writes x_hat and
+// (for the backward) u and the straight-through mask. A zero scale gives a signed zero, u = 0, m = 0.
+struct Quantized {
+    float xhat;
+    float u;
+    float q;       // signed E2M1 value
+    uint32_t code;
+    bool m;
+};
+
+__device__ __forceinline__ Quantized quantize_element(float x, float sq, float sdq, bool ste_clip) {
+    Quantized r;
+    uint32_t sign = __float_as_uint(x) & 0x80000000u;
+    if (sdq == 0.0f || sq == 0.0f) {
+        r.u = 0.0f;
+        r.q = __uint_as_float(sign);
+        r.code = sign >> 28;
+        r.m = false;
+    } else {
+        float u = x / sq;
+        float a = __builtin_fabsf(u);
+        uint32_t idx = e2m1_index(a);
+        r.u = u;
+        r.q = __uint_as_float(e2m1_magnitude_bits(idx) | sign);
+        r.code = (sign >> 28) | idx;
+        r.m = ste_clip ? (a <= 6.0f) : true;
+    }
+    r.xhat = r.q * sdq;
+    return r;
+}
+
+// Dequantisation scale of one weight block from its learnable copy (Eq. 4): MXFP4 2^E8M0_up(s),
+// NVFP4 fl32(alpha * Q_E4M3(s)). Also returns the exported scale byte.
+__device__ __forceinline__ float weight_sdq(int fmt, float s, float alpha, uint32_t &byte, bool &nan_seen) {
+    if (fmt == kFmtMX) {
+        int e = e8m0_ceil_exp(s, nan_seen);
+        byte = (uint32_t)(e + 127);
+        return exp2i(e);
+    }
+    byte = e4m3_code(s, nan_seen);
+    return alpha * e4m3_value(byte);
+}
+
+// a coefficient outside the domain (c <= 0, NaN or inf)
+__device__ __forceinline__ bool bad_coeff(float c) {
+    return !(c > 0.0f) || __float_as_uint(c) == 0x7F800000u;
+}
+
+// Sticky flag in the first word of the workspace. Plain stores of the same value from many lanes
+// are benign; nothing on the hot path writes it unless an input is outside the domain.
+__device__ __forceinline__ void raise_domain_flag(uint32_t *flag) { *reinterpret_cast<volatile uint32_t *>(flag) = 1u; }
+
+}  // namespace focus

@@ -1,0 +1,54 @@
+// Launchers shared between the translation units of libfocus (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+namespace focus {
+
+constexpr int kStreamGridCap = 4096;  // workgroups of a grid-stride streaming kernel
+constexpr int kAbsmaxParts = 1024;    // partial maxima of the tensor-absmax pass
+constexpr size_t kWsHeader = 256;     // workspace bytes reserved for the domain flag
+
+hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64_t rows, int64_t K,
+                            const float *s_fp, const float *c, int sb, const float *alpha, void *w_hat,
+                            uint8_t *codes, uint8_t *scale_bytes, uint32_t *flag, hipStream_t st);
+hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t rows, int64_t K,
+                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, float *alpha_out,
+                         float *partial, uint32_t *flag, hipStream_t st);
+hipError_t launch_scales_init(int fmt, int in_dt, const void *W, int64_t rows, int64_t K, float *s_fp,
+                              float *c, int sb, float *alpha_out, float *partial, hipStream_t st);
+hipError_t launch_fq_bwd(int fmt, int w_dt, const float *G, int64_t rows, int64_t K, const void *W,
+                         const float *s_fp, const float *c, int sb, const float *alpha, int ste_clip,
+                         float *grad_s, float *grad_c, uint32_t *flag, hipStream_t st);
+
+// ---- reconstruction GEMMs ----------------------------------------------------------------------
+// Geometry of a forward launch: output tiles of tm x tn; column partial sums [mtiles][N] (double).
+struct FwdPlan {
+    int path;       // 0 = VALU (fp32 / small), 1 = MFMA bf16
+    int64_t mtiles;
+    size_t ws_bytes;
+};
+// Geometry of a backward launch: G tiles of tn x tk, the token range split `splits` ways with
+// `chunk` tokens per split; partial gradient sums [splits][N][K/B] and [splits][N][K/sb] (float).
+struct BwdPlan {
+    int path;
+    int64_t splits;
+    int64_t chunk;
+    size_t ws_bytes;
+};
+
+FwdPlan plan_fwd(int op_dt, int64_t M, int64_t N, int64_t K);
+BwdPlan plan_bwd(int op_dt, int fmt, int sb, int64_t M, int64_t N, int64_t K, bool want_G);
+
+hipError_t launch_recon_fwd(const FwdPlan &p, int op_dt, const void *X, const void *W, int64_t M,
+                            int64_t N, int64_t K, const void *Yref, void *dY, double *loss_out,
+                            double *col_sq_opt, void *ws, hipStream_t st);
+hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int ste_clip, const void *dY,
+                            const void *X, int64_t M, int64_t N, int64_t K, const void *W, int w_dt,
+                            const float *s_fp, const float *c, const float *alpha, float *grad_s,
+                            float *grad_c, float *G_out, void *ws, uint32_t *flag, hipStream_t st);
+
+}  // namespace focus

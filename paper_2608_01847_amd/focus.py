@@ -1,0 +1,229 @@
+"""Thin ctypes binding of libfocus (include/focus.h) for torch tensors.
+
+Argument marshalling only: every computation runs in the library's HIP kernels on the caller's
+current torch stream. PyTorch provides device memory and streams. Importing this module loads
+nothing; the first call opens libfocus.so and raises if it is not built.
+"""
+from __future__ import annotations
+
+import ctypes
+from pathlib import Path
+
+import torch
+
+LIBRARY = Path(__file__).resolve().parent / "libfocus.so"
+
+MXFP4, NVFP4 = 0, 1
+F32, BF16 = 0, 1
+CALL_SCALES_INIT, CALL_FAKEQUANT_FWD, CALL_FAKEQUANT_BWD = 0, 1, 2
+CALL_RECON_GEMM_FWD, CALL_RECON_GEMM_BWD, CALL_EXPORT_PACKED = 3, 4, 5
+
+OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_CONFIG, ERR_WORKSPACE, ERR_DOMAIN, ERR_HIP = range(8)
+
+EXPORTED = ("focus_workspace_size", "focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd",
+            "focus_recon_gemm_fwd", "focus_recon_gemm_bwd", "focus_export_packed", "focus_check_flags",
+            "focus_status_string")
+
+
+class QConfig(ctypes.Structure):
+    _fields_ = [("format", ctypes.c_int32), ("sub_block", ctypes.c_int32),
+                ("ste_clip", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class FocusError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+_LIB = None
+
+
+def lib() -> ctypes.CDLL:
+    """Opens libfocus.so (built by __graft_entry__.build()); raises if it is missing."""
+    global _LIB
+    if _LIB is None:
+        if not LIBRARY.exists():
+            raise RuntimeError(f"{LIBRARY} is not built: run __graft_entry__.build() first")
+        L = ctypes.CDLL(str(LIBRARY))
+        p, i32, i64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
+        q = ctypes.POINTER(QConfig)
+        L.focus_workspace_size.argtypes = [i32, q, i64, i64, i64]
+        L.focus_workspace_size.restype = sz
+        L.focus_scales_init.argtypes = [q, p, i32, i64, i64, p, p, p, p, sz, p]
+        L.focus_fakequant_fwd.argtypes = [q, p, i32, i64, i64, p, p, p, p, i32, p, p, p, p, sz, p]
+        L.focus_fakequant_bwd.argtypes = [q, p, i64, i64, p, i32, p, p, p, p, p, p, sz, p]
+        L.focus_recon_gemm_fwd.argtypes = [p, p, i32, i64, i64, i64, p, p, p, p, p, sz, p]
+        L.focus_recon_gemm_bwd.argtypes = [q, p, p, i32, i64, i64, i64, p, i32, p, p, p, p, p, p, p, sz, p]
+        L.focus_export_packed.argtypes = [q, p, i32, i64, i64, p, p, p, p, p, p, sz, p]
+        L.focus_check_flags.argtypes = [p, p]
+        L.focus_status_string.argtypes = [i32]
+        L.focus_status_string.restype = ctypes.c_char_p
+        for name in ("focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd", "focus_recon_gemm_fwd",
+                     "focus_recon_gemm_bwd", "focus_export_packed", "focus_check_flags"):
+            getattr(L, name).restype = ctypes.c_int
+        _LIB = L
+    return _LIB
+
+
+def status_string(status: int) -> str:
+    return lib().focus_status_string(status).decode()
+
+
+def qconfig(fmt: int, sub_block: int, ste_clip: int = 1) -> QConfig:
+    return QConfig(fmt, sub_block, ste_clip, 0)
+
+
+def block_size(fmt: int) -> int:
+    return 32 if fmt == MXFP4 else 16
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t: torch.Tensor | None):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libfocus must be contiguous")
+    return t.data_ptr()
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _check(status: int, where: str) -> None:
+    if status != OK:
+        raise FocusError(status, where)
+
+
+def workspace_size(call: int, q: QConfig, M: int = 0, N: int = 0, K: int = 0) -> int:
+    return int(lib().focus_workspace_size(call, ctypes.byref(q), M, N, K))
+
+
+def workspace(nbytes: int, device="cuda") -> torch.Tensor:
+    """A zero-filled workspace (torch's device allocations are at least 256-byte aligned)."""
+    ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=device)
+    assert ws.data_ptr() % 256 == 0
+    return ws
+
+
+def _ws(ws: torch.Tensor | None, call: int, q: QConfig, M: int, N: int, K: int, device) -> torch.Tensor:
+    need = workspace_size(call, q, M, N, K)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, device)
+    return ws
+
+
+def scales_init(W: torch.Tensor, fmt: int, sub_block: int, ws=None, out=None):
+    """Absmax initialisation -> (s_fp [N][K/B], c [N][K/sb] = 1, alpha [1])."""
+    N, K = W.shape
+    q = qconfig(fmt, sub_block)
+    if out is None:
+        s_fp = torch.empty(N, K // block_size(fmt), dtype=torch.float32, device=W.device)
+        c = torch.empty(N, K // sub_block, dtype=torch.float32, device=W.device)
+        alpha = torch.ones(1, dtype=torch.float32, device=W.device)
+    else:
+        s_fp, c, alpha = out
+    ws = _ws(ws, CALL_SCALES_INIT, q, 0, N, K, W.device)
+    _check(lib().focus_scales_init(ctypes.byref(q), _ptr(W), _dt(W), N, K, _ptr(s_fp), _ptr(c), _ptr(alpha),
+                                   _ptr(ws), ws.numel(), _stream()), "focus_scales_init")
+    return s_fp, c, alpha
+
+
+def fakequant_fwd(X: torch.Tensor, fmt: int, sub_block: int = 8, s_fp=None, c=None, alpha=None,
+                  out_dtype=None, want_codes: bool = False, want_scale_bytes: bool = False,
+                  want_alpha: bool = False, ste_clip: int = 1, ws=None, out=None):
+    """Fake quantisation forward. Weight mode when s_fp is given, dynamic activation mode otherwise.
+
+    Returns (x_hat, packed_codes or None, scale_bytes or None, alpha_x or None)."""
+    rows, K = X.shape
+    q = qconfig(fmt, sub_block, ste_clip)
+    out_dtype = out_dtype or X.dtype
+    x_hat = out if out is not None else torch.empty(rows, K, dtype=out_dtype, device=X.device)
+    codes = torch.empty(rows, K // 2, dtype=torch.uint8, device=X.device) if want_codes else None
+    sbytes = torch.empty(rows, K // block_size(fmt), dtype=torch.uint8, device=X.device) if want_scale_bytes else None
+    alpha_out = torch.empty(1, dtype=torch.float32, device=X.device) if want_alpha else None
+    ws = _ws(ws, CALL_FAKEQUANT_FWD, q, 0, rows, K, X.device)
+    _check(lib().focus_fakequant_fwd(ctypes.byref(q), _ptr(X), _dt(X), rows, K, _ptr(s_fp), _ptr(c), _ptr(alpha),
+                                     _ptr(x_hat), _dt(x_hat), _ptr(codes), _ptr(sbytes), _ptr(alpha_out),
+                                     _ptr(ws), ws.numel(), _stream()), "focus_fakequant_fwd")
+    return x_hat, codes, sbytes, alpha_out
+
+
+def fakequant_bwd(G: torch.Tensor, W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha=None,
+                  ste_clip: int = 1, ws=None):
+    """Straight-through backward from G = dL/dW_hat (fp32) -> (grad_s, grad_c)."""
+    N, K = W.shape
+    q = qconfig(fmt, sub_block, ste_clip)
+    grad_s = torch.empty(N, K // block_size(fmt), dtype=torch.float32, device=W.device)
+    grad_c = torch.empty(N, K // sub_block, dtype=torch.float32, device=W.device)
+    ws = _ws(ws, CALL_FAKEQUANT_BWD, q, 0, N, K, W.device)
+    _check(lib().focus_fakequant_bwd(ctypes.byref(q), _ptr(G), N, K, _ptr(W), _dt(W), _ptr(s_fp), _ptr(c),
+                                     _ptr(alpha), _ptr(grad_s), _ptr(grad_c), _ptr(ws), ws.numel(), _stream()),
+           "focus_fakequant_bwd")
+    return grad_s, grad_c
+
+
+def recon_gemm_fwd(X_hat: torch.Tensor, W_hat: torch.Tensor, Y_ref=None, want_col_sq: bool = False, ws=None,
+                   out=None, loss=None):
+    """Y_hat = X_hat W_hat^T with the MSE epilogue -> (dY (or Y_hat when Y_ref is None), loss, col_sq)."""
+    M, K = X_hat.shape
+    N = W_hat.shape[0]
+    dY = out if out is not None else torch.empty(M, N, dtype=X_hat.dtype, device=X_hat.device)
+    loss_t = None
+    if Y_ref is not None:
+        loss_t = loss if loss is not None else torch.empty(1, dtype=torch.float64, device=X_hat.device)
+    col_sq = torch.empty(N, dtype=torch.float64, device=X_hat.device) if want_col_sq else None
+    q = qconfig(MXFP4, 8)
+    ws = _ws(ws, CALL_RECON_GEMM_FWD, q, M, N, K, X_hat.device)
+    _check(lib().focus_recon_gemm_fwd(_ptr(X_hat), _ptr(W_hat), _dt(X_hat), M, N, K, _ptr(Y_ref), _ptr(dY),
+                                      _ptr(loss_t), _ptr(col_sq), _ptr(ws), ws.numel(), _stream()),
+           "focus_recon_gemm_fwd")
+    return dY, loss_t, col_sq
+
+
+def recon_gemm_bwd(dY: torch.Tensor, X_hat: torch.Tensor, W: torch.Tensor, fmt: int, sub_block: int, s_fp,
+                   c=None, alpha=None, ste_clip: int = 1, want_G: bool = False, ws=None, out=None):
+    """Fused backward -> (grad_s, grad_c, G or None)."""
+    M, K = X_hat.shape
+    N = W.shape[0]
+    q = qconfig(fmt, sub_block, ste_clip)
+    if out is None:
+        grad_s = torch.empty(N, K // block_size(fmt), dtype=torch.float32, device=W.device)
+        grad_c = torch.empty(N, K // sub_block, dtype=torch.float32, device=W.device)
+    else:
+        grad_s, grad_c = out
+    G = torch.empty(N, K, dtype=torch.float32, device=W.device) if want_G else None
+    ws = _ws(ws, CALL_RECON_GEMM_BWD, q, M, N, K, W.device)
+    _check(lib().focus_recon_gemm_bwd(ctypes.byref(q), _ptr(dY), _ptr(X_hat), _dt(X_hat), M, N, K, _ptr(W),
+                                      _dt(W), _ptr(s_fp), _ptr(c), _ptr(alpha), _ptr(grad_s), _ptr(grad_c),
+                                      _ptr(G), _ptr(ws), ws.numel(), _stream()), "focus_recon_gemm_bwd")
+    return grad_s, grad_c, G
+
+
+def export_packed(W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha=None, ws=None, out=None):
+    """Deployable export -> (packed codes [N][K/2], scale bytes [N][K/B])."""
+    N, K = W.shape
+    q = qconfig(fmt, sub_block)
+    if out is None:
+        packed = torch.empty(N, K // 2, dtype=torch.uint8, device=W.device)
+        sbytes = torch.empty(N, K // block_size(fmt), dtype=torch.uint8, device=W.device)
+    else:
+        packed, sbytes = out
+    ws = _ws(ws, CALL_EXPORT_PACKED, q, 0, N, K, W.device)
+    _check(lib().focus_export_packed(ctypes.byref(q), _ptr(W), _dt(W), N, K, _ptr(s_fp), _ptr(c), _ptr(alpha),
+                                     _ptr(packed), _ptr(sbytes), _ptr(ws), ws.numel(), _stream()),
+           "focus_export_packed")
+    return packed, sbytes
+
+
+def check_flags(ws: torch.Tensor) -> int:
+    """Synchronises the current stream; returns OK or ERR_DOMAIN (and clears the flag)."""
+    return int(lib().focus_check_flags(_ptr(ws), _stream()))

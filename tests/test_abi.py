@@ -1,0 +1,113 @@
+"""The C ABI on the CPU: libfocus loads, exports every function include/focus.h declares, and its
+host-side checks reject bad arguments with the documented status before anything is launched.
+
+No test here launches a kernel: every call carries an argument that a check must refuse, and the
+pointers are never dereferenced. On a machine with a visible GPU the argument-check tests are
+skipped (they belong to the CPU suite).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_01847_amd import focus
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "focus.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    # declarations: a return type at the start of a line, then the function name and "("
+    return sorted(set(re.findall(r"^(?:focus_status|size_t|const char \*)\s*(focus_[a-z_]+)\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not focus.LIBRARY.exists():
+        pytest.skip("libfocus.so is not built")
+    return focus.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert set(names) == set(focus.EXPORTED)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    for s in range(8):
+        assert focus.status_string(s) and focus.status_string(s) != "unknown status"
+    assert focus.status_string(99) == "unknown status"
+
+
+def test_workspace_sizes_host_only(L):
+    q = focus.qconfig(focus.MXFP4, 8)
+    assert focus.workspace_size(focus.CALL_FAKEQUANT_BWD, q) == 256
+    assert focus.workspace_size(focus.CALL_FAKEQUANT_FWD, q) >= 256 + 4 * 1024
+    fwd = focus.workspace_size(focus.CALL_RECON_GEMM_FWD, q, 1000, 300, 256)
+    assert fwd >= 256 + 8 * 300 * (1000 // 256)
+    bwd = focus.workspace_size(focus.CALL_RECON_GEMM_BWD, q, 65536, 1024, 2560)
+    assert bwd >= 256 + 4 * 1024 * (2560 // 32 + 2560 // 8)
+    # invalid configurations size to 0
+    assert focus.workspace_size(focus.CALL_RECON_GEMM_BWD, focus.qconfig(focus.NVFP4, 32), 1, 1, 16) == 0
+    assert focus.workspace_size(focus.CALL_RECON_GEMM_BWD, q, 16, 4, 48) == 0  # K % 32
+    assert focus.workspace_size(99, q) == 0
+
+
+BOGUS = ctypes.c_void_p(1 << 20)  # never dereferenced: every call below fails a host check first
+
+
+@pytest.fixture()
+def cpu_only():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("argument-check tests run in the CPU suite only")
+
+
+def fq_fwd(L, q, K=64, rows=4, x_dt=1, xh_dt=1, X=BOGUS, s_fp=None, c=None, alpha=None, ws=BOGUS, ws_bytes=1 << 20):
+    return L.focus_fakequant_fwd(ctypes.byref(q), X, x_dt, rows, K, s_fp, c, alpha, BOGUS, xh_dt, None, None,
+                                 None, ws, ws_bytes, None)
+
+
+def test_argument_checks(L, cpu_only):
+    mx = focus.qconfig(focus.MXFP4, 8)
+    assert fq_fwd(L, focus.qconfig(2, 8)) == focus.ERR_CONFIG
+    assert fq_fwd(L, focus.qconfig(focus.MXFP4, 3)) == focus.ERR_CONFIG
+    assert fq_fwd(L, focus.qconfig(focus.NVFP4, 32)) == focus.ERR_CONFIG  # sub-block larger than the block
+    assert fq_fwd(L, focus.qconfig(focus.MXFP4, 8, 2)) == focus.ERR_CONFIG
+    assert fq_fwd(L, focus.QConfig(0, 8, 1, 5)) == focus.ERR_CONFIG
+    assert fq_fwd(L, mx, X=None) == focus.ERR_NULL
+    assert fq_fwd(L, mx, x_dt=7) == focus.ERR_DTYPE
+    assert fq_fwd(L, mx, K=48) == focus.ERR_SHAPE          # not a multiple of 32
+    assert fq_fwd(L, mx, rows=-1) == focus.ERR_SHAPE
+    assert fq_fwd(L, mx, rows=1 << 31) == focus.ERR_SHAPE
+    assert fq_fwd(L, mx, ws=None) == focus.ERR_WORKSPACE
+    assert fq_fwd(L, mx, ws=ctypes.c_void_p((1 << 20) + 8)) == focus.ERR_WORKSPACE  # misaligned
+    assert fq_fwd(L, mx, ws_bytes=16) == focus.ERR_WORKSPACE
+    assert fq_fwd(L, mx, c=BOGUS) == focus.ERR_CONFIG       # activation mode takes no coefficients
+    nv = focus.qconfig(focus.NVFP4, 8)
+    assert fq_fwd(L, nv, K=64, s_fp=BOGUS) == focus.ERR_NULL  # NVFP4 weights need alpha
+    # fused backward
+    assert L.focus_recon_gemm_bwd(ctypes.byref(mx), BOGUS, BOGUS, 1, 64, 4, 40, BOGUS, 1, BOGUS, None, None,
+                                  BOGUS, BOGUS, None, BOGUS, 1 << 30, None) == focus.ERR_SHAPE
+    assert L.focus_recon_gemm_bwd(ctypes.byref(mx), BOGUS, BOGUS, 1, 64, 4, 64, BOGUS, 1, None, None, None,
+                                  BOGUS, BOGUS, None, BOGUS, 1 << 30, None) == focus.ERR_NULL
+    assert L.focus_recon_gemm_bwd(ctypes.byref(mx), BOGUS, BOGUS, 1, 64, 4, 64, BOGUS, 1, BOGUS, None, None,
+                                  BOGUS, BOGUS, None, BOGUS, 16, None) == focus.ERR_WORKSPACE
+    # forward GEMM
+    assert L.focus_recon_gemm_fwd(BOGUS, BOGUS, 1, 8, 8, 24, None, BOGUS, None, None, BOGUS, 1 << 30,
+                                  None) == focus.ERR_SHAPE
+    assert L.focus_recon_gemm_fwd(BOGUS, BOGUS, 1, 8, 8, 32, BOGUS, BOGUS, None, None, BOGUS, 1 << 30,
+                                  None) == focus.ERR_NULL  # MSE mode needs loss_out
+    assert L.focus_recon_gemm_fwd(BOGUS, BOGUS, 3, 8, 8, 32, None, BOGUS, None, None, BOGUS, 1 << 30,
+                                  None) == focus.ERR_DTYPE
+    # export and init
+    assert L.focus_export_packed(ctypes.byref(mx), BOGUS, 1, 4, 64, BOGUS, None, None, None, BOGUS, BOGUS,
+                                 1 << 20, None) == focus.ERR_NULL
+    assert L.focus_scales_init(ctypes.byref(nv), BOGUS, 1, 4, 64, BOGUS, BOGUS, None, BOGUS, 1 << 20,
+                               None) == focus.ERR_NULL
+    assert L.focus_fakequant_bwd(ctypes.byref(mx), BOGUS, 4, 64, BOGUS, 0, BOGUS, None, None, BOGUS, BOGUS,
+                                 BOGUS, 8, None) == focus.ERR_WORKSPACE
+    assert L.focus_check_flags(None, None) == focus.ERR_WORKSPACE
