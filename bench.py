@@ -1,0 +1,252 @@
+"""Benchmark of the FOCUS scale-learning step on one MI355X.
+
+One step = one fwd+bwd scale-learning pass over one decoder block for one batch of calibration
+tokens: dynamic activation fake-quant of the block's four distinct inputs, then for each of the
+seven linears the weight fake-quant with learned scales, the reconstruction GEMM with the MSE
+epilogue, and the fused straight-through backward to the scales and coefficients. Inputs are
+seeded synthetic tensors resident in HBM before timing starts. Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+REPO = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, REPO)
+
+METRIC = "ms per fwd+bwd scale-learning step per decoder block; fake-quant GB/s"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="block2560_mxfp4")
+    p.add_argument("--tokens", type=int, default=0, help="override the token count (0 = the workload's)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample-tokens", type=int, default=16384)
+    p.add_argument("--cpu-sample-rows", type=int, default=128)
+    return p.parse_args()
+
+
+class Timer:
+    """HIP events on the current stream around each library call, grouped by kernel family."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.spans = {}
+
+    def run(self, name, fn, units):
+        t = self.torch
+        a, b = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
+        a.record()
+        out = fn()
+        b.record()
+        self.spans.setdefault(name, []).append((a, b, units))
+        return out
+
+    def summary(self):
+        res = {}
+        for name, spans in self.spans.items():
+            ms = [a.elapsed_time(b) for a, b, _ in spans]
+            res[name] = {"launches": len(ms), "total_ms": sum(ms), "avg_ms": sum(ms) / len(ms),
+                         "units": sum(u for _, _, u in spans)}
+        return res
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(REPO, "paper_2608_01847_amd", "csrc"))):
+        with open(os.path.join(REPO, "paper_2608_01847_amd", "csrc", f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(kernel: str, src_hash: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it is current."""
+    path = os.path.join(REPO, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        data = json.load(f)
+    entry = data.get(kernel)
+    if not entry or entry.get("source_hash") != src_hash:
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the data-parallel path across GPUs is not built "
+              f"(asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_01847_amd import focus as F
+    from paper_2608_01847_amd import synth
+
+    w = synth.WORKLOADS[args.workload]
+    if args.tokens:
+        w = synth.scaled(w, M=args.tokens, name=w.name)
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    fmt, sb, M = w.fmt, w.sub_block, w.M
+    B = w.block
+
+    # ---- inputs and state, resident in HBM before timing (untimed) ----
+    acts = {src: synth.activation(w, src, device=dev) for src in w.inputs}
+    layers = []
+    for lin in w.linears:
+        W = synth.weight(w, lin, device=dev)
+        Y = synth.reference_output(acts[lin.source], W)
+        s, c, a = F.scales_init(W, fmt, sb)
+        layers.append(dict(lin=lin, W=W, Y=Y, s=s, c=c, a=a,
+                           W_hat=torch.empty_like(W),
+                           gs=torch.empty_like(s), gc=torch.empty_like(c),
+                           loss=torch.empty(1, dtype=torch.float64, device=dev)))
+    x_hat = {src: torch.empty_like(x) for src, x in acts.items()}
+    max_n = max(l.N for l in w.linears)
+    dY_buf = torch.empty(M * max_n, dtype=acts[w.linears[0].source].dtype, device=dev)
+    q = F.qconfig(fmt, sb)
+    ws_fq = F.workspace(F.workspace_size(F.CALL_FAKEQUANT_FWD, q, 0, M, max(w.inputs.values())))
+    ws_fwd = F.workspace(max(F.workspace_size(F.CALL_RECON_GEMM_FWD, q, M, l.N, l.K) for l in w.linears))
+    ws_bwd = F.workspace(max(F.workspace_size(F.CALL_RECON_GEMM_BWD, q, M, l.N, l.K) for l in w.linears))
+    torch.cuda.synchronize()
+
+    def step(timer):
+        for src, x in acts.items():
+            rows, K = x.shape
+            timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src]), rows * K)
+        for L in layers:
+            lin = L["lin"]
+            xh = x_hat[lin.source]
+            dY = dY_buf[:M * lin.N].view(M, lin.N)
+            timer.run("fakequant_weight",
+                      lambda: F.fakequant_fwd(L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws_fq, out=L["W_hat"]),
+                      lin.N * lin.K)
+            timer.run("recon_gemm_fwd",
+                      lambda: F.recon_gemm_fwd(xh, L["W_hat"], L["Y"], ws=ws_fwd, out=dY, loss=L["loss"]),
+                      2 * M * lin.N * lin.K)
+            timer.run("recon_gemm_bwd",
+                      lambda: F.recon_gemm_bwd(dY, xh, L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws_bwd,
+                                               out=(L["gs"], L["gc"])),
+                      2 * M * lin.N * lin.K)
+
+    for _ in range(args.warmup):
+        step(Timer(torch))
+    torch.cuda.synchronize()
+    if F.check_flags(ws_fq) != F.OK:
+        raise RuntimeError("domain error in the warm-up steps")
+
+    timer = Timer(torch)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step(timer)
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+    kern = timer.summary()
+    block_loss = float(sum(L["loss"].item() for L in layers))
+
+    # ---- algorithmic work ----
+    # fake quantisation bytes per element: activations read 2 + write 2 (bf16) (+2 for the NVFP4
+    # tensor-absmax pass); weights read W 2 + S_fp 4/B + c 4/sb, write W_hat 2
+    esz = 2 if w.dtype == "bf16" else 4
+    act_b = (2 * esz + (esz if fmt == 1 else 0))
+    wt_b = 2 * esz + 4.0 / B + 4.0 / sb
+    fq_bytes = kern["fakequant_act"]["units"] * act_b + kern["fakequant_weight"]["units"] * wt_b
+    fq_ms = kern["fakequant_act"]["total_ms"] + kern["fakequant_weight"]["total_ms"]
+    gemm_flops = kern["recon_gemm_fwd"]["units"] + kern["recon_gemm_bwd"]["units"]
+    gemm_ms = kern["recon_gemm_fwd"]["total_ms"] + kern["recon_gemm_bwd"]["total_ms"]
+
+    dominant = max(("recon_gemm_fwd", "recon_gemm_bwd"), key=lambda k: kern[k]["total_ms"])
+    d = kern[dominant]
+    per_launch_flops = d["units"] / d["launches"]
+    achieved = per_launch_flops / (d["avg_ms"] * 1e-3) / 1e12
+    src_hash = kernel_source_hash()
+    kname = {"recon_gemm_fwd": "fwd_mfma_kernel", "recon_gemm_bwd": "bwd_mfma_kernel"}[dominant]
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_from_profile(kname, src_hash),
+                "kernel": kname, "avg_launch_ms": round(d["avg_ms"], 4), "launches": d["launches"],
+                "flops_per_launch": per_launch_flops}
+
+    result = {
+        "metric": METRIC, "value": round(ms_per_step, 4), "unit": "ms per step", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if esz == 2 else "f32",
+        "data": "synthetic (seeded; shapes and distributions of the calibration workload)",
+        "config": {"workload": w.name, "tokens": M, "format": "mxfp4" if fmt == 0 else "nvfp4", "sub_block": sb,
+                   "linears": {l.name: [l.N, l.K] for l in w.linears}},
+        "roofline": roofline,
+        "fakequant_GBps": round(fq_bytes / (fq_ms * 1e-3) / 1e9, 1),
+        "fakequant_frac_hbm": round(fq_bytes / (fq_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "gemm_TFLOPs": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
+        "gemm_frac_bf16": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "total_ms_per_step": round(v["total_ms"] / args.steps, 4),
+                        "launches_per_step": v["launches"] // args.steps} for k, v in kern.items()},
+        "block_loss": block_loss,
+        "source_hash": src_hash,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens, args.cpu_sample_rows)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(w, sample_tokens, sample_rows):
+    """The CPU oracle on a bounded sample of the same step, extrapolated linearly to the full step.
+
+    Sample: for every input, `sample_tokens` tokens are fake-quantised; for every linear,
+    `sample_rows` weight rows are fake-quantised and their reconstruction loss and gradients are
+    computed over those tokens. Each part is linear in the tokens and/or rows it covers, so the
+    full-step time is each part's time scaled by the covered fraction."""
+    import numpy as np
+    import torch
+
+    from oracle import focus_oracle as O
+    from paper_2608_01847_amd import synth
+
+    O._lib()
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    Ms = min(sample_tokens, w.M)
+    full_ms = 0.0
+    sample_s = 0.0
+    xs = {}
+    for src, K in w.inputs.items():
+        X = synth.activation(w, src, M=Ms, device="cpu").float().numpy()
+        t0 = time.perf_counter()
+        xo, _, _, _ = O.fq_act(X, w.fmt)
+        dt = time.perf_counter() - t0
+        sample_s += dt
+        full_ms += dt * 1e3 * (w.M / Ms)
+        xs[src] = (X, O.gemm_operand(xo, w.dtype == "bf16"))
+    for lin in w.linears:
+        R = min(sample_rows, lin.N)
+        W = synth.weight(synth.scaled(w, M=Ms, name=w.name), lin, device="cpu")[:R].float().numpy()
+        X, X_op = xs[lin.source]
+        Y = (X.astype(np.float64) @ W.astype(np.float64).T)
+        t0 = time.perf_counter()
+        s, c, a = O.init_scales(W, w.fmt, w.sub_block)
+        fq = O.fq_weight(W, w.fmt, w.sub_block, s, c, a)
+        t1 = time.perf_counter()
+        O.recon_layer(X_op, O.gemm_operand(fq.w_hat, w.dtype == "bf16"), Y, fq, w.fmt, w.sub_block, a)
+        t2 = time.perf_counter()
+        sample_s += t2 - t0
+        full_ms += (t1 - t0) * 1e3 * (lin.N / R) + (t2 - t1) * 1e3 * (lin.N / R) * (w.M / Ms)
+    return {"value": round(full_ms, 1), "unit": "ms per step", "cores": threads, "kind": "oracle",
+            "sample": f"{Ms} of {w.M} tokens per input; {sample_rows} weight rows per linear "
+                      f"({sample_s:.1f} s measured), extrapolated linearly to the full step"}
+
+
+if __name__ == "__main__":
+    main()

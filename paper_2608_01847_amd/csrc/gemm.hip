@@ -234,12 +234,26 @@ BwdPlan plan_bwd(int op_dt, int fmt, int sb, int64_t M, int64_t N, int64_t K, bo
     const int64_t tn = p.path == 1 ? kMfmaTileN : 64, tk = p.path == 1 ? kMfmaTileK : 64;
     const int64_t step = p.path == 1 ? kMfmaTokenStep : 16;
     const int64_t tiles = cdiv(N, tn) * cdiv(K, tk);
+    const int64_t steps_total = cdiv(std::max<int64_t>(M, 1), step);
     int64_t splits = 1;
     if (!want_G) {
-        const int64_t target = p.path == 1 ? kMfmaBwdTargetWgs : 2048;
-        splits = std::max<int64_t>(1, std::min<int64_t>(cdiv(target, tiles), cdiv(M, 256)));
+        // The token range is split so that tiles * splits workgroups fill the chip in whole rounds
+        // (one 256 x 256 workgroup per CU on the MFMA path, several 64 x 64 ones on the VALU path):
+        // minimise rounds * (steps per split + epilogue), each split keeping >= 4 steps.
+        const int64_t slots = p.path == 1 ? kMfmaConcurrentWgs : 2048;
+        const int64_t epilogue_steps = 4;
+        const int64_t max_splits = std::max<int64_t>(1, std::min<int64_t>(steps_total / 4, 4096));
+        int64_t best = -1;
+        for (int64_t s = 1; s <= max_splits; s++) {
+            const int64_t rounds = cdiv(tiles * s, slots);
+            const int64_t cost = rounds * (cdiv(steps_total, s) + epilogue_steps);
+            if (best < 0 || cost < best) {
+                best = cost;
+                splits = s;
+            }
+        }
     }
-    p.chunk = std::max<int64_t>(step, cdiv(cdiv(std::max<int64_t>(M, 1), splits), step) * step);
+    p.chunk = cdiv(steps_total, splits) * step;
     p.splits = std::max<int64_t>(1, cdiv(M, p.chunk));
     const int64_t nb = K / block_of(fmt), ns = K / sb;
     p.ws_bytes = kWsHeader + (size_t)(p.splits * N * (nb + ns)) * sizeof(float);

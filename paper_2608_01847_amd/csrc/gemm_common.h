@@ -31,7 +31,7 @@ constexpr int kMfmaTileM = 256;       // forward output tile: tokens
 constexpr int kMfmaTileN = 256;       // backward output tile: out features
 constexpr int kMfmaTileK = 256;       // backward output tile: in features
 constexpr int kMfmaTokenStep = 64;    // backward reduction step over tokens
-constexpr int kMfmaBwdTargetWgs = 1024;
+constexpr int kMfmaConcurrentWgs = 256;  // one 128 KB-LDS workgroup per CU, 256 CUs
 
 bool mfma_fwd_supported(int64_t M, int64_t N, int64_t K);
 bool mfma_bwd_supported(int64_t M, int64_t N, int64_t K);

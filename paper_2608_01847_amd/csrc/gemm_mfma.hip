@@ -1,20 +1,471 @@
-// bf16 MFMA reconstruction GEMMs for gfx950 (not yet enabled: every shape takes the VALU path).
+// bf16 MFMA reconstruction GEMMs for gfx950 (v_mfma_f32_32x32x16_bf16, fp32 accumulation).
+//
+// Both kernels share one main loop: a 256 x 256 output tile per workgroup of 256 threads (four
+// waves, 2 x 2, each owning 128 x 128 = 4 x 4 MFMA tiles of 32 x 32), a reduction step of 64, and
+// two LDS stages of 2 x 32 KB. The next step's tiles are fetched into registers while the current
+// step's MFMAs run, then stored into the other stage; one barrier per step.
+//
+// MFMA operand layout (32x32x16): lane l holds 8 consecutive reduction values of row l % 32 of A
+// (resp. column l % 32 of B), starting at reduction index 8 (l / 32). Accumulator register r of
+// lane l holds C[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].
+//
+// Forward:  C = X_hat W_hat^T (rows = tokens, columns = out features). X_hat [M][K] and
+//           W_hat [N][K] are K-contiguous, so tiles are copied straight into LDS. The epilogue
+//           forms D = C - Y_ref, dY = D * 2/(M N) and per-column sums of D^2: a lane owns one
+//           column, so the column sums are in-lane plus one cross-lane add.
+// Backward: C = X_hat^T dY (rows = in features k, columns = out features n), i.e. G^T with the
+//           reduction over tokens. Both operands are token-major in memory, so each thread loads
+//           an 8 x 8 block and transposes it in registers before the LDS store. In the epilogue a
+//           lane holds 4 consecutive k of one n per register group, so a sub-block of 8 is an
+//           in-lane sum of 4 plus one exchange with lane l ^ 32, and a block of 32 is 16 in-lane
+//           values plus the same exchange.
 #include "gemm_common.h"
+
+#include <utility>
 
 namespace focus {
 
-bool mfma_fwd_supported(int64_t, int64_t, int64_t) { return false; }
-bool mfma_bwd_supported(int64_t, int64_t, int64_t) { return false; }
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-hipError_t launch_fwd_mfma(const void *, const void *, int64_t, int64_t, int64_t, const void *, void *, float,
-                           double *, hipStream_t) {
-    return hipErrorInvalidValue;
+namespace {
+
+constexpr int kTile = 256;            // output tile edge
+constexpr int kStep = 64;             // reduction step
+constexpr int kThreads = 256;         // four waves
+constexpr int kOpBytes = kTile * 128; // one operand tile in LDS: 256 rows x 64 bf16
+constexpr int kStageBytes = 2 * kOpBytes;
+constexpr int kLdsBytes = 2 * kStageBytes;
+
+static_assert(kTile == kMfmaTileM && kTile == kMfmaTileN && kTile == kMfmaTileK, "tile geometry");
+static_assert(kStep == kMfmaTokenStep, "token step");
+
+// Byte offset of 16-byte chunk `chunk` (0..7) of LDS tile row `row`. The chunk is xor-ed with the
+// row's bits 0-2 and 3-5: the fragment reads (8 consecutive rows, one chunk) and the transposed
+// stores (rows 8 apart, one chunk) then each touch 8 distinct chunk slots of a 128-byte row.
+__device__ __forceinline__ uint32_t lds_off(uint32_t row, uint32_t chunk) {
+    return row * 128u + ((chunk ^ (row & 7u) ^ ((row >> 3) & 7u)) << 4);
 }
 
-hipError_t launch_bwd_mfma(int, int, const void *, const void *, int64_t, int64_t, int64_t, int64_t, int64_t,
-                           const void *, const float *, const float *, int, const float *, int, float *, float *,
-                           uint32_t *, hipStream_t) {
-    return hipErrorInvalidValue;
+__device__ __forceinline__ uint32_t word_of(const uint4 &v, int p) {
+    return p == 0 ? v.x : p == 1 ? v.y : p == 2 ? v.z : v.w;
+}
+
+// Raw buffer resources: a load whose offset is at or past num_records returns zeros and a store
+// there is dropped, so bounds are handled by the hardware range check instead of branches.
+constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr int kRsrcWord3 = 0x00020000;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, int64_t bytes) {
+    const int64_t n = bytes < 0 ? 0 : (bytes > 0x7FFFFFFF ? 0x7FFFFFFF : bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)n, kRsrcWord3);
+}
+
+__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// 256 x 64 tile of a row-major [R][K] bf16 operand at (r0, k0): thread t copies chunk t & 7 of the
+// rows (t >> 3) + 32 i. Rows past R and chunks past K read as zero. The resource starts at row r0,
+// so offsets stay below 256 * K * 2 bytes.
+struct DirectTile {
+    uint4 v[8];
+    __device__ __forceinline__ void load(const uint16_t *__restrict__ base, int64_t R, int64_t K, int64_t r0,
+                                         int64_t k0, int t) {
+        const __amdgpu_buffer_rsrc_t rs = make_rsrc(base + r0 * K, (R - r0) * K * 2);
+        const int64_t k = k0 + (t & 7) * 8;
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            const uint32_t row = (t >> 3) + 32 * i;
+            v[i] = buffer_load16(rs, k < K ? (uint32_t)((row * K + k) * 2) : kOutOfRange);
+        }
+    }
+    __device__ __forceinline__ void store(char *lds, int t) const {
+#pragma unroll
+        for (int i = 0; i < 8; i++)
+            *reinterpret_cast<uint4 *>(lds + lds_off((t >> 3) + 32 * i, t & 7)) = v[i];
+    }
+};
+
+// 64 x 256 tile of a row-major [T][C] bf16 operand (reduction rows t0.., columns c0..), stored
+// transposed as 256 LDS rows of 64 reduction values. Thread t loads reduction rows
+// 8 (t >> 5) + 0..7 of columns 8 (t & 31) + 0..7 and writes column j of that block as LDS row
+// 8 (t & 31) + j, chunk t >> 5. Rows at or past t_end and columns past C read as zero (C % 8 == 0).
+// The resource starts at row t0, so offsets stay below 64 * C * 2 bytes.
+struct TransposedTile {
+    uint4 v[8];
+    __device__ __forceinline__ void load(const uint16_t *__restrict__ base, int64_t t_end, int64_t C, int64_t t0,
+                                         int64_t c0, int t) {
+        const __amdgpu_buffer_rsrc_t rs = make_rsrc(base + t0 * C, (t_end - t0) * C * 2);
+        const int64_t col = c0 + (t & 31) * 8;
+#pragma unroll
+        for (int rr = 0; rr < 8; rr++) {
+            const uint32_t tt = (t >> 5) * 8 + rr;
+            v[rr] = buffer_load16(rs, col < C ? (uint32_t)((tt * C + col) * 2) : kOutOfRange);
+        }
+    }
+    __device__ __forceinline__ void store(char *lds, int t) const {
+#pragma unroll
+        for (int j = 0; j < 8; j++) {
+            const int p = j >> 1;
+            uint32_t w[4];
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+                const uint32_t x = word_of(v[2 * q], p), y = word_of(v[2 * q + 1], p);
+                w[q] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
+            }
+            *reinterpret_cast<uint4 *>(lds + lds_off((t & 31) * 8 + j, t >> 5)) = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+    }
+};
+
+// Fragments of one k16 step: A rows / B columns of the wave's 128 x 128 sub-tile.
+struct Frags {
+    bf16x8_t a[4], b[4];
+};
+
+__device__ __forceinline__ void load_frags(Frags &f, const char *As, const char *Bs, int ks, int wm, int wn,
+                                           int lane) {
+    const uint32_t lr = lane & 31, lh = lane >> 5;
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        f.a[i] = *reinterpret_cast<const bf16x8_t *>(As + lds_off(wm * 128 + i * 32 + lr, ks * 2 + lh));
+        f.b[i] = *reinterpret_cast<const bf16x8_t *>(Bs + lds_off(wn * 128 + i * 32 + lr, ks * 2 + lh));
+    }
+}
+
+__device__ __forceinline__ void mma_frags(const Frags &f, f32x16_t (&acc)[4][4]) {
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+}
+
+// One reduction step of 64 on the wave's 128 x 128 sub-tile. `f` holds the fragments of k16 step 0
+// on entry; the fragments of step ks + 1 are read while the 16 MFMAs of step ks run.
+__device__ __forceinline__ void mma_step(const char *As, const char *Bs, Frags &f, f32x16_t (&acc)[4][4], int wm,
+                                         int wn, int lane) {
+    Frags g;
+    load_frags(g, As, Bs, 1, wm, wn, lane);
+    mma_frags(f, acc);
+    load_frags(f, As, Bs, 2, wm, wn, lane);
+    mma_frags(g, acc);
+    load_frags(g, As, Bs, 3, wm, wn, lane);
+    mma_frags(f, acc);
+    mma_frags(g, acc);
+}
+
+// Calls f(std::integral_constant<int, 0>) ... f(<N-1>): every accumulator index is then a
+// compile-time constant, so the accumulators stay in registers.
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, Is...>) {
+    (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(kThreads, 1)
+fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, int64_t M, int64_t N, int64_t K,
+                const uint16_t *__restrict__ Yref, uint16_t *__restrict__ dY, float dscale,
+                double *__restrict__ colpart, int tiles_n) {
+    __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
+    const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+    const int64_t m0 = (int64_t)tm * kTile, n0 = (int64_t)tn * kTile;
+
+    f32x16_t acc[4][4];
+    const f32x16_t zero = {};
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) acc[i][j] = zero;
+
+    DirectTile a, b;
+    const int64_t nk = (K + kStep - 1) / kStep;
+    a.load(X, M, K, m0, 0, t);
+    b.load(W, N, K, n0, 0, t);
+    a.store(smem, t);
+    b.store(smem + kOpBytes, t);
+    __syncthreads();
+    Frags f;
+    load_frags(f, smem, smem + kOpBytes, 0, wm, wn, lane);
+    for (int64_t kt = 0; kt < nk; kt++) {
+        char *cur = smem + (kt & 1) * kStageBytes;
+        char *nxt = smem + ((kt + 1) & 1) * kStageBytes;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            a.load(X, M, K, m0, (kt + 1) * kStep, t);
+            b.load(W, N, K, n0, (kt + 1) * kStep, t);
+        }
+        mma_step(cur, cur + kOpBytes, f, acc, wm, wn, lane);
+        if (more) {
+            a.store(nxt, t);
+            b.store(nxt + kOpBytes, t);
+        }
+        __syncthreads();
+        if (more) load_frags(f, nxt, nxt + kOpBytes, 0, wm, wn, lane);
+    }
+
+    // ---- epilogue: D = Y_hat - Y_ref, dY = D * dscale, column sums of D^2 ----
+    // The 256 x 256 bf16 tile of Y_ref is brought into LDS (free after the main loop) with
+    // coalesced 16-byte loads; each lane then reads its accumulators' Y values from LDS, writes dY
+    // over them, and the dY tile leaves with coalesced 16-byte stores. Rows past M and columns past
+    // N hold zero accumulators and read Y_ref as zero, so they add nothing to the column sums, and
+    // their stores fall outside the resource and are dropped. Tile rows are 512 bytes; the two
+    // 64-byte halves of each 128-byte span are swapped on rows with bit 2 set, so the lanes reading
+    // rows m and m + 4 of one column group use different banks.
+    const int lr = lane & 31, lh = lane >> 5;
+    const uint32_t N32 = (uint32_t)N;  // offsets are below 256 * N * 2 < 2^31 (checked when chosen)
+    const __amdgpu_buffer_rsrc_t rs_y = make_rsrc(Yref + m0 * N, Yref ? (M - m0) * N * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rs_d = make_rsrc(dY + m0 * N, (M - m0) * N * 2);
+    auto tile_off = [](uint32_t row, uint32_t chunk) {  // chunk: 8 columns (16 bytes), 0..31
+        return row * 512u + ((chunk ^ (((row >> 2) & 1u) << 2)) << 4);
+    };
+    if (Yref) {
+#pragma unroll 8
+        for (int i = 0; i < 32; i++) {
+            const uint32_t cidx = t + 256 * i, row = cidx >> 5, chunk = cidx & 31;
+            const int64_t col = n0 + chunk * 8;
+            const uint32_t off = col < N ? (row * N32 + (uint32_t)col) * 2u : kOutOfRange;
+            *reinterpret_cast<uint4 *>(smem + tile_off(row, chunk)) = buffer_load16(rs_y, off);
+        }
+        __syncthreads();
+    }
+    double csum[4] = {0.0, 0.0, 0.0, 0.0};
+    static_for<4>([&](auto i) {
+        static_for<4>([&](auto j) {
+            const uint32_t n = wn * 128 + j * 32 + lr;  // column in the tile
+            static_for<16>([&](auto r) {
+                const uint32_t m = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);  // row in the tile
+                uint16_t *p = reinterpret_cast<uint16_t *>(smem + tile_off(m, n >> 3)) + (n & 7);
+                const float v = acc[i][j][(int)r];
+                if (Yref) {
+                    const float d = v - __uint_as_float((uint32_t)*p << 16);
+                    *p = (uint16_t)f32_to_bf16_bits(d * dscale);
+                    csum[j] += (double)d * (double)d;
+                } else {
+                    *p = (uint16_t)f32_to_bf16_bits(v);
+                }
+            });
+        });
+    });
+    __syncthreads();
+#pragma unroll 8
+    for (int i = 0; i < 32; i++) {
+        const uint32_t cidx = t + 256 * i, row = cidx >> 5, chunk = cidx & 31;
+        const int64_t col = n0 + chunk * 8;
+        const uint32_t off = col < N ? (row * N32 + (uint32_t)col) * 2u : kOutOfRange;
+        const uint4 v = *reinterpret_cast<const uint4 *>(smem + tile_off(row, chunk));
+        typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 w = {v.x, v.y, v.z, v.w};
+        __builtin_amdgcn_raw_buffer_store_b128(w, rs_d, (int)off, 0, 0);
+    }
+    if (!Yref) return;
+#pragma unroll
+    for (int j = 0; j < 4; j++) csum[j] += __shfl_xor(csum[j], 32, 64);  // lanes l and l ^ 32 share a column
+    double *red = reinterpret_cast<double *>(smem);                     // [2 waves along M][256 columns]
+    __syncthreads();                                                    // the dY tile has left LDS
+    if (lh == 0) {
+#pragma unroll
+        for (int j = 0; j < 4; j++) red[wm * kTile + wn * 128 + j * 32 + lr] = csum[j];
+    }
+    __syncthreads();
+    if (n0 + t < N) colpart[(int64_t)tm * N + n0 + t] = red[t] + red[kTile + t];
+}
+
+// ------------------------------------------------------------------------------------------------
+template <int FMT, int WDT>
+__global__ void __launch_bounds__(kThreads, 1)
+bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X, int64_t M, int64_t N, int64_t K,
+                int64_t chunk, const void *__restrict__ W, const float *__restrict__ s_fp,
+                const float *__restrict__ c, int sb_log2, const float *__restrict__ alpha_ptr, int ste_clip,
+                float *__restrict__ part_s, float *__restrict__ part_c, uint32_t *flag, int tiles_n) {
+    __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
+    const int tk = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+    const int64_t k0 = (int64_t)tk * kTile, n0 = (int64_t)tn * kTile;
+    const int64_t split = blockIdx.y;
+    const int64_t t_begin = split * chunk, t_end = std::min<int64_t>(M, t_begin + chunk);
+
+    f32x16_t acc[4][4];
+    const f32x16_t zero = {};
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) acc[i][j] = zero;
+
+    TransposedTile a, b;  // a: X_hat columns k0.. (rows of C); b: dY columns n0.. (columns of C)
+    const int64_t nk = t_end > t_begin ? (t_end - t_begin + kStep - 1) / kStep : 0;
+    if (nk > 0) {
+        a.load(X, t_end, K, t_begin, k0, t);
+        b.load(dY, t_end, N, t_begin, n0, t);
+        a.store(smem, t);
+        b.store(smem + kOpBytes, t);
+    }
+    __syncthreads();
+    Frags f;
+    if (nk > 0) load_frags(f, smem, smem + kOpBytes, 0, wm, wn, lane);
+    for (int64_t kt = 0; kt < nk; kt++) {
+        char *cur = smem + (kt & 1) * kStageBytes;
+        char *nxt = smem + ((kt + 1) & 1) * kStageBytes;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            a.load(X, t_end, K, t_begin + (kt + 1) * kStep, k0, t);
+            b.load(dY, t_end, N, t_begin + (kt + 1) * kStep, n0, t);
+        }
+        mma_step(cur, cur + kOpBytes, f, acc, wm, wn, lane);
+        if (more) {
+            a.store(nxt, t);
+            b.store(nxt + kOpBytes, t);
+        }
+        __syncthreads();
+        if (more) load_frags(f, nxt, nxt + kOpBytes, 0, wm, wn, lane);
+    }
+
+    // ---- fused straight-through epilogue on G^T = acc ----
+    constexpr int B = block_of(FMT);
+    const float alpha = FMT == kFmtNV ? *alpha_ptr : 1.0f;
+    const int sb = 1 << sb_log2;
+    const int64_t nb = K / B, ns = K >> sb_log2;
+    const int lr = lane & 31, lh = lane >> 5;
+    bool bad = false;
+    static_for<4>([&](auto j) {
+        const int64_t n = n0 + wn * 128 + j * 32 + lr;
+        const bool n_ok = n < N;
+        static_for<4>([&](auto i) {
+            const int64_t kb = k0 + wm * 128 + i * 32;  // 32 consecutive k: one MXFP4 / two NVFP4 blocks
+            float tc[4][2];                              // per group of 8 k: sums of elements 0-1 / 2-3
+            float ts[4];                                 // per group of 8 k
+            static_for<4>([&](auto g) {
+                const int64_t kg = kb + 8 * g;           // group start; this lane has kg + 4 lh + 0..3
+                const int64_t k = kg + 4 * lh;
+                tc[g][0] = tc[g][1] = ts[g] = 0.0f;
+                if (n_ok && kg < K) {
+                    float w[4];
+                    if (WDT == kBF16) {
+                        const uint2 p = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(W) + n * K + k);
+                        w[0] = __uint_as_float(p.x << 16);
+                        w[1] = __uint_as_float(p.x & 0xFFFF0000u);
+                        w[2] = __uint_as_float(p.y << 16);
+                        w[3] = __uint_as_float(p.y & 0xFFFF0000u);
+                    } else {
+                        const float4 p = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(W) + n * K + k);
+                        w[0] = p.x; w[1] = p.y; w[2] = p.z; w[3] = p.w;
+                    }
+                    uint32_t byte;
+                    const float sdq = weight_sdq(FMT, s_fp[n * nb + kg / B], alpha, byte, bad);
+                    float cv0 = 1.0f, cv1 = 1.0f;
+                    if (c) {
+                        cv0 = c[n * ns + (k >> sb_log2)];
+                        cv1 = sb == 2 ? c[n * ns + ((k + 2) >> sb_log2)] : cv0;
+                        bad = bad || bad_coeff(cv0) || bad_coeff(cv1);
+                    }
+                    static_for<4>([&](auto e) {
+                        float a1, a2;
+                        ste_terms(acc[i][j][(int)(4 * g + e)], w[e], sdq, e < 2 ? cv0 : cv1, ste_clip != 0, a1, a2);
+                        tc[g][e >> 1] += a1;
+                        ts[g] += a2;
+                    });
+                }
+            });
+            // ---- sub-block sums of G m w (scaled by -1/c^2 after the split reduction) ----
+            if (sb <= 4) {
+                // a sub-block lies inside one lane's 4 consecutive k
+                static_for<4>([&](auto g) {
+                    const int64_t k = kb + 8 * g + 4 * lh;
+                    if (n_ok && kb + 8 * g < K) {
+                        float *dst = part_c + (split * N + n) * ns;
+                        if (sb == 4) {
+                            dst[k >> 2] = tc[g][0] + tc[g][1];
+                        } else {
+                            dst[k >> 1] = tc[g][0];
+                            dst[(k >> 1) + 1] = tc[g][1];
+                        }
+                    }
+                });
+            } else {
+                float s8[4];
+                static_for<4>([&](auto g) {
+                    s8[g] = tc[g][0] + tc[g][1];
+                    s8[g] += __shfl_xor(s8[g], 32, 64);
+                });
+                if (lh == 0 && n_ok) {
+                    float *dst = part_c + (split * N + n) * ns;
+                    if (sb == 8) {
+                        static_for<4>([&](auto g) {
+                            if (kb + 8 * g < K) dst[(kb >> 3) + g] = s8[g];
+                        });
+                    } else if (sb == 16) {
+                        if (kb < K) dst[kb >> 4] = s8[0] + s8[1];
+                        if (kb + 16 < K) dst[(kb >> 4) + 1] = s8[2] + s8[3];
+                    } else {
+                        if (kb < K) dst[kb >> 5] = (s8[0] + s8[1]) + (s8[2] + s8[3]);
+                    }
+                }
+            }
+            // ---- block sums of G (q - m u) ----
+            float h0 = ts[0] + ts[1], h1 = ts[2] + ts[3];
+            h0 += __shfl_xor(h0, 32, 64);
+            h1 += __shfl_xor(h1, 32, 64);
+            if (lh == 0 && n_ok) {
+                float *dst = part_s + (split * N + n) * nb;
+                if (B == 32) {
+                    if (kb < K) dst[kb >> 5] = h0 + h1;
+                } else {
+                    if (kb < K) dst[kb >> 4] = h0;
+                    if (kb + 16 < K) dst[(kb >> 4) + 1] = h1;
+                }
+            }
+        });
+    });
+    if (bad) raise_domain_flag(flag);
+}
+
+// ================================================================================================
+
+// Buffer offsets are 32-bit: a tile's rows must span less than 2^31 bytes.
+bool mfma_fwd_supported(int64_t M, int64_t N, int64_t K) {
+    return M > 0 && N > 0 && N % 8 == 0 && K % 16 == 0 && int64_t(kTile) * K * 2 < (int64_t(1) << 31) &&
+           int64_t(kTile) * N * 2 < (int64_t(1) << 31) &&
+           (M + kTile - 1) / kTile * ((N + kTile - 1) / kTile) < (int64_t(1) << 31);
+}
+
+bool mfma_bwd_supported(int64_t M, int64_t N, int64_t K) {
+    return N % 8 == 0 && K % 16 == 0 && N > 0 && K > 0 && M >= 0 && int64_t(kStep) * N * 2 < (int64_t(1) << 31) &&
+           int64_t(kStep) * K * 2 < (int64_t(1) << 31);
+}
+
+hipError_t launch_fwd_mfma(const void *X, const void *W, int64_t M, int64_t N, int64_t K, const void *Yref, void *dY,
+                           float dscale, double *colpart, hipStream_t st) {
+    const int tiles_m = (int)((M + kTile - 1) / kTile), tiles_n = (int)((N + kTile - 1) / kTile);
+    fwd_mfma_kernel<<<dim3((unsigned)tiles_m * tiles_n), kThreads, 0, st>>>(
+        static_cast<const uint16_t *>(X), static_cast<const uint16_t *>(W), M, N, K,
+        static_cast<const uint16_t *>(Yref), static_cast<uint16_t *>(dY), dscale, colpart, tiles_n);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_mfma(int fmt, int w_dt, const void *dY, const void *X, int64_t M, int64_t N, int64_t K,
+                           int64_t chunk, int64_t splits, const void *W, const float *s_fp, const float *c, int sb,
+                           const float *alpha, int ste_clip, float *part_s, float *part_c, uint32_t *flag,
+                           hipStream_t st) {
+    const int tiles_k = (int)((K + kTile - 1) / kTile), tiles_n = (int)((N + kTile - 1) / kTile);
+    int sbl = 0;
+    while ((1 << sbl) < sb) sbl++;
+    const dim3 grid((unsigned)tiles_k * tiles_n, (unsigned)splits);
+    const uint16_t *dy = static_cast<const uint16_t *>(dY), *x = static_cast<const uint16_t *>(X);
+#define BM(F, WD) bwd_mfma_kernel<F, WD><<<grid, kThreads, 0, st>>>(dy, x, M, N, K, chunk, W, s_fp, c, sbl, alpha, ste_clip, part_s, part_c, flag, tiles_n)
+    if (fmt == kFmtMX) { if (w_dt == kBF16) BM(kFmtMX, kBF16); else BM(kFmtMX, kF32); }
+    else { if (w_dt == kBF16) BM(kFmtNV, kBF16); else BM(kFmtNV, kF32); }
+#undef BM
+    return hipGetLastError();
 }
 
 }  // namespace focus
