@@ -1,9 +1,12 @@
 // bf16 MFMA reconstruction GEMMs for gfx950 (v_mfma_f32_32x32x16_bf16, fp32 accumulation).
 //
-// Both kernels share one main loop: a 256 x 256 output tile per workgroup of 256 threads (four
-// waves, 2 x 2, each owning 128 x 128 = 4 x 4 MFMA tiles of 32 x 32), a reduction step of 64, and
-// two LDS stages of 2 x 32 KB. The next step's tiles are fetched into registers while the current
-// step's MFMAs run, then stored into the other stage; one barrier per step.
+// Both kernels compute a 256 x 256 output tile per workgroup of 256 threads (four waves, 2 x 2,
+// each owning 128 x 128 = 4 x 4 MFMA tiles of 32 x 32), with one barrier per reduction step:
+//   forward : operand tiles go straight from memory into four LDS stages of 32 of K
+//             (buffer_load ... lds), three steps ahead of the MFMAs;
+//   backward: operand tiles are token-major and must be transposed, so each thread fetches the
+//             next 64-token step into registers while the current one runs, transposes 8 x 8
+//             blocks in registers and stores them into the other of two LDS stages.
 //
 // MFMA operand layout (32x32x16): lane l holds 8 consecutive reduction values of row l % 32 of A
 // (resp. column l % 32 of B), starting at reduction index 8 (l / 32). Accumulator register r of
@@ -67,28 +70,6 @@ __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-// 256 x 64 tile of a row-major [R][K] bf16 operand at (r0, k0): thread t copies chunk t & 7 of the
-// rows (t >> 3) + 32 i. Rows past R and chunks past K read as zero. The resource starts at row r0,
-// so offsets stay below 256 * K * 2 bytes.
-struct DirectTile {
-    uint4 v[8];
-    __device__ __forceinline__ void load(const uint16_t *__restrict__ base, int64_t R, int64_t K, int64_t r0,
-                                         int64_t k0, int t) {
-        const __amdgpu_buffer_rsrc_t rs = make_rsrc(base + r0 * K, (R - r0) * K * 2);
-        const int64_t k = k0 + (t & 7) * 8;
-#pragma unroll
-        for (int i = 0; i < 8; i++) {
-            const uint32_t row = (t >> 3) + 32 * i;
-            v[i] = buffer_load16(rs, k < K ? (uint32_t)((row * K + k) * 2) : kOutOfRange);
-        }
-    }
-    __device__ __forceinline__ void store(char *lds, int t) const {
-#pragma unroll
-        for (int i = 0; i < 8; i++)
-            *reinterpret_cast<uint4 *>(lds + lds_off((t >> 3) + 32 * i, t & 7)) = v[i];
-    }
-};
-
 // 64 x 256 tile of a row-major [T][C] bf16 operand (reduction rows t0.., columns c0..), stored
 // transposed as 256 LDS rows of 64 reduction values. Thread t loads reduction rows
 // 8 (t >> 5) + 0..7 of columns 8 (t & 31) + 0..7 and writes column j of that block as LDS row
@@ -121,6 +102,56 @@ struct TransposedTile {
     }
 };
 
+// ---- forward operand staging: direct-to-LDS buffer loads ---------------------------------------
+// The forward operands are K-contiguous, so their tiles go from HBM / L2 straight into LDS with
+// buffer_load_dwordx4 ... lds (no VGPR round trip, no LDS store instructions). A step covers 32
+// of K; four 32 KB stages keep the loads of three steps in flight while one step is computed.
+constexpr int kFwdStep = 32;
+constexpr int kFwdOpBytes = kTile * 64;   // 256 rows x 32 bf16 = 16 KB
+constexpr int kFwdStageBytes = 2 * kFwdOpBytes;
+constexpr int kFwdStages = 4;
+static_assert(kFwdStages * kFwdStageBytes <= kLdsBytes, "forward stages fit the LDS allocation");
+
+typedef __attribute__((address_space(3))) char lds_char;
+
+// Byte offset of 16-byte chunk `chunk` (0..3) of row `row` in a 64-byte-row tile; the chunk is
+// xor-ed with row bits 1-2 so the fragment reads of 8 consecutive rows hit 8 distinct bank groups.
+__device__ __forceinline__ uint32_t fwd_off(uint32_t row, uint32_t chunk) {
+    return row * 64u + ((chunk ^ ((row >> 1) & 3u)) << 4);
+}
+
+// A direct-to-LDS load writes lane L's 16 bytes at LDS byte 16 L from the instruction's base, so
+// each wave fills 1 KB blocks: lane L of block q lands in row 16 q + L / 4, physical chunk L % 4,
+// which must hold logical chunk (L % 4) ^ ((row >> 1) & 3) = (L % 4) ^ ((L >> 3) & 3). Each
+// thread's byte offsets at k0 = 0 are fixed for the whole tile.
+struct FwdDma {
+    uint32_t lane_off[4];
+    uint32_t kk;  // k offset of this lane's chunk inside a step
+    __device__ __forceinline__ void init(int64_t K, int wave, int lane) {
+        kk = (uint32_t)(((lane & 3) ^ ((lane >> 3) & 3)) * 8);
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            const uint32_t row = (wave * 4 + i) * 16 + (lane >> 2);
+            lane_off[i] = (row * (uint32_t)K + kk) * 2u;
+        }
+    }
+    // Issues the 4 loads of this wave for the step starting at k0. Chunks at or past K get bit 31
+    // of the offset set: out of range, they read as zeros (an arithmetic mask, not a branch).
+    __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, int64_t K, int64_t k0, lds_char *dst,
+                                          int wave) const {
+        const int32_t lim = (int32_t)(K - k0);
+        const uint32_t bad = ((uint32_t)(lim - 1 - (int32_t)kk) >> 31) << 31;
+        const uint32_t base = (uint32_t)k0 * 2u;
+#pragma unroll
+        for (int i = 0; i < 4; i++)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst + (wave * 4 + i) * 1024, 16,
+                                                     (int)((lane_off[i] + base) | bad), 0, 0, 0);
+    }
+};
+
+// s_waitcnt with vmcnt <= n (n < 64) and the LDS and export counters unconstrained
+#define FOCUS_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (0x7 << 4) | (0xF << 8))
+
 // Fragments of one k16 step: A rows / B columns of the wave's 128 x 128 sub-tile.
 struct Frags {
     bf16x8_t a[4], b[4];
@@ -133,6 +164,16 @@ __device__ __forceinline__ void load_frags(Frags &f, const char *As, const char 
     for (int i = 0; i < 4; i++) {
         f.a[i] = *reinterpret_cast<const bf16x8_t *>(As + lds_off(wm * 128 + i * 32 + lr, ks * 2 + lh));
         f.b[i] = *reinterpret_cast<const bf16x8_t *>(Bs + lds_off(wn * 128 + i * 32 + lr, ks * 2 + lh));
+    }
+}
+
+__device__ __forceinline__ void load_frags_fwd(Frags &f, const char *As, const char *Bs, int ks, int wm, int wn,
+                                               int lane) {
+    const uint32_t lr = lane & 31, lh = lane >> 5;
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        f.a[i] = *reinterpret_cast<const bf16x8_t *>(As + fwd_off(wm * 128 + i * 32 + lr, ks * 2 + lh));
+        f.b[i] = *reinterpret_cast<const bf16x8_t *>(Bs + fwd_off(wn * 128 + i * 32 + lr, ks * 2 + lh));
     }
 }
 
@@ -188,31 +229,39 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
 #pragma unroll
         for (int j = 0; j < 4; j++) acc[i][j] = zero;
 
-    DirectTile a, b;
-    const int64_t nk = (K + kStep - 1) / kStep;
-    a.load(X, M, K, m0, 0, t);
-    b.load(W, N, K, n0, 0, t);
-    a.store(smem, t);
-    b.store(smem + kOpBytes, t);
-    __syncthreads();
-    Frags f;
-    load_frags(f, smem, smem + kOpBytes, 0, wm, wn, lane);
-    for (int64_t kt = 0; kt < nk; kt++) {
-        char *cur = smem + (kt & 1) * kStageBytes;
-        char *nxt = smem + ((kt + 1) & 1) * kStageBytes;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            a.load(X, M, K, m0, (kt + 1) * kStep, t);
-            b.load(W, N, K, n0, (kt + 1) * kStep, t);
-        }
-        mma_step(cur, cur + kOpBytes, f, acc, wm, wn, lane);
-        if (more) {
-            a.store(nxt, t);
-            b.store(nxt + kOpBytes, t);
-        }
-        __syncthreads();
-        if (more) load_frags(f, nxt, nxt + kOpBytes, 0, wm, wn, lane);
+    // Four LDS stages of 32 of K; the loads of steps kt + 1 .. kt + 3 are in flight while step kt
+    // is computed. Loads past the end of K read zeros into stages that are never read.
+    lds_char *const lsm = (lds_char *)smem;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    FwdDma pa, pb;
+    pa.init(K, wave_u, lane);
+    pb.init(K, wave_u, lane);
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(X + m0 * K, (M - m0) * K * 2);
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc(W + n0 * K, (N - n0) * K * 2);
+    const int64_t nk = (K + kFwdStep - 1) / kFwdStep;
+#pragma unroll
+    for (int s0 = 0; s0 < kFwdStages - 1; s0++) {
+        pa.issue(ra, K, s0 * kFwdStep, lsm + s0 * kFwdStageBytes, wave_u);
+        pb.issue(rb, K, s0 * kFwdStep, lsm + s0 * kFwdStageBytes + kFwdOpBytes, wave_u);
     }
+    for (int64_t kt = 0; kt < nk; kt++) {
+        // this thread's 8 loads of step kt have landed (steps kt + 1, kt + 2 may still be in
+        // flight); after the barrier everyone's have, and stage (kt + 3) % 4, last read in step
+        // kt - 1, is free. A bare s_barrier: __syncthreads would also wait for the loads in flight.
+        FOCUS_WAIT_VMCNT(16);
+        asm volatile("s_barrier" ::: "memory");
+        const int cs = (int)(kt & 3), nsg = (int)((kt + 3) & 3);
+        const char *As = smem + cs * kFwdStageBytes, *Bs = As + kFwdOpBytes;
+        Frags f, g;
+        load_frags_fwd(f, As, Bs, 0, wm, wn, lane);
+        pa.issue(ra, K, (kt + 3) * kFwdStep, lsm + nsg * kFwdStageBytes, wave_u);
+        pb.issue(rb, K, (kt + 3) * kFwdStep, lsm + nsg * kFwdStageBytes + kFwdOpBytes, wave_u);
+        load_frags_fwd(g, As, Bs, 1, wm, wn, lane);
+        mma_frags(f, acc);
+        mma_frags(g, acc);
+    }
+    FOCUS_WAIT_VMCNT(0);
+    __syncthreads();
 
     // ---- epilogue: D = Y_hat - Y_ref, dY = D * dscale, column sums of D^2 ----
     // The 256 x 256 bf16 tile of Y_ref is brought into LDS (free after the main loop) with
