@@ -114,21 +114,26 @@ static_assert(kFwdStages * kFwdStageBytes <= kLdsBytes, "forward stages fit the 
 
 typedef __attribute__((address_space(3))) char lds_char;
 
-// Byte offset of 16-byte chunk `chunk` (0..3) of row `row` in a 64-byte-row tile; the chunk is
-// xor-ed with row bits 1-2 so the fragment reads of 8 consecutive rows hit 8 distinct bank groups.
+// Row `row`'s xor key for the 64-byte-row tile: ((row >> 1) & 3) ^ ((row >> 3) & 1). A fragment
+// read serves 8 or 16 consecutive rows of one logical chunk per cycle; with this key those rows
+// land on distinct 16-byte slots of a 128- or 256-byte bank span.
+__device__ __forceinline__ uint32_t fwd_key(uint32_t row) { return ((row >> 1) & 3u) ^ ((row >> 3) & 1u); }
+
+// Byte offset of 16-byte chunk `chunk` (0..3) of row `row` in a 64-byte-row tile.
 __device__ __forceinline__ uint32_t fwd_off(uint32_t row, uint32_t chunk) {
-    return row * 64u + ((chunk ^ ((row >> 1) & 3u)) << 4);
+    return row * 64u + ((chunk ^ fwd_key(row)) << 4);
 }
 
 // A direct-to-LDS load writes lane L's 16 bytes at LDS byte 16 L from the instruction's base, so
 // each wave fills 1 KB blocks: lane L of block q lands in row 16 q + L / 4, physical chunk L % 4,
-// which must hold logical chunk (L % 4) ^ ((row >> 1) & 3) = (L % 4) ^ ((L >> 3) & 3). Each
-// thread's byte offsets at k0 = 0 are fixed for the whole tile.
+// which must hold logical chunk (L % 4) ^ fwd_key(row). The key depends on row bits 1-3 only,
+// i.e. on L alone, so one k offset serves all four blocks. Each thread's byte offsets at k0 = 0
+// are fixed for the whole tile.
 struct FwdDma {
     uint32_t lane_off[4];
     uint32_t kk;  // k offset of this lane's chunk inside a step
     __device__ __forceinline__ void init(int64_t K, int wave, int lane) {
-        kk = (uint32_t)(((lane & 3) ^ ((lane >> 3) & 3)) * 8);
+        kk = (uint32_t)(((uint32_t)(lane & 3) ^ fwd_key((uint32_t)lane >> 2)) * 8);
 #pragma unroll
         for (int i = 0; i < 4; i++) {
             const uint32_t row = (wave * 4 + i) * 16 + (lane >> 2);
@@ -199,6 +204,13 @@ __device__ __forceinline__ void mma_step(const char *As, const char *Bs, Frags &
     mma_frags(g, acc);
 }
 
+// Workgroups are dealt to the 8 XCDs round-robin (id % 8), each XCD with its own L2. Renumbering
+// so that XCD x runs a contiguous block of tiles keeps tiles that share operand panels in one L2.
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t id, uint32_t count) {
+    const uint32_t per = count / 8u;
+    return id < per * 8u ? (id % 8u) * per + id / 8u : id;
+}
+
 // Calls f(std::integral_constant<int, 0>) ... f(<N-1>): every accumulator index is then a
 // compile-time constant, so the accumulators stay in registers.
 template <typename F, int... Is>
@@ -213,13 +225,15 @@ __device__ __forceinline__ void static_for(F &&f) {
 }  // namespace
 
 // ------------------------------------------------------------------------------------------------
+template <bool MSE>  // MSE epilogue against Y_ref, or the plain product
 __global__ void __launch_bounds__(kThreads, 1)
 fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, int64_t M, int64_t N, int64_t K,
                 const uint16_t *__restrict__ Yref, uint16_t *__restrict__ dY, float dscale,
                 double *__restrict__ colpart, int tiles_n) {
     __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
-    const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+    const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
+    const int tm = tile / tiles_n, tn = tile % tiles_n;
     const int64_t m0 = (int64_t)tm * kTile, n0 = (int64_t)tn * kTile;
 
     f32x16_t acc[4][4];
@@ -244,20 +258,26 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
         pa.issue(ra, K, s0 * kFwdStep, lsm + s0 * kFwdStageBytes, wave_u);
         pb.issue(rb, K, s0 * kFwdStep, lsm + s0 * kFwdStageBytes + kFwdOpBytes, wave_u);
     }
+    // Before the barrier of step kt, this thread's loads of steps kt and kt + 1 have landed (only
+    // step kt + 2's 8 loads may still be in flight); after it, everyone's have, so the first
+    // fragments of step kt + 1 can be read while step kt's MFMAs run, and stage (kt + 3) % 4, last
+    // read in step kt - 1, can be refilled. A bare s_barrier: __syncthreads would also wait for
+    // the loads still in flight.
+    FOCUS_WAIT_VMCNT(8);
+    asm volatile("s_barrier" ::: "memory");
+    Frags f, g;
+    load_frags_fwd(f, smem, smem + kFwdOpBytes, 0, wm, wn, lane);
     for (int64_t kt = 0; kt < nk; kt++) {
-        // this thread's 8 loads of step kt have landed (steps kt + 1, kt + 2 may still be in
-        // flight); after the barrier everyone's have, and stage (kt + 3) % 4, last read in step
-        // kt - 1, is free. A bare s_barrier: __syncthreads would also wait for the loads in flight.
-        FOCUS_WAIT_VMCNT(16);
+        FOCUS_WAIT_VMCNT(8);
         asm volatile("s_barrier" ::: "memory");
-        const int cs = (int)(kt & 3), nsg = (int)((kt + 3) & 3);
-        const char *As = smem + cs * kFwdStageBytes, *Bs = As + kFwdOpBytes;
-        Frags f, g;
-        load_frags_fwd(f, As, Bs, 0, wm, wn, lane);
+        const char *As = smem + (int)(kt & 3) * kFwdStageBytes, *Bs = As + kFwdOpBytes;
+        const char *An = smem + (int)((kt + 1) & 3) * kFwdStageBytes, *Bn = An + kFwdOpBytes;
+        const int nsg = (int)((kt + 3) & 3);
         pa.issue(ra, K, (kt + 3) * kFwdStep, lsm + nsg * kFwdStageBytes, wave_u);
         pb.issue(rb, K, (kt + 3) * kFwdStep, lsm + nsg * kFwdStageBytes + kFwdOpBytes, wave_u);
         load_frags_fwd(g, As, Bs, 1, wm, wn, lane);
         mma_frags(f, acc);
+        load_frags_fwd(f, An, Bn, 0, wm, wn, lane);
         mma_frags(g, acc);
     }
     FOCUS_WAIT_VMCNT(0);
@@ -273,12 +293,12 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
     // rows m and m + 4 of one column group use different banks.
     const int lr = lane & 31, lh = lane >> 5;
     const uint32_t N32 = (uint32_t)N;  // offsets are below 256 * N * 2 < 2^31 (checked when chosen)
-    const __amdgpu_buffer_rsrc_t rs_y = make_rsrc(Yref + m0 * N, Yref ? (M - m0) * N * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rs_y = make_rsrc(Yref + m0 * N, MSE ? (M - m0) * N * 2 : 0);
     const __amdgpu_buffer_rsrc_t rs_d = make_rsrc(dY + m0 * N, (M - m0) * N * 2);
     auto tile_off = [](uint32_t row, uint32_t chunk) {  // chunk: 8 columns (16 bytes), 0..31
         return row * 512u + ((chunk ^ (((row >> 2) & 1u) << 2)) << 4);
     };
-    if (Yref) {
+    if (MSE) {
 #pragma unroll 8
         for (int i = 0; i < 32; i++) {
             const uint32_t cidx = t + 256 * i, row = cidx >> 5, chunk = cidx & 31;
@@ -288,22 +308,33 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
         }
         __syncthreads();
     }
+    // Per 32 x 32 accumulator tile: the 16 Y values are read first, then the 16 dY values are
+    // written (the compiler cannot reorder LDS reads across the writes, so batching them keeps one
+    // wait per tile instead of one per element). D^2 is summed per tile in fp32 (16 terms), then
+    // into the column's fp64 total.
     double csum[4] = {0.0, 0.0, 0.0, 0.0};
     static_for<4>([&](auto i) {
         static_for<4>([&](auto j) {
             const uint32_t n = wn * 128 + j * 32 + lr;  // column in the tile
+            uint16_t *p[16];
+            float y[16];
             static_for<16>([&](auto r) {
                 const uint32_t m = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);  // row in the tile
-                uint16_t *p = reinterpret_cast<uint16_t *>(smem + tile_off(m, n >> 3)) + (n & 7);
+                p[r] = reinterpret_cast<uint16_t *>(smem + tile_off(m, n >> 3)) + (n & 7);
+                y[r] = MSE ? __uint_as_float((uint32_t)*p[r] << 16) : 0.0f;
+            });
+            float sq = 0.0f;
+            static_for<16>([&](auto r) {
                 const float v = acc[i][j][(int)r];
-                if (Yref) {
-                    const float d = v - __uint_as_float((uint32_t)*p << 16);
-                    *p = (uint16_t)f32_to_bf16_bits(d * dscale);
-                    csum[j] += (double)d * (double)d;
+                if (MSE) {
+                    const float d = v - y[r];
+                    *p[r] = (uint16_t)f32_to_bf16_bits(d * dscale);
+                    sq = __builtin_fmaf(d, d, sq);
                 } else {
-                    *p = (uint16_t)f32_to_bf16_bits(v);
+                    *p[r] = (uint16_t)f32_to_bf16_bits(v);
                 }
             });
+            csum[j] += (double)sq;
         });
     });
     __syncthreads();
@@ -317,7 +348,7 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
         const u32x4 w = {v.x, v.y, v.z, v.w};
         __builtin_amdgcn_raw_buffer_store_b128(w, rs_d, (int)off, 0, 0);
     }
-    if (!Yref) return;
+    if (!MSE) return;
 #pragma unroll
     for (int j = 0; j < 4; j++) csum[j] += __shfl_xor(csum[j], 32, 64);  // lanes l and l ^ 32 share a column
     double *red = reinterpret_cast<double *>(smem);                     // [2 waves along M][256 columns]
@@ -495,9 +526,12 @@ bool mfma_bwd_supported(int64_t M, int64_t N, int64_t K) {
 hipError_t launch_fwd_mfma(const void *X, const void *W, int64_t M, int64_t N, int64_t K, const void *Yref, void *dY,
                            float dscale, double *colpart, hipStream_t st) {
     const int tiles_m = (int)((M + kTile - 1) / kTile), tiles_n = (int)((N + kTile - 1) / kTile);
-    fwd_mfma_kernel<<<dim3((unsigned)tiles_m * tiles_n), kThreads, 0, st>>>(
-        static_cast<const uint16_t *>(X), static_cast<const uint16_t *>(W), M, N, K,
-        static_cast<const uint16_t *>(Yref), static_cast<uint16_t *>(dY), dscale, colpart, tiles_n);
+    const dim3 grid((unsigned)tiles_m * tiles_n);
+    const uint16_t *x = static_cast<const uint16_t *>(X), *w = static_cast<const uint16_t *>(W);
+    const uint16_t *y = static_cast<const uint16_t *>(Yref);
+    uint16_t *d = static_cast<uint16_t *>(dY);
+    if (Yref) fwd_mfma_kernel<true><<<grid, kThreads, 0, st>>>(x, w, M, N, K, y, d, dscale, colpart, tiles_n);
+    else fwd_mfma_kernel<false><<<grid, kThreads, 0, st>>>(x, w, M, N, K, y, d, dscale, colpart, tiles_n);
     return hipGetLastError();
 }
 
