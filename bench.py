@@ -33,6 +33,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=16384)
     p.add_argument("--cpu-sample-rows", type=int, default=128)
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="run an untimed 1 GiB device copy first (a known-size reference for HBM counters)")
     return p.parse_args()
 
 
@@ -93,6 +95,12 @@ def main():
     from paper_2608_01847_amd import focus as F
     from paper_2608_01847_amd import synth
 
+    if args.copy_calibration:
+        src = torch.ones(1 << 29, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     w = synth.WORKLOADS[args.workload]
     if args.tokens:
         w = synth.scaled(w, M=args.tokens, name=w.name)

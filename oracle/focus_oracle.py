@@ -261,9 +261,9 @@ class LayerResult:
     loss_part: float       # sum(col_sq) / (M N); the full loss when rows covers every n
 
 
-def recon_layer(X_op: np.ndarray, W_op: np.ndarray, Y_ref: np.ndarray, fq: WeightFQ, fmt: int,
+def recon_layer(X_op: np.ndarray, W_op: np.ndarray, Y_ref, fq: WeightFQ, fmt: int,
                 sb: int, alpha: float = 1.0, rows=None, keep_dy: bool = False,
-                chunk: int = 8192) -> LayerResult:
+                chunk: int = 8192, y_ref_cols: np.ndarray | None = None) -> LayerResult:
     """One layer of the scale-learning step, computed for the output features ``rows``.
 
     X_op [M][K] and W_op [N][K] are the GEMM operands (fp32 arrays holding the exact operand
@@ -276,7 +276,8 @@ def recon_layer(X_op: np.ndarray, W_op: np.ndarray, Y_ref: np.ndarray, fq: Weigh
         grad_S_dq   = sum over the block of G_j dW_hat/dS_dq
         grad S_fp   = grad_S_dq (MXFP4, STE through Q_E8M0); alpha * grad_S_dq (NVFP4, Delta_fp)
     Loss and gradients for output feature n depend only on row n of W and column n of Y_ref, so a
-    subset of rows is exact for those rows.
+    subset of rows is exact for those rows. `y_ref_cols` may carry Y_ref already restricted to the
+    columns `rows` ([M][|rows|]); Y_ref is then not used.
     """
     M, K = X_op.shape
     N = W_op.shape[0]
@@ -291,7 +292,8 @@ def recon_layer(X_op: np.ndarray, W_op: np.ndarray, Y_ref: np.ndarray, fq: Weigh
     for t0 in range(0, M, chunk):
         Xc = X_op[t0:t0 + chunk].astype(np.float64)
         Yc = Xc @ WR.T
-        Dc = Yc - Y_ref[t0:t0 + chunk][:, rows].astype(np.float64)
+        Yr = y_ref_cols[t0:t0 + chunk] if y_ref_cols is not None else Y_ref[t0:t0 + chunk][:, rows]
+        Dc = Yc - Yr.astype(np.float64)
         col_sq += (Dc * Dc).sum(axis=0)
         Dc *= scale
         if keep_dy:
