@@ -211,6 +211,19 @@ __device__ __forceinline__ uint32_t xcd_tile(uint32_t id, uint32_t count) {
     return id < per * 8u ? (id % 8u) * per + id / 8u : id;
 }
 
+// Position t of a rows x cols tile grid in grouped order: groups of kGroupRows row-tiles are
+// walked column by column, so the ~32 workgroups an XCD runs at once cover about 4 x 8 tiles and
+// share 4 row panels and 8 column panels instead of 1 and 32.
+constexpr uint32_t kGroupRows = 4;
+__device__ __forceinline__ void grouped_tile(uint32_t t, uint32_t rows, uint32_t cols, uint32_t &r, uint32_t &c) {
+    const uint32_t per_group = kGroupRows * cols;
+    const uint32_t first = (t / per_group) * kGroupRows;
+    const uint32_t in_group = rows - first < kGroupRows ? rows - first : kGroupRows;
+    const uint32_t u = t % per_group;
+    r = first + u % in_group;
+    c = u / in_group;
+}
+
 // Calls f(std::integral_constant<int, 0>) ... f(<N-1>): every accumulator index is then a
 // compile-time constant, so the accumulators stay in registers.
 template <typename F, int... Is>
@@ -232,8 +245,8 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
                 double *__restrict__ colpart, int tiles_n) {
     __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
-    const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
-    const int tm = tile / tiles_n, tn = tile % tiles_n;
+    uint32_t tm, tn;
+    grouped_tile(xcd_tile(blockIdx.x, gridDim.x), gridDim.x / tiles_n, tiles_n, tm, tn);
     const int64_t m0 = (int64_t)tm * kTile, n0 = (int64_t)tn * kTile;
 
     f32x16_t acc[4][4];
@@ -243,8 +256,10 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
 #pragma unroll
         for (int j = 0; j < 4; j++) acc[i][j] = zero;
 
-    // Four LDS stages of 32 of K; the loads of steps kt + 1 .. kt + 3 are in flight while step kt
-    // is computed. Loads past the end of K read zeros into stages that are never read.
+    // Four LDS stages of 32 of K. Load "slot" j fills stage j % 4: for j < nk it is step j of the
+    // operands; slots nk .. nk + 3 bring the four 64-row quarters of the Y_ref tile (zeros in the
+    // plain mode), so the epilogue's input arrives while the last steps' MFMAs run. Every slot is
+    // 8 loads per thread, which is what the vmcnt waits below count on.
     lds_char *const lsm = (lds_char *)smem;
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
     FwdDma pa, pb;
@@ -252,14 +267,40 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
     pb.init(K, wave_u, lane);
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(X + m0 * K, (M - m0) * K * 2);
     const __amdgpu_buffer_rsrc_t rb = make_rsrc(W + n0 * K, (N - n0) * K * 2);
+    const __amdgpu_buffer_rsrc_t rs_y = make_rsrc(MSE ? Yref + m0 * N : dY, MSE ? (M - m0) * N * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rs_d = make_rsrc(dY + m0 * N, (M - m0) * N * 2);
+    const uint32_t N32 = (uint32_t)N;  // offsets are below 256 * N * 2 < 2^31 (checked when chosen)
     const int64_t nk = (K + kFwdStep - 1) / kFwdStep;
+    // Quarter q of the output tile holds tile rows q*32 + 0..31 and 128 + q*32 + 0..31 (local rows
+    // 0..63), i.e. accumulator block i == q of every wave. In LDS a quarter is 64 rows of 512 bytes;
+    // the two 64-byte halves of each 128-byte span are swapped on rows with bit 2 set, so the lanes
+    // reading rows r and r + 4 of one column group use different banks.
+    auto q_row = [](uint32_t rl, uint32_t q) { return (rl >> 5) * 128u + q * 32u + (rl & 31u); };
+    auto q_off = [](uint32_t rl, uint32_t chunk) { return rl * 512u + ((chunk ^ (((rl >> 2) & 1u) << 2)) << 4); };
+    auto issue_slot = [&](int64_t j) {
+        lds_char *st = lsm + (int)(j & 3) * kFwdStageBytes;
+        if (j < nk) {
+            pa.issue(ra, K, j * kFwdStep, st, wave_u);
+            pb.issue(rb, K, j * kFwdStep, st + kFwdOpBytes, wave_u);
+        } else {
+            // 32 one-KB blocks of two rows each; this wave fills blocks 8 wave .. 8 wave + 7, lane L
+            // of block b lands in local row 2 b + L / 32, physical chunk L % 32
+            const uint32_t q = (uint32_t)((j - nk) & 3);
 #pragma unroll
-    for (int s0 = 0; s0 < kFwdStages - 1; s0++) {
-        pa.issue(ra, K, s0 * kFwdStep, lsm + s0 * kFwdStageBytes, wave_u);
-        pb.issue(rb, K, s0 * kFwdStep, lsm + s0 * kFwdStageBytes + kFwdOpBytes, wave_u);
-    }
+            for (int i = 0; i < 8; i++) {
+                const uint32_t blk = wave_u * 8 + i, rl = 2 * blk + (lane >> 5);
+                const uint32_t chunk = (uint32_t)(lane & 31) ^ (((rl >> 2) & 1u) << 2);
+                const uint32_t col = (uint32_t)n0 + chunk * 8;
+                const uint32_t bad = ((uint32_t)((int32_t)N32 - 1 - (int32_t)col) >> 31) << 31;  // col >= N
+                const uint32_t off = ((q_row(rl, q) * N32 + col) * 2u) | bad;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_y, st + blk * 1024, 16, (int)off, 0, 0, 0);
+            }
+        }
+    };
+#pragma unroll
+    for (int s0 = 0; s0 < kFwdStages - 1; s0++) issue_slot(s0);
     // Before the barrier of step kt, this thread's loads of steps kt and kt + 1 have landed (only
-    // step kt + 2's 8 loads may still be in flight); after it, everyone's have, so the first
+    // slot kt + 2's 8 loads may still be in flight); after it, everyone's have, so the first
     // fragments of step kt + 1 can be read while step kt's MFMAs run, and stage (kt + 3) % 4, last
     // read in step kt - 1, can be refilled. A bare s_barrier: __syncthreads would also wait for
     // the loads still in flight.
@@ -272,60 +313,44 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
         asm volatile("s_barrier" ::: "memory");
         const char *As = smem + (int)(kt & 3) * kFwdStageBytes, *Bs = As + kFwdOpBytes;
         const char *An = smem + (int)((kt + 1) & 3) * kFwdStageBytes, *Bn = An + kFwdOpBytes;
-        const int nsg = (int)((kt + 3) & 3);
-        pa.issue(ra, K, (kt + 3) * kFwdStep, lsm + nsg * kFwdStageBytes, wave_u);
-        pb.issue(rb, K, (kt + 3) * kFwdStep, lsm + nsg * kFwdStageBytes + kFwdOpBytes, wave_u);
+        issue_slot(kt + 3);
         load_frags_fwd(g, As, Bs, 1, wm, wn, lane);
         mma_frags(f, acc);
         load_frags_fwd(f, An, Bn, 0, wm, wn, lane);
         mma_frags(g, acc);
     }
-    FOCUS_WAIT_VMCNT(0);
-    __syncthreads();
+    // the last quarter goes into the stage of the last step, once every wave is done with it
+    asm volatile("s_barrier" ::: "memory");
+    issue_slot(nk + 3);
 
-    // ---- epilogue: D = Y_hat - Y_ref, dY = D * dscale, column sums of D^2 ----
-    // The 256 x 256 bf16 tile of Y_ref is brought into LDS (free after the main loop) with
-    // coalesced 16-byte loads; each lane then reads its accumulators' Y values from LDS, writes dY
-    // over them, and the dY tile leaves with coalesced 16-byte stores. Rows past M and columns past
-    // N hold zero accumulators and read Y_ref as zero, so they add nothing to the column sums, and
-    // their stores fall outside the resource and are dropped. Tile rows are 512 bytes; the two
-    // 64-byte halves of each 128-byte span are swapped on rows with bit 2 set, so the lanes reading
-    // rows m and m + 4 of one column group use different banks.
+    // ---- epilogue, one quarter at a time: D = Y_hat - Y_ref, dY = D * dscale, column sums of D^2
+    // Each lane reads its 16 Y values of an accumulator tile from LDS, then writes the 16 dY values
+    // over them (batched: the compiler cannot move LDS reads across the writes); the quarter then
+    // leaves with coalesced 16-byte stores, which drain while the next quarter is processed. Rows
+    // past M and columns past N hold zero accumulators and read Y_ref as zero, so they add nothing
+    // to the column sums; their stores fall outside the resource and are dropped. D^2 is summed per
+    // accumulator tile in fp32 (16 terms), then into the column's fp64 total.
     const int lr = lane & 31, lh = lane >> 5;
-    const uint32_t N32 = (uint32_t)N;  // offsets are below 256 * N * 2 < 2^31 (checked when chosen)
-    const __amdgpu_buffer_rsrc_t rs_y = make_rsrc(Yref + m0 * N, MSE ? (M - m0) * N * 2 : 0);
-    const __amdgpu_buffer_rsrc_t rs_d = make_rsrc(dY + m0 * N, (M - m0) * N * 2);
-    auto tile_off = [](uint32_t row, uint32_t chunk) {  // chunk: 8 columns (16 bytes), 0..31
-        return row * 512u + ((chunk ^ (((row >> 2) & 1u) << 2)) << 4);
-    };
-    if (MSE) {
-#pragma unroll 8
-        for (int i = 0; i < 32; i++) {
-            const uint32_t cidx = t + 256 * i, row = cidx >> 5, chunk = cidx & 31;
-            const int64_t col = n0 + chunk * 8;
-            const uint32_t off = col < N ? (row * N32 + (uint32_t)col) * 2u : kOutOfRange;
-            *reinterpret_cast<uint4 *>(smem + tile_off(row, chunk)) = buffer_load16(rs_y, off);
-        }
-        __syncthreads();
-    }
-    // Per 32 x 32 accumulator tile: the 16 Y values are read first, then the 16 dY values are
-    // written (the compiler cannot reorder LDS reads across the writes, so batching them keeps one
-    // wait per tile instead of one per element). D^2 is summed per tile in fp32 (16 terms), then
-    // into the column's fp64 total.
     double csum[4] = {0.0, 0.0, 0.0, 0.0};
-    static_for<4>([&](auto i) {
+    static_for<4>([&](auto q) {
+        if (q == 0) {
+            FOCUS_WAIT_VMCNT(24);  // this thread's loads of quarter 0 have landed
+            asm volatile("s_barrier" ::: "memory");
+        }
+        lds_char *qb = lsm + (int)((nk + q) & 3) * kFwdStageBytes;
         static_for<4>([&](auto j) {
             const uint32_t n = wn * 128 + j * 32 + lr;  // column in the tile
-            uint16_t *p[16];
+            typedef __attribute__((address_space(3))) uint16_t lds_u16;
+            lds_u16 *p[16];
             float y[16];
             static_for<16>([&](auto r) {
-                const uint32_t m = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);  // row in the tile
-                p[r] = reinterpret_cast<uint16_t *>(smem + tile_off(m, n >> 3)) + (n & 7);
+                const uint32_t rl = wm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);  // local row of the quarter
+                p[r] = reinterpret_cast<lds_u16 *>(qb + q_off(rl, n >> 3)) + (n & 7);
                 y[r] = MSE ? __uint_as_float((uint32_t)*p[r] << 16) : 0.0f;
             });
             float sq = 0.0f;
             static_for<16>([&](auto r) {
-                const float v = acc[i][j][(int)r];
+                const float v = acc[q][j][(int)r];
                 if (MSE) {
                     const float d = v - y[r];
                     *p[r] = (uint16_t)f32_to_bf16_bits(d * dscale);
@@ -336,23 +361,26 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
             });
             csum[j] += (double)sq;
         });
+        // After quarter 0 every thread waits for its remaining loads (no store has been issued
+        // yet, so the count is exact); the barrier then makes all four quarters visible.
+        if (q == 0) FOCUS_WAIT_VMCNT(0);
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            const uint32_t cidx = t + 256 * i, rl = cidx >> 5, chunk = cidx & 31;
+            const uint32_t col = (uint32_t)n0 + chunk * 8;
+            const uint32_t bad = ((uint32_t)((int32_t)N32 - 1 - (int32_t)col) >> 31) << 31;  // col >= N
+            const uint32_t off = ((q_row(rl, q) * N32 + col) * 2u) | bad;
+            typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+            const u32x4 w = *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(qb + q_off(rl, chunk));
+            __builtin_amdgcn_raw_buffer_store_b128(w, rs_d, (int)off, 0, 0);
+        }
     });
-    __syncthreads();
-#pragma unroll 8
-    for (int i = 0; i < 32; i++) {
-        const uint32_t cidx = t + 256 * i, row = cidx >> 5, chunk = cidx & 31;
-        const int64_t col = n0 + chunk * 8;
-        const uint32_t off = col < N ? (row * N32 + (uint32_t)col) * 2u : kOutOfRange;
-        const uint4 v = *reinterpret_cast<const uint4 *>(smem + tile_off(row, chunk));
-        typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-        const u32x4 w = {v.x, v.y, v.z, v.w};
-        __builtin_amdgcn_raw_buffer_store_b128(w, rs_d, (int)off, 0, 0);
-    }
     if (!MSE) return;
 #pragma unroll
     for (int j = 0; j < 4; j++) csum[j] += __shfl_xor(csum[j], 32, 64);  // lanes l and l ^ 32 share a column
     double *red = reinterpret_cast<double *>(smem);                     // [2 waves along M][256 columns]
-    __syncthreads();                                                    // the dY tile has left LDS
+    __syncthreads();                                                    // every quarter has left LDS
     if (lh == 0) {
 #pragma unroll
         for (int j = 0; j < 4; j++) red[wm * kTile + wn * 128 + j * 32 + lr] = csum[j];
@@ -370,9 +398,13 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
                 float *__restrict__ part_s, float *__restrict__ part_c, uint32_t *flag, int tiles_n) {
     __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
-    const int tk = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+    // linear id -> (split, tile): splits outermost, tiles of one split in grouped order, so that an
+    // XCD's concurrent workgroups share the operand panels of one token range
+    const uint32_t id = xcd_tile(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
+    uint32_t tk, tn;
+    grouped_tile(id % gridDim.x, gridDim.x / tiles_n, tiles_n, tk, tn);
     const int64_t k0 = (int64_t)tk * kTile, n0 = (int64_t)tn * kTile;
-    const int64_t split = blockIdx.y;
+    const int64_t split = id / gridDim.x;
     const int64_t t_begin = split * chunk, t_end = std::min<int64_t>(M, t_begin + chunk);
 
     f32x16_t acc[4][4];
