@@ -140,17 +140,17 @@ struct FwdDma {
             lane_off[i] = (row * (uint32_t)K + kk) * 2u;
         }
     }
-    // Issues the 4 loads of this wave for the step starting at k0. Chunks at or past K get bit 31
-    // of the offset set: out of range, they read as zeros (an arithmetic mask, not a branch).
-    __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, int64_t K, int64_t k0, lds_char *dst,
-                                          int wave) const {
+    // Offset bits of the step starting at k0: chunks at or past K get bit 31 set, so they are out
+    // of range and read as zeros (an arithmetic mask, not a branch).
+    __device__ __forceinline__ uint32_t step_bad(int64_t K, int64_t k0) const {
         const int32_t lim = (int32_t)(K - k0);
-        const uint32_t bad = ((uint32_t)(lim - 1 - (int32_t)kk) >> 31) << 31;
-        const uint32_t base = (uint32_t)k0 * 2u;
-#pragma unroll
-        for (int i = 0; i < 4; i++)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst + (wave * 4 + i) * 1024, 16,
-                                                     (int)((lane_off[i] + base) | bad), 0, 0, 0);
+        return ((uint32_t)(lim - 1 - (int32_t)kk) >> 31) << 31;
+    }
+    // Load i (0..3) of this wave for the step starting at k0 (base = 2 k0).
+    __device__ __forceinline__ void issue_one(__amdgpu_buffer_rsrc_t rs, uint32_t base, uint32_t bad,
+                                              lds_char *dst, int wave, int i) const {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst + (wave * 4 + i) * 1024, 16,
+                                                 (int)((lane_off[i] + base) | bad), 0, 0, 0);
     }
 };
 
@@ -262,9 +262,8 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
     // 8 loads per thread, which is what the vmcnt waits below count on.
     lds_char *const lsm = (lds_char *)smem;
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-    FwdDma pa, pb;
-    pa.init(K, wave_u, lane);
-    pb.init(K, wave_u, lane);
+    FwdDma dma;  // X and W panels have the same row length K, so one set of offsets serves both
+    dma.init(K, wave_u, lane);
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(X + m0 * K, (M - m0) * K * 2);
     const __amdgpu_buffer_rsrc_t rb = make_rsrc(W + n0 * K, (N - n0) * K * 2);
     const __amdgpu_buffer_rsrc_t rs_y = make_rsrc(MSE ? Yref + m0 * N : dY, MSE ? (M - m0) * N * 2 : 0);
@@ -277,24 +276,33 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
     // reading rows r and r + 4 of one column group use different banks.
     auto q_row = [](uint32_t rl, uint32_t q) { return (rl >> 5) * 128u + q * 32u + (rl & 31u); };
     auto q_off = [](uint32_t rl, uint32_t chunk) { return rl * 512u + ((chunk ^ (((rl >> 2) & 1u) << 2)) << 4); };
-    auto issue_slot = [&](int64_t j) {
+    // Load i (0..7) of slot j: loads 0-3 bring X rows, 4-7 W rows of an operand step; a Y_ref
+    // quarter is 32 one-KB blocks of two rows each, this wave filling blocks 8 wave .. 8 wave + 7
+    // (lane L of block b lands in local row 2 b + L / 32, physical chunk L % 32).
+    auto issue_op = [&](int64_t j, int i) {
         lds_char *st = lsm + (int)(j & 3) * kFwdStageBytes;
+        const int64_t k0 = j * kFwdStep;
+        const uint32_t base = (uint32_t)k0 * 2u, bad = dma.step_bad(K, k0);
+        if (i < 4) dma.issue_one(ra, base, bad, st, wave_u, i);
+        else dma.issue_one(rb, base, bad, st + kFwdOpBytes, wave_u, i - 4);
+    };
+    auto issue_y = [&](int64_t j, int i) {
+        lds_char *st = lsm + (int)(j & 3) * kFwdStageBytes;
+        const uint32_t q = (uint32_t)((j - nk) & 3);
+        const uint32_t blk = wave_u * 8 + i, rl = 2 * blk + (lane >> 5);
+        const uint32_t chunk = (uint32_t)(lane & 31) ^ (((rl >> 2) & 1u) << 2);
+        const uint32_t col = (uint32_t)n0 + chunk * 8;
+        const uint32_t bad = ((uint32_t)((int32_t)N32 - 1 - (int32_t)col) >> 31) << 31;  // col >= N
+        const uint32_t off = ((q_row(rl, q) * N32 + col) * 2u) | bad;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_y, st + blk * 1024, 16, (int)off, 0, 0, 0);
+    };
+    auto issue_slot = [&](int64_t j) {
         if (j < nk) {
-            pa.issue(ra, K, j * kFwdStep, st, wave_u);
-            pb.issue(rb, K, j * kFwdStep, st + kFwdOpBytes, wave_u);
-        } else {
-            // 32 one-KB blocks of two rows each; this wave fills blocks 8 wave .. 8 wave + 7, lane L
-            // of block b lands in local row 2 b + L / 32, physical chunk L % 32
-            const uint32_t q = (uint32_t)((j - nk) & 3);
 #pragma unroll
-            for (int i = 0; i < 8; i++) {
-                const uint32_t blk = wave_u * 8 + i, rl = 2 * blk + (lane >> 5);
-                const uint32_t chunk = (uint32_t)(lane & 31) ^ (((rl >> 2) & 1u) << 2);
-                const uint32_t col = (uint32_t)n0 + chunk * 8;
-                const uint32_t bad = ((uint32_t)((int32_t)N32 - 1 - (int32_t)col) >> 31) << 31;  // col >= N
-                const uint32_t off = ((q_row(rl, q) * N32 + col) * 2u) | bad;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_y, st + blk * 1024, 16, (int)off, 0, 0, 0);
-            }
+            for (int i = 0; i < 8; i++) issue_op(j, i);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; i++) issue_y(j, i);
         }
     };
 #pragma unroll
@@ -308,20 +316,36 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
     asm volatile("s_barrier" ::: "memory");
     Frags f, g;
     load_frags_fwd(f, smem, smem + kFwdOpBytes, 0, wm, wn, lane);
-    for (int64_t kt = 0; kt < nk; kt++) {
+    // One step. The 8 loads of slot kt + 3 go out one after every second MFMA of the first half:
+    // issued back to back they would fill the texture unit's queue, and a wave stalled on a full
+    // queue issues no MFMA. The scheduling barriers keep the compiler from regrouping them.
+    auto step = [&](int64_t kt, auto y_slot) {
         FOCUS_WAIT_VMCNT(8);
         asm volatile("s_barrier" ::: "memory");
         const char *As = smem + (int)(kt & 3) * kFwdStageBytes, *Bs = As + kFwdOpBytes;
         const char *An = smem + (int)((kt + 1) & 3) * kFwdStageBytes, *Bn = An + kFwdOpBytes;
-        issue_slot(kt + 3);
         load_frags_fwd(g, As, Bs, 1, wm, wn, lane);
-        mma_frags(f, acc);
+        static_for<16>([&](auto idx) {
+            constexpr int i = idx / 4, jj = idx % 4;
+            acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[jj], acc[i][jj], 0, 0, 0);
+            if constexpr (idx % 2 == 1) {
+                __builtin_amdgcn_sched_barrier(0);
+                if constexpr (decltype(y_slot)::value) issue_y(kt + 3, idx / 2);
+                else issue_op(kt + 3, idx / 2);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        });
         load_frags_fwd(f, An, Bn, 0, wm, wn, lane);
         mma_frags(g, acc);
-    }
+    };
+    const int64_t n_op = nk > 3 ? nk - 3 : 0;  // steps whose slot kt + 3 is an operand step
+    int64_t kt = 0;
+    for (; kt < n_op; kt++) step(kt, std::false_type{});
+    for (; kt < nk; kt++) step(kt, std::true_type{});
     // the last quarter goes into the stage of the last step, once every wave is done with it
     asm volatile("s_barrier" ::: "memory");
-    issue_slot(nk + 3);
+#pragma unroll
+    for (int i = 0; i < 8; i++) issue_y(nk + 3, i);
 
     // ---- epilogue, one quarter at a time: D = Y_hat - Y_ref, dY = D * dscale, column sums of D^2
     // Each lane reads its 16 Y values of an accumulator tile from LDS, then writes the 16 dY values
