@@ -34,29 +34,14 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 namespace {
 
 constexpr int kTile = 256;            // output tile edge
-constexpr int kStep = 64;             // reduction step
 constexpr int kThreads = 256;         // four waves
-constexpr int kOpBytes = kTile * 128; // one operand tile in LDS: 256 rows x 64 bf16
-constexpr int kStageBytes = 2 * kOpBytes;
-constexpr int kLdsBytes = 2 * kStageBytes;
+constexpr int kLdsBytes = 128 * 1024; // four 32 KB stages
 
 static_assert(kTile == kMfmaTileM && kTile == kMfmaTileN && kTile == kMfmaTileK, "tile geometry");
-static_assert(kStep == kMfmaTokenStep, "token step");
-
-// Byte offset of 16-byte chunk `chunk` (0..7) of LDS tile row `row`. The chunk is xor-ed with the
-// row's bits 0-2 and 3-5: the fragment reads (8 consecutive rows, one chunk) and the transposed
-// stores (rows 8 apart, one chunk) then each touch 8 distinct chunk slots of a 128-byte row.
-__device__ __forceinline__ uint32_t lds_off(uint32_t row, uint32_t chunk) {
-    return row * 128u + ((chunk ^ (row & 7u) ^ ((row >> 3) & 7u)) << 4);
-}
-
-__device__ __forceinline__ uint32_t word_of(const uint4 &v, int p) {
-    return p == 0 ? v.x : p == 1 ? v.y : p == 2 ? v.z : v.w;
-}
 
 // Raw buffer resources: a load whose offset is at or past num_records returns zeros and a store
-// there is dropped, so bounds are handled by the hardware range check instead of branches.
-constexpr uint32_t kOutOfRange = 0x80000000u;
+// there is dropped, so bounds are handled by the hardware range check instead of branches (an
+// offset with bit 31 set is always past it, since num_records is kept below 2^31).
 constexpr int kRsrcWord3 = 0x00020000;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, int64_t bytes) {
@@ -64,43 +49,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, in
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)n, kRsrcWord3);
 }
 
-__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
-    return make_uint4(v.x, v.y, v.z, v.w);
-}
 
-// 64 x 256 tile of a row-major [T][C] bf16 operand (reduction rows t0.., columns c0..), stored
-// transposed as 256 LDS rows of 64 reduction values. Thread t loads reduction rows
-// 8 (t >> 5) + 0..7 of columns 8 (t & 31) + 0..7 and writes column j of that block as LDS row
-// 8 (t & 31) + j, chunk t >> 5. Rows at or past t_end and columns past C read as zero (C % 8 == 0).
-// The resource starts at row t0, so offsets stay below 64 * C * 2 bytes.
-struct TransposedTile {
-    uint4 v[8];
-    __device__ __forceinline__ void load(const uint16_t *__restrict__ base, int64_t t_end, int64_t C, int64_t t0,
-                                         int64_t c0, int t) {
-        const __amdgpu_buffer_rsrc_t rs = make_rsrc(base + t0 * C, (t_end - t0) * C * 2);
-        const int64_t col = c0 + (t & 31) * 8;
-#pragma unroll
-        for (int rr = 0; rr < 8; rr++) {
-            const uint32_t tt = (t >> 5) * 8 + rr;
-            v[rr] = buffer_load16(rs, col < C ? (uint32_t)((tt * C + col) * 2) : kOutOfRange);
-        }
-    }
-    __device__ __forceinline__ void store(char *lds, int t) const {
-#pragma unroll
-        for (int j = 0; j < 8; j++) {
-            const int p = j >> 1;
-            uint32_t w[4];
-#pragma unroll
-            for (int q = 0; q < 4; q++) {
-                const uint32_t x = word_of(v[2 * q], p), y = word_of(v[2 * q + 1], p);
-                w[q] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
-            }
-            *reinterpret_cast<uint4 *>(lds + lds_off((t & 31) * 8 + j, t >> 5)) = make_uint4(w[0], w[1], w[2], w[3]);
-        }
-    }
-};
 
 // ---- forward operand staging: direct-to-LDS buffer loads ---------------------------------------
 // The forward operands are K-contiguous, so their tiles go from HBM / L2 straight into LDS with
@@ -154,6 +103,50 @@ struct FwdDma {
     }
 };
 
+// Backward operands are token-major tiles, [32 tokens][256 columns] of bf16, staged as they lie
+// in memory and transposed by the fragment reads. The 16-byte chunk index of a row is xor-ed with
+// 4 (row & 3): a transposing read touches 4 rows x 64 contiguous bytes per 32 lanes, which then
+// fall on 256 distinct bytes.
+constexpr int kBwdStep = 32;                          // tokens per step
+constexpr int kBwdRowBytes = kTile * 2;               // 256 columns of bf16
+constexpr int kBwdOpBytes = kBwdStep * kBwdRowBytes;  // 16 KB
+constexpr int kBwdStageBytes = 2 * kBwdOpBytes;
+constexpr int kBwdStages = 4;
+static_assert(kBwdStages * kBwdStageBytes <= kLdsBytes, "backward stages fit the LDS allocation");
+static_assert(kMfmaTokenStep % kBwdStep == 0, "token ranges of a split are whole steps");
+
+__device__ __forceinline__ uint32_t bwd_off(uint32_t r, uint32_t c) {
+    return r * (uint32_t)kBwdRowBytes + (((c >> 3) ^ ((r & 3u) << 2)) << 4) + (c & 7u) * 2u;
+}
+
+// Block q (1 KB) of a backward tile holds token rows 2 q and 2 q + 1: lane L lands in row
+// 2 q + L / 32, physical chunk L % 32, which holds logical chunk (L % 32) ^ (4 (row & 3)). A wave
+// fills blocks 4 wave .. 4 wave + 3. Offsets are relative to the step's first token row and fixed
+// for the whole tile; columns at or past C get bit 31 set and read as zeros, and rows at or past
+// the end of the token range fall outside the step's resource.
+struct BwdDma {
+    uint32_t off[4];
+    __device__ __forceinline__ void init(int64_t C, int64_t c0, int wave, int lane) {
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            const uint32_t row = 2 * (wave * 4 + i) + (lane >> 5);
+            const uint32_t chunk = (uint32_t)(lane & 31) ^ ((row & 3u) << 2);
+            const uint32_t col = (uint32_t)c0 + chunk * 8;
+            const uint32_t bad = ((uint32_t)((int32_t)C - 1 - (int32_t)col) >> 31) << 31;
+            off[i] = ((row * (uint32_t)C + col) * 2u) | bad;
+        }
+    }
+    // The resource of the step starting at token t0 of a [.., C] matrix (no rows past t_end).
+    __device__ __forceinline__ static __amdgpu_buffer_rsrc_t step_rsrc(const uint16_t *base, int64_t C, int64_t t0,
+                                                                     int64_t t_end) {
+        const int64_t rows = t_end - t0 < kBwdStep ? t_end - t0 : kBwdStep;
+        return make_rsrc(base + t0 * C, rows * C * 2);
+    }
+    __device__ __forceinline__ void issue_one(__amdgpu_buffer_rsrc_t rs, lds_char *dst, int wave, int i) const {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst + (wave * 4 + i) * 1024, 16, (int)off[i], 0, 0, 0);
+    }
+};
+
 // s_waitcnt with vmcnt <= n (n < 64) and the LDS and export counters unconstrained
 #define FOCUS_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (0x7 << 4) | (0xF << 8))
 
@@ -161,16 +154,6 @@ struct FwdDma {
 struct Frags {
     bf16x8_t a[4], b[4];
 };
-
-__device__ __forceinline__ void load_frags(Frags &f, const char *As, const char *Bs, int ks, int wm, int wn,
-                                           int lane) {
-    const uint32_t lr = lane & 31, lh = lane >> 5;
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-        f.a[i] = *reinterpret_cast<const bf16x8_t *>(As + lds_off(wm * 128 + i * 32 + lr, ks * 2 + lh));
-        f.b[i] = *reinterpret_cast<const bf16x8_t *>(Bs + lds_off(wn * 128 + i * 32 + lr, ks * 2 + lh));
-    }
-}
 
 __device__ __forceinline__ void load_frags_fwd(Frags &f, const char *As, const char *Bs, int ks, int wm, int wn,
                                                int lane) {
@@ -190,18 +173,61 @@ __device__ __forceinline__ void mma_frags(const Frags &f, f32x16_t (&acc)[4][4])
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
 }
 
-// One reduction step of 64 on the wave's 128 x 128 sub-tile. `f` holds the fragments of k16 step 0
-// on entry; the fragments of step ks + 1 are read while the 16 MFMAs of step ks run.
-__device__ __forceinline__ void mma_step(const char *As, const char *Bs, Frags &f, f32x16_t (&acc)[4][4], int wm,
-                                         int wn, int lane) {
-    Frags g;
-    load_frags(g, As, Bs, 1, wm, wn, lane);
-    mma_frags(f, acc);
-    load_frags(f, As, Bs, 2, wm, wn, lane);
-    mma_frags(g, acc);
-    load_frags(g, As, Bs, 3, wm, wn, lane);
-    mma_frags(f, acc);
-    mma_frags(g, acc);
+// Fragment of 32 operand rows (columns c .. c + 31 of a token-major tile) for the k16 step whose
+// first token row is t0: lane l needs tokens t0 + 8 (l / 32) + 0..7 of column c + l % 32. A
+// transposing read hands lane i of a 16-lane group element i % 4 of the 8-byte pieces addressed
+// by lanes 4 e + i / 4 (e = 0..3); pointing lane j at row t0' + j / 4, columns c' + 4 (j % 4) .. + 3
+// gives lane i tokens t0' .. t0' + 3 of column c' + i. Two reads (rows r and r + 4, the same
+// swizzle) cover the 8 tokens.
+//
+// The reads are issued as inline assembly: the compiler's builtin for them carries no aliasing
+// information, so the compiler would make every such read wait for all direct-to-LDS loads in
+// flight (vmcnt(0)), draining the pipeline each step. The price is that the compiler does not
+// track these reads: `tr_wait` must run before their registers are used, and it takes the
+// fragments as operands so that no consumer can be scheduled above it.
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t lds_addr(const char *p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char *)p;
+}
+
+template <int OFF>
+__device__ __forceinline__ i16x4_t ds_read_tr(uint32_t addr) {
+    i16x4_t r;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+
+// Per-lane byte offset, inside a tile, of the lower read of the fragment at columns c (step 0).
+__device__ __forceinline__ uint32_t tr_lane_off(uint32_t c, int lane) {
+    const uint32_t j = lane & 15;
+    const uint32_t cc = c + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+    const uint32_t r = 8 * (lane >> 5) + (j >> 2);
+    return bwd_off(r, cc);
+}
+
+// Fragments of k16 step KS of a stage; a_off / b_off are the lanes' tr_lane_off of the four A
+// and four B fragments (relative to the stage), base the stage's LDS address.
+template <int KS>
+__device__ __forceinline__ void load_frags_tr(Frags &f, uint32_t base, const uint32_t (&a_off)[4],
+                                              const uint32_t (&b_off)[4]) {
+    constexpr int kRow = KS * 16 * kBwdRowBytes;  // first token row of the k16 step
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const i16x4_t a_lo = ds_read_tr<kRow>(base + a_off[i]);
+        const i16x4_t a_hi = ds_read_tr<kRow + 4 * kBwdRowBytes>(base + a_off[i]);
+        const i16x4_t b_lo = ds_read_tr<kBwdOpBytes + kRow>(base + b_off[i]);
+        const i16x4_t b_hi = ds_read_tr<kBwdOpBytes + kRow + 4 * kBwdRowBytes>(base + b_off[i]);
+        const i16x4_t va[2] = {a_lo, a_hi}, vb[2] = {b_lo, b_hi};
+        f.a[i] = __builtin_bit_cast(bf16x8_t, va);
+        f.b[i] = __builtin_bit_cast(bf16x8_t, vb);
+    }
+}
+
+__device__ __forceinline__ void tr_wait(Frags &f) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(f.a[0]), "+v"(f.a[1]), "+v"(f.a[2]), "+v"(f.a[3]), "+v"(f.b[0]), "+v"(f.b[1]),
+                   "+v"(f.b[2]), "+v"(f.b[3]));
 }
 
 // Workgroups are dealt to the 8 XCDs round-robin (id % 8), each XCD with its own L2. Renumbering
@@ -438,33 +464,65 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
 #pragma unroll
         for (int j = 0; j < 4; j++) acc[i][j] = zero;
 
-    TransposedTile a, b;  // a: X_hat columns k0.. (rows of C); b: dY columns n0.. (columns of C)
-    const int64_t nk = t_end > t_begin ? (t_end - t_begin + kStep - 1) / kStep : 0;
-    if (nk > 0) {
-        a.load(X, t_end, K, t_begin, k0, t);
-        b.load(dY, t_end, N, t_begin, n0, t);
-        a.store(smem, t);
-        b.store(smem + kOpBytes, t);
+    // A = X_hat^T (rows = in features k), B = dY (columns = out features n), both staged as
+    // token-major tiles. Four stages of 32 tokens, pipelined as in the forward kernel: slot j
+    // (8 loads per thread) fills stage j % 4 with step j; slots past the token range are empty
+    // resources whose loads only write zeros, which keeps every slot at 8 loads for the waits.
+    lds_char *const lsm = (lds_char *)smem;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    BwdDma pa, pb;
+    pa.init(K, k0, wave_u, lane);
+    pb.init(N, n0, wave_u, lane);
+    const int64_t nk = t_end > t_begin ? (t_end - t_begin + kBwdStep - 1) / kBwdStep : 0;
+#pragma unroll
+    for (int s0 = 0; s0 < kBwdStages - 1; s0++) {
+        const int64_t t0 = t_begin + s0 * kBwdStep;
+        const __amdgpu_buffer_rsrc_t ra = BwdDma::step_rsrc(X, K, t0, t_end), rb = BwdDma::step_rsrc(dY, N, t0, t_end);
+        lds_char *st = lsm + s0 * kBwdStageBytes;
+#pragma unroll
+        for (int i = 0; i < 4; i++) pa.issue_one(ra, st, wave_u, i);
+#pragma unroll
+        for (int i = 0; i < 4; i++) pb.issue_one(rb, st + kBwdOpBytes, wave_u, i);
     }
-    __syncthreads();
-    Frags f;
-    if (nk > 0) load_frags(f, smem, smem + kOpBytes, 0, wm, wn, lane);
+    uint32_t a_off[4], b_off[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        a_off[i] = tr_lane_off(wm * 128 + i * 32, lane);
+        b_off[i] = tr_lane_off(wn * 128 + i * 32, lane);
+    }
+    const uint32_t lds0 = lds_addr(smem);
+    FOCUS_WAIT_VMCNT(8);
+    asm volatile("s_barrier" ::: "memory");
+    Frags f, g;
+    load_frags_tr<0>(f, lds0, a_off, b_off);
     for (int64_t kt = 0; kt < nk; kt++) {
-        char *cur = smem + (kt & 1) * kStageBytes;
-        char *nxt = smem + ((kt + 1) & 1) * kStageBytes;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            a.load(X, t_end, K, t_begin + (kt + 1) * kStep, k0, t);
-            b.load(dY, t_end, N, t_begin + (kt + 1) * kStep, n0, t);
-        }
-        mma_step(cur, cur + kOpBytes, f, acc, wm, wn, lane);
-        if (more) {
-            a.store(nxt, t);
-            b.store(nxt + kOpBytes, t);
-        }
-        __syncthreads();
-        if (more) load_frags(f, nxt, nxt + kOpBytes, 0, wm, wn, lane);
+        FOCUS_WAIT_VMCNT(8);
+        asm volatile("s_barrier" ::: "memory");
+        const uint32_t cur = lds0 + (uint32_t)(kt & 3) * kBwdStageBytes;
+        const uint32_t nxt = lds0 + (uint32_t)((kt + 1) & 3) * kBwdStageBytes;
+        const int64_t t0 = t_begin + (kt + 3) * kBwdStep;
+        const __amdgpu_buffer_rsrc_t ra = BwdDma::step_rsrc(X, K, t0, t_end), rb = BwdDma::step_rsrc(dY, N, t0, t_end);
+        lds_char *st = lsm + (int)((kt + 3) & 3) * kBwdStageBytes;
+        tr_wait(f);  // f (read during the previous step's second half) has landed
+        load_frags_tr<1>(g, cur, a_off, b_off);
+        // the 8 loads of slot kt + 3 go out one after every second MFMA (see the forward kernel)
+        static_for<16>([&](auto idx) {
+            constexpr int i = idx / 4, jj = idx % 4;
+            acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[jj], acc[i][jj], 0, 0, 0);
+            if constexpr (idx % 2 == 1) {
+                __builtin_amdgcn_sched_barrier(0);
+                if constexpr (idx / 2 < 4) pa.issue_one(ra, st, wave_u, idx / 2);
+                else pb.issue_one(rb, st + kBwdOpBytes, wave_u, idx / 2 - 4);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        });
+        tr_wait(g);  // read before the first half's MFMAs, long landed
+        load_frags_tr<0>(f, nxt, a_off, b_off);
+        mma_frags(g, acc);
     }
+    tr_wait(f);  // no read may still be in flight when the workgroup ends
+    // the empty slots' zero writes must land before the workgroup's LDS is handed on
+    FOCUS_WAIT_VMCNT(0);
 
     // ---- fused straight-through epilogue on G^T = acc ----
     constexpr int B = block_of(FMT);
@@ -575,8 +633,8 @@ bool mfma_fwd_supported(int64_t M, int64_t N, int64_t K) {
 }
 
 bool mfma_bwd_supported(int64_t M, int64_t N, int64_t K) {
-    return N % 8 == 0 && K % 16 == 0 && N > 0 && K > 0 && M >= 0 && int64_t(kStep) * N * 2 < (int64_t(1) << 31) &&
-           int64_t(kStep) * K * 2 < (int64_t(1) << 31);
+    return N % 8 == 0 && K % 16 == 0 && N > 0 && K > 0 && M >= 0 && int64_t(kBwdStep) * N * 2 < (int64_t(1) << 31) &&
+           int64_t(kBwdStep) * K * 2 < (int64_t(1) << 31);
 }
 
 hipError_t launch_fwd_mfma(const void *X, const void *W, int64_t M, int64_t N, int64_t K, const void *Yref, void *dY,
