@@ -32,24 +32,26 @@ __device__ __forceinline__ uint32_t e2m1_index(float a) {
 // fp32 bit pattern of the magnitude with index idx: for idx >= 2 it is (1 + (idx & 1) / 2) *
 // 2^((idx >> 1) - 1); index 1 is 0.5 and index 0 is 0.
 __device__ __forceinline__ uint32_t e2m1_magnitude_bits(uint32_t idx) {
-    uint32_t hi = (((idx >> 1) + 126u) << 23) | ((idx & 1u) << 22);
-    return idx >= 2u ? hi : (idx ? 0x3F000000u : 0u);
+    const uint32_t hi = (((idx >> 1) + 126u) << 23) | ((idx & 1u) << 22);
+    // integer masks instead of a select chain, which the compiler turns into a divergent branch
+    const uint32_t ge2 = 0u - (uint32_t)(idx >= 2u), is1 = 0u - (uint32_t)(idx == 1u);
+    return (hi & ge2) | (0x3F000000u & is1);
 }
 
 // ---- E8M0 (scale rounded up to a power of two) ---------------------------------------------------
 // Smallest e in [-127, 127] with 2^e >= s. Non-positive s (and -0) -> -127; +inf -> 127;
 // NaN sets *nan_seen and gives -127.
 __device__ __forceinline__ int e8m0_ceil_exp(float s, bool &nan_seen) {
-    uint32_t b = __float_as_uint(s);
-    if ((b & 0x7FFFFFFFu) > 0x7F800000u) {
-        nan_seen = true;
-        return -127;
-    }
-    if ((int32_t)b <= 0) return -127;
-    uint32_t E = b >> 23, man = b & 0x7FFFFFu;
-    if (E == 0u) return man > 0x400000u ? -126 : -127;  // subnormal s < 2^-126; 2^-127 is man 0x400000
+    // every case computed, the result selected (no divergent branches)
+    const uint32_t b = __float_as_uint(s);
+    const bool nan = (b & 0x7FFFFFFFu) > 0x7F800000u;
+    const uint32_t E = b >> 23, man = b & 0x7FFFFFu;
     int e = (int)E - 127 + (man != 0u);
-    return e > 127 ? 127 : e;
+    e = E == 0u ? (man > 0x400000u ? -126 : -127) : e;  // subnormal s < 2^-126; 2^-127 is man 0x400000
+    e = e > 127 ? 127 : e;
+    e = (nan || (int32_t)b <= 0) ? -127 : e;
+    nan_seen = nan_seen || nan;
+    return e;
 }
 
 // 2^e as fp32 for e in [-127, 127]; 2^-127 is the subnormal 0x00400000.
@@ -60,20 +62,22 @@ __device__ __forceinline__ float exp2i(int e) {
 // ---- E4M3 (OCP E4M3FN: bias 7, max 448, subnormals m * 2^-9, no infinities) -----------------------
 // Round to nearest, ties to even, saturating at 448; x <= 0 -> 0; NaN sets *nan_seen.
 __device__ __forceinline__ uint32_t e4m3_code(float x, bool &nan_seen) {
-    uint32_t b = __float_as_uint(x);
-    if ((b & 0x7FFFFFFFu) > 0x7F800000u) {
-        nan_seen = true;
-        return 0u;
-    }
-    if ((int32_t)b <= 0) return 0u;
-    if (x >= 448.0f) return 0x7Eu;
-    if (x >= 0.015625f) {  // normal E4M3 range: keep 3 mantissa bits with round-half-even
-        uint32_t r = b + 0x7FFFFu + ((b >> 20) & 1u);
-        uint32_t code = (((r >> 23) - 120u) << 3) | ((r >> 20) & 7u);
-        return code > 0x7Eu ? 0x7Eu : code;
-    }
-    // subnormal range: the nearest multiple of 2^-9, ties to even (x * 512 is exact)
-    return (uint32_t)__builtin_rintf(x * 512.0f);
+    // every case computed, the result selected (no divergent branches)
+    const uint32_t b = __float_as_uint(x);
+    const bool nan = (b & 0x7FFFFFFFu) > 0x7F800000u;
+    // normal E4M3 range [2^-6, 448): keep 3 mantissa bits with round-half-even
+    const uint32_t r = b + 0x7FFFFu + ((b >> 20) & 1u);
+    uint32_t normal = (((r >> 23) - 120u) << 3) | ((r >> 20) & 7u);
+    normal = normal > 0x7Eu ? 0x7Eu : normal;
+    // subnormal range: the nearest multiple of 2^-9, ties to even (x * 512 is exact); the clamp
+    // only keeps the conversion defined for inputs the selects below discard
+    const float t = __builtin_fminf(__builtin_fmaxf(x * 512.0f, 0.0f), 512.0f);
+    const uint32_t sub = (uint32_t)__builtin_rintf(t);
+    uint32_t code = x >= 0.015625f ? normal : sub;
+    code = x >= 448.0f ? 0x7Eu : code;
+    code = (nan || (int32_t)b <= 0) ? 0u : code;
+    nan_seen = nan_seen || nan;
+    return code;
 }
 
 __device__ __forceinline__ float e4m3_value(uint32_t code) {
@@ -138,22 +142,18 @@ struct Quantized {
 };
 
 __device__ __forceinline__ Quantized quantize_element(float x, float sq, float sdq, bool ste_clip) {
+    // both cases are computed and the result masked: no divergent branch per element
     Quantized r;
-    uint32_t sign = __float_as_uint(x) & 0x80000000u;
-    if (sdq == 0.0f || sq == 0.0f) {
-        r.u = 0.0f;
-        r.q = __uint_as_float(sign);
-        r.code = sign >> 28;
-        r.m = false;
-    } else {
-        float u = x / sq;
-        float a = __builtin_fabsf(u);
-        uint32_t idx = e2m1_index(a);
-        r.u = u;
-        r.q = __uint_as_float(e2m1_magnitude_bits(idx) | sign);
-        r.code = (sign >> 28) | idx;
-        r.m = ste_clip ? (a <= 6.0f) : true;
-    }
+    const uint32_t sign = __float_as_uint(x) & 0x80000000u;
+    const bool zero = sdq == 0.0f || sq == 0.0f;
+    const uint32_t keep = 0u - (uint32_t)!zero;  // all ones unless the scale is zero
+    const float u = x / (zero ? 1.0f : sq);
+    const float a = __builtin_fabsf(u);
+    const uint32_t idx = e2m1_index(a) & keep;    // index 0 for a zero scale
+    r.u = __uint_as_float(__float_as_uint(u) & keep);
+    r.q = __uint_as_float(e2m1_magnitude_bits(idx) | sign);
+    r.code = (sign >> 28) | idx;
+    r.m = !zero && (ste_clip ? (a <= 6.0f) : true);
     r.xhat = r.q * sdq;
     return r;
 }

@@ -167,14 +167,24 @@ bwd_valu_kernel(const void *__restrict__ dY, const void *__restrict__ X, int64_t
 // ------------------------------------------------------------------------------------------------
 // Deterministic finishing reductions (fixed summation order, no atomics).
 
-// col_sq[n] = sum over m-tiles (in tile order) of colpart[mt][n]
+// col_sq[n] = sum over m-tiles of colpart[mt][n] in a fixed order: 16 row groups (mt mod 16, each
+// summed in ascending mt), then a fixed pairwise tree over the groups. A workgroup covers 16
+// columns, so even a narrow layer spreads over many workgroups.
 __global__ void __launch_bounds__(256)
 colsum_kernel(const double *__restrict__ colpart, int64_t mtiles, int64_t N, double *__restrict__ col_sq) {
-    for (int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x; n < N; n += (int64_t)gridDim.x * 256) {
-        double s = 0.0;
-        for (int64_t mt = 0; mt < mtiles; mt++) s += colpart[mt * N + n];
-        col_sq[n] = s;
+    __shared__ double red[16][16];
+    const int cx = threadIdx.x & 15, grp = threadIdx.x >> 4;
+    const int64_t n = (int64_t)blockIdx.x * 16 + cx;
+    double s = 0.0;
+    if (n < N)
+        for (int64_t mt = grp; mt < mtiles; mt += 16) s += colpart[mt * N + n];
+    red[grp][cx] = s;
+    __syncthreads();
+    for (int w = 8; w > 0; w >>= 1) {
+        if (grp < w) red[grp][cx] += red[grp + w][cx];
+        __syncthreads();
     }
+    if (grp == 0 && n < N) col_sq[n] = red[0][cx];
 }
 
 // loss = (sum over n of col_sq[n]) / (M N); one workgroup, strided partial sums then a fixed tree
@@ -239,9 +249,11 @@ BwdPlan plan_bwd(int op_dt, int fmt, int sb, int64_t M, int64_t N, int64_t K, bo
     if (!want_G) {
         // The token range is split so that tiles * splits workgroups fill the chip in whole rounds
         // (one 256 x 256 workgroup per CU on the MFMA path, several 64 x 64 ones on the VALU path):
-        // minimise rounds * (steps per split + epilogue), each split keeping >= 4 steps.
+        // minimise rounds * (steps per split + epilogue), each split keeping >= 4 steps. The MFMA
+        // path's straight-through epilogue (a 256 x 256 tile at one wave per SIMD) costs about as
+        // much as 36 of its 64-token steps, as measured on MI355X.
         const int64_t slots = p.path == 1 ? kMfmaConcurrentWgs : 2048;
-        const int64_t epilogue_steps = 4;
+        const int64_t epilogue_steps = p.path == 1 ? 36 : 4;
         const int64_t max_splits = std::max<int64_t>(1, std::min<int64_t>(steps_total / 4, 4096));
         int64_t best = -1;
         for (int64_t s = 1; s <= max_splits; s++) {
@@ -277,8 +289,7 @@ hipError_t launch_recon_fwd(const FwdPlan &p, int op_dt, const void *X, const vo
         if (e != hipSuccess) return e;
     }
     if (!Yref) return hipSuccess;
-    const unsigned g = (unsigned)std::min<int64_t>(cdiv(N, 256), 1024);
-    colsum_kernel<<<g, 256, 0, st>>>(colpart, p.mtiles, N, col_sq);
+    colsum_kernel<<<(unsigned)cdiv(N, 16), 256, 0, st>>>(colpart, p.mtiles, N, col_sq);
     if (loss_out) loss_kernel<<<1, 256, 0, st>>>(col_sq, N, 1.0 / ((double)M * (double)N), loss_out);
     return hipGetLastError();
 }

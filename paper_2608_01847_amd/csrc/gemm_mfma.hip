@@ -35,7 +35,7 @@ namespace {
 
 constexpr int kTile = 256;            // output tile edge
 constexpr int kThreads = 256;         // four waves
-constexpr int kLdsBytes = 128 * 1024; // four 32 KB stages
+constexpr int kLdsBytes = 160 * 1024; // LDS of one gfx950 CU
 
 static_assert(kTile == kMfmaTileM && kTile == kMfmaTileN && kTile == kMfmaTileK, "tile geometry");
 
@@ -58,8 +58,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, in
 constexpr int kFwdStep = 32;
 constexpr int kFwdOpBytes = kTile * 64;   // 256 rows x 32 bf16 = 16 KB
 constexpr int kFwdStageBytes = 2 * kFwdOpBytes;
-constexpr int kFwdStages = 4;
-static_assert(kFwdStages * kFwdStageBytes <= kLdsBytes, "forward stages fit the LDS allocation");
+#ifndef FOCUS_FWD_STAGES
+#define FOCUS_FWD_STAGES 5
+#endif
+constexpr int kFwdStages = FOCUS_FWD_STAGES;
+static_assert(kFwdStages >= 4 && kFwdStages * kFwdStageBytes <= kLdsBytes, "forward stages fit the LDS");
 
 typedef __attribute__((address_space(3))) char lds_char;
 
@@ -269,7 +272,7 @@ __global__ void __launch_bounds__(kThreads, 1)
 fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, int64_t M, int64_t N, int64_t K,
                 const uint16_t *__restrict__ Yref, uint16_t *__restrict__ dY, float dscale,
                 double *__restrict__ colpart, int tiles_n) {
-    __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+    __shared__ __attribute__((aligned(16))) char smem[kFwdStages * kFwdStageBytes];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
     uint32_t tm, tn;
     grouped_tile(xcd_tile(blockIdx.x, gridDim.x), gridDim.x / tiles_n, tiles_n, tm, tn);
@@ -282,10 +285,11 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
 #pragma unroll
         for (int j = 0; j < 4; j++) acc[i][j] = zero;
 
-    // Four LDS stages of 32 of K. Load "slot" j fills stage j % 4: for j < nk it is step j of the
-    // operands; slots nk .. nk + 3 bring the four 64-row quarters of the Y_ref tile (zeros in the
-    // plain mode), so the epilogue's input arrives while the last steps' MFMAs run. Every slot is
-    // 8 loads per thread, which is what the vmcnt waits below count on.
+    // S = kFwdStages LDS stages of 32 of K. Load "slot" j fills stage j % S: for j < nk it is
+    // step j of the operands; slots nk .. nk + 3 bring the four 64-row quarters of the Y_ref tile
+    // (zeros in the plain mode), so the epilogue's input arrives while the last steps' MFMAs run.
+    // Every slot is 8 loads per thread, which is what the vmcnt waits below count on.
+    constexpr int S = kFwdStages;
     lds_char *const lsm = (lds_char *)smem;
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
     FwdDma dma;  // X and W panels have the same row length K, so one set of offsets serves both
@@ -302,18 +306,17 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
     // reading rows r and r + 4 of one column group use different banks.
     auto q_row = [](uint32_t rl, uint32_t q) { return (rl >> 5) * 128u + q * 32u + (rl & 31u); };
     auto q_off = [](uint32_t rl, uint32_t chunk) { return rl * 512u + ((chunk ^ (((rl >> 2) & 1u) << 2)) << 4); };
-    // Load i (0..7) of slot j: loads 0-3 bring X rows, 4-7 W rows of an operand step; a Y_ref
-    // quarter is 32 one-KB blocks of two rows each, this wave filling blocks 8 wave .. 8 wave + 7
-    // (lane L of block b lands in local row 2 b + L / 32, physical chunk L % 32).
-    auto issue_op = [&](int64_t j, int i) {
-        lds_char *st = lsm + (int)(j & 3) * kFwdStageBytes;
+    auto stage = [&](int sidx) { return lsm + sidx * kFwdStageBytes; };
+    // Load i (0..7) of slot j into stage st: loads 0-3 bring X rows, 4-7 W rows of an operand
+    // step; a Y_ref quarter is 32 one-KB blocks of two rows each, this wave filling blocks
+    // 8 wave .. 8 wave + 7 (lane L of block b lands in local row 2 b + L / 32, physical chunk L % 32).
+    auto issue_op = [&](lds_char *st, int64_t j, int i) {
         const int64_t k0 = j * kFwdStep;
         const uint32_t base = (uint32_t)k0 * 2u, bad = dma.step_bad(K, k0);
         if (i < 4) dma.issue_one(ra, base, bad, st, wave_u, i);
         else dma.issue_one(rb, base, bad, st + kFwdOpBytes, wave_u, i - 4);
     };
-    auto issue_y = [&](int64_t j, int i) {
-        lds_char *st = lsm + (int)(j & 3) * kFwdStageBytes;
+    auto issue_y = [&](lds_char *st, int64_t j, int i) {
         const uint32_t q = (uint32_t)((j - nk) & 3);
         const uint32_t blk = wave_u * 8 + i, rl = 2 * blk + (lane >> 5);
         const uint32_t chunk = (uint32_t)(lane & 31) ^ (((rl >> 2) & 1u) << 2);
@@ -323,55 +326,61 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_y, st + blk * 1024, 16, (int)off, 0, 0, 0);
     };
     auto issue_slot = [&](int64_t j) {
+        lds_char *st = stage((int)(j % S));
         if (j < nk) {
 #pragma unroll
-            for (int i = 0; i < 8; i++) issue_op(j, i);
+            for (int i = 0; i < 8; i++) issue_op(st, j, i);
         } else {
 #pragma unroll
-            for (int i = 0; i < 8; i++) issue_y(j, i);
+            for (int i = 0; i < 8; i++) issue_y(st, j, i);
         }
     };
 #pragma unroll
-    for (int s0 = 0; s0 < kFwdStages - 1; s0++) issue_slot(s0);
-    // Before the barrier of step kt, this thread's loads of steps kt and kt + 1 have landed (only
-    // slot kt + 2's 8 loads may still be in flight); after it, everyone's have, so the first
-    // fragments of step kt + 1 can be read while step kt's MFMAs run, and stage (kt + 3) % 4, last
-    // read in step kt - 1, can be refilled. A bare s_barrier: __syncthreads would also wait for
-    // the loads still in flight.
-    FOCUS_WAIT_VMCNT(8);
+    for (int s0 = 0; s0 < S - 1; s0++) issue_slot(s0);
+    // Before the barrier of step kt, this thread's loads of slots up to kt + 1 have landed (only
+    // slots kt + 2 .. kt + S - 2 may still be in flight); after it, everyone's have, so the first
+    // fragments of step kt + 1 can be read while step kt's MFMAs run, and stage (kt - 1) % S,
+    // last read in step kt - 1, can be refilled with slot kt + S - 1. A bare s_barrier:
+    // __syncthreads would also wait for the loads still in flight.
+    FOCUS_WAIT_VMCNT(8 * (S - 3));
     asm volatile("s_barrier" ::: "memory");
     Frags f, g;
     load_frags_fwd(f, smem, smem + kFwdOpBytes, 0, wm, wn, lane);
-    // One step. The 8 loads of slot kt + 3 go out one after every second MFMA of the first half:
-    // issued back to back they would fill the texture unit's queue, and a wave stalled on a full
-    // queue issues no MFMA. The scheduling barriers keep the compiler from regrouping them.
-    auto step = [&](int64_t kt, auto y_slot) {
-        FOCUS_WAIT_VMCNT(8);
+    // One step (sc = kt % S). The 8 loads of slot kt + S - 1 go out one after every second MFMA
+    // of the first half: issued back to back they would fill the texture unit's queue, and a wave
+    // stalled on a full queue issues no MFMA. The scheduling barriers keep the compiler from
+    // regrouping them.
+    auto step = [&](int64_t kt, int sc, auto y_slot) {
+        FOCUS_WAIT_VMCNT(8 * (S - 3));
         asm volatile("s_barrier" ::: "memory");
-        const char *As = smem + (int)(kt & 3) * kFwdStageBytes, *Bs = As + kFwdOpBytes;
-        const char *An = smem + (int)((kt + 1) & 3) * kFwdStageBytes, *Bn = An + kFwdOpBytes;
+        const int sn = sc == S - 1 ? 0 : sc + 1, sl = sc == 0 ? S - 1 : sc - 1;
+        const char *As = smem + sc * kFwdStageBytes, *Bs = As + kFwdOpBytes;
+        const char *An = smem + sn * kFwdStageBytes, *Bn = An + kFwdOpBytes;
+        lds_char *st = stage(sl);
         load_frags_fwd(g, As, Bs, 1, wm, wn, lane);
         static_for<16>([&](auto idx) {
             constexpr int i = idx / 4, jj = idx % 4;
             acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[jj], acc[i][jj], 0, 0, 0);
             if constexpr (idx % 2 == 1) {
                 __builtin_amdgcn_sched_barrier(0);
-                if constexpr (decltype(y_slot)::value) issue_y(kt + 3, idx / 2);
-                else issue_op(kt + 3, idx / 2);
+                if constexpr (decltype(y_slot)::value) issue_y(st, kt + S - 1, idx / 2);
+                else issue_op(st, kt + S - 1, idx / 2);
                 __builtin_amdgcn_sched_barrier(0);
             }
         });
         load_frags_fwd(f, An, Bn, 0, wm, wn, lane);
         mma_frags(g, acc);
     };
-    const int64_t n_op = nk > 3 ? nk - 3 : 0;  // steps whose slot kt + 3 is an operand step
+    const int64_t n_op = nk > S - 1 ? nk - (S - 1) : 0;  // steps whose slot kt + S - 1 is an operand step
     int64_t kt = 0;
-    for (; kt < n_op; kt++) step(kt, std::false_type{});
-    for (; kt < nk; kt++) step(kt, std::true_type{});
-    // the last quarter goes into the stage of the last step, once every wave is done with it
-    asm volatile("s_barrier" ::: "memory");
-#pragma unroll
-    for (int i = 0; i < 8; i++) issue_y(nk + 3, i);
+    int sc = 0;
+    for (; kt < n_op; kt++, sc = sc == S - 1 ? 0 : sc + 1) step(kt, sc, std::false_type{});
+    for (; kt < nk; kt++, sc = sc == S - 1 ? 0 : sc + 1) step(kt, sc, std::true_type{});
+    // quarters not yet issued (S == 4: the last one) go into stages whose steps every wave is done with
+    if constexpr (S < 5) {
+        asm volatile("s_barrier" ::: "memory");
+        for (int64_t j = nk + S - 1; j <= nk + 3; j++) issue_slot(j);
+    }
 
     // ---- epilogue, one quarter at a time: D = Y_hat - Y_ref, dY = D * dscale, column sums of D^2
     // Each lane reads its 16 Y values of an accumulator tile from LDS, then writes the 16 dY values
@@ -387,7 +396,7 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
             FOCUS_WAIT_VMCNT(24);  // this thread's loads of quarter 0 have landed
             asm volatile("s_barrier" ::: "memory");
         }
-        lds_char *qb = lsm + (int)((nk + q) & 3) * kFwdStageBytes;
+        lds_char *qb = stage((int)((nk + q) % S));
         static_for<4>([&](auto j) {
             const uint32_t n = wn * 128 + j * 32 + lr;  // column in the tile
             typedef __attribute__((address_space(3))) uint16_t lds_u16;
@@ -446,7 +455,7 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
                 int64_t chunk, const void *__restrict__ W, const float *__restrict__ s_fp,
                 const float *__restrict__ c, int sb_log2, const float *__restrict__ alpha_ptr, int ste_clip,
                 float *__restrict__ part_s, float *__restrict__ part_c, uint32_t *flag, int tiles_n) {
-    __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+    __shared__ __attribute__((aligned(16))) char smem[kBwdStages * kBwdStageBytes];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
     // linear id -> (split, tile): splits outermost, tiles of one split in grouped order, so that an
     // XCD's concurrent workgroups share the operand panels of one token range
@@ -525,64 +534,111 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
     FOCUS_WAIT_VMCNT(0);
 
     // ---- fused straight-through epilogue on G^T = acc ----
+    // acc[i][j][r] is G[n][k] for n = n0 + 128 wn + 32 j + (lane % 32) and
+    // k = k0 + 128 wm + 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4: lane l holds, for each group g of
+    // 8 k, the 4 consecutive k 4 (l / 32) .. + 3, and lanes l, l ^ 32 together hold the whole group.
     constexpr int B = block_of(FMT);
+    constexpr int NBI = 32 / B;                   // blocks per 32 k (1 MXFP4, 2 NVFP4)
+    constexpr int WB = WDT == kBF16 ? 2 : 4;      // bytes per weight element
     const float alpha = FMT == kFmtNV ? *alpha_ptr : 1.0f;
     const int sb = 1 << sb_log2;
     const int64_t nb = K / B, ns = K >> sb_log2;
     const int lr = lane & 31, lh = lane >> 5;
+    const bool has_c = c != nullptr;
     bool bad = false;
+    // W, S_fp and c of the tile's rows come through range-checked buffer loads: rows past N read
+    // as zeros, and so do columns past K (bit 31 of the offset). Out-of-range elements have G = 0
+    // and w = 0 and add exactly zero to every sum; they are kept out of the domain check, and
+    // their partial sums are not stored (bit 31 again: the store is dropped). All offsets are
+    // 32-bit: a tile spans 256 rows of W (checked when the path is chosen).
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(reinterpret_cast<const char *>(W) + n0 * K * WB, (N - n0) * K * WB);
+    const __amdgpu_buffer_rsrc_t rsf = make_rsrc(s_fp + n0 * nb, (N - n0) * nb * 4);
+    const __amdgpu_buffer_rsrc_t rc = make_rsrc(has_c ? c + n0 * ns : s_fp, has_c ? (N - n0) * ns * 4 : 0);
+    const __amdgpu_buffer_rsrc_t rps = make_rsrc(part_s + (split * N + n0) * nb, (N - n0) * nb * 4);
+    const __amdgpu_buffer_rsrc_t rpc = make_rsrc(part_c + (split * N + n0) * ns, (N - n0) * ns * 4);
+    const uint32_t K32 = (uint32_t)K, nb32 = (uint32_t)nb, ns32 = (uint32_t)ns;
+    auto past = [&](uint32_t k) { return (uint32_t)(k >= K32) << 31; };  // k < 2^31 (K is)
+    const uint32_t lh_drop = (uint32_t)lh << 31;  // stores made by the lane pair's lower lane only
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
     static_for<4>([&](auto j) {
-        const int64_t n = n0 + wn * 128 + j * 32 + lr;
-        const bool n_ok = n < N;
+        const uint32_t nl = wn * 128 + j * 32 + lr;  // row of W inside the tile (< 256)
+        const bool n_ok = n0 + nl < N;
+        const uint32_t n_drop = (uint32_t)!n_ok << 31;
+        // all loads of this column first
+        float wv[4][4][4];   // [i][g][e]
+        float sv[4][NBI];    // [i][block]
+        float cv[4][4][2];   // [i][g][elements 0-1 / 2-3]
         static_for<4>([&](auto i) {
-            const int64_t kb = k0 + wm * 128 + i * 32;  // 32 consecutive k: one MXFP4 / two NVFP4 blocks
-            float tc[4][2];                              // per group of 8 k: sums of elements 0-1 / 2-3
-            float ts[4];                                 // per group of 8 k
+            const uint32_t kb = (uint32_t)k0 + wm * 128 + i * 32;
             static_for<4>([&](auto g) {
-                const int64_t kg = kb + 8 * g;           // group start; this lane has kg + 4 lh + 0..3
-                const int64_t k = kg + 4 * lh;
-                tc[g][0] = tc[g][1] = ts[g] = 0.0f;
-                if (n_ok && kg < K) {
-                    float w[4];
-                    if (WDT == kBF16) {
-                        const uint2 p = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(W) + n * K + k);
-                        w[0] = __uint_as_float(p.x << 16);
-                        w[1] = __uint_as_float(p.x & 0xFFFF0000u);
-                        w[2] = __uint_as_float(p.y << 16);
-                        w[3] = __uint_as_float(p.y & 0xFFFF0000u);
-                    } else {
-                        const float4 p = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(W) + n * K + k);
-                        w[0] = p.x; w[1] = p.y; w[2] = p.z; w[3] = p.w;
-                    }
-                    uint32_t byte;
-                    const float sdq = weight_sdq(FMT, s_fp[n * nb + kg / B], alpha, byte, bad);
-                    float cv0 = 1.0f, cv1 = 1.0f;
-                    if (c) {
-                        cv0 = c[n * ns + (k >> sb_log2)];
-                        cv1 = sb == 2 ? c[n * ns + ((k + 2) >> sb_log2)] : cv0;
-                        bad = bad || bad_coeff(cv0) || bad_coeff(cv1);
-                    }
-                    static_for<4>([&](auto e) {
-                        float a1, a2;
-                        ste_terms(acc[i][j][(int)(4 * g + e)], w[e], sdq, e < 2 ? cv0 : cv1, ste_clip != 0, a1, a2);
-                        tc[g][e >> 1] += a1;
-                        ts[g] += a2;
-                    });
+                const uint32_t k = kb + 8 * g + 4 * lh;  // this lane's 4 consecutive k
+                const uint32_t wo = ((nl * K32 + k) * WB) | past(k);
+                if constexpr (WDT == kBF16) {
+                    const u32x2 p = __builtin_amdgcn_raw_buffer_load_b64(rw, (int)wo, 0, 0);
+                    wv[i][g][0] = __uint_as_float(p.x << 16);
+                    wv[i][g][1] = __uint_as_float(p.x & 0xFFFF0000u);
+                    wv[i][g][2] = __uint_as_float(p.y << 16);
+                    wv[i][g][3] = __uint_as_float(p.y & 0xFFFF0000u);
+                } else {
+                    const u32x4 p = __builtin_amdgcn_raw_buffer_load_b128(rw, (int)wo, 0, 0);
+                    wv[i][g][0] = __uint_as_float(p.x);
+                    wv[i][g][1] = __uint_as_float(p.y);
+                    wv[i][g][2] = __uint_as_float(p.z);
+                    wv[i][g][3] = __uint_as_float(p.w);
                 }
+                // coefficients of elements 0-1 and 2-3 (the same sub-block unless sb == 2); without
+                // c the resource is empty and the select makes them 1
+                const uint32_t c0 = ((nl * ns32 + (k >> sb_log2)) * 4u) | past(k);
+                const uint32_t c1 = ((nl * ns32 + ((k + 2) >> sb_log2)) * 4u) | past(k);
+                const float l0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rc, (int)c0, 0, 0));
+                const float l1 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rc, (int)c1, 0, 0));
+                cv[i][g][0] = has_c ? l0 : 1.0f;
+                cv[i][g][1] = has_c ? l1 : 1.0f;
+            });
+            static_for<NBI>([&](auto h) {
+                const uint32_t kh = kb + h * B;
+                const uint32_t so = ((nl * nb32 + kh / B) * 4u) | past(kh);
+                sv[i][h] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsf, (int)so, 0, 0));
+            });
+        });
+        static_for<4>([&](auto i) {
+            const uint32_t kb = (uint32_t)k0 + wm * 128 + i * 32;  // one MXFP4 / two NVFP4 blocks
+            float sdq[NBI];
+            static_for<NBI>([&](auto h) {
+                bool nan = false;
+                uint32_t byte;
+                sdq[h] = weight_sdq(FMT, sv[i][h], alpha, byte, nan);
+                bad = bad || (n_ok && kb + h * B < K32 && nan);
+            });
+            float tc[4][2];  // per group of 8 k: this lane's sums of G m w over elements 0-1 / 2-3
+            float ts[4];     // per group of 8 k: this lane's sum of G (q - m u)
+            static_for<4>([&](auto g) {
+                const float sd = sdq[(8 * g) / B];
+                const float cv0 = cv[i][g][0], cv1 = cv[i][g][1];
+                bad = bad || (n_ok && kb + 8 * g < K32 && has_c && (bad_coeff(cv0) || bad_coeff(cv1)));
+                tc[g][0] = tc[g][1] = ts[g] = 0.0f;
+                static_for<4>([&](auto e) {
+                    float a1, a2;
+                    ste_terms(acc[i][j][(int)(4 * g + e)], wv[i][g][e], sd, e < 2 ? cv0 : cv1, ste_clip != 0, a1, a2);
+                    tc[g][e >> 1] += a1;
+                    ts[g] += a2;
+                });
             });
             // ---- sub-block sums of G m w (scaled by -1/c^2 after the split reduction) ----
             if (sb <= 4) {
                 // a sub-block lies inside one lane's 4 consecutive k
                 static_for<4>([&](auto g) {
-                    const int64_t k = kb + 8 * g + 4 * lh;
-                    if (n_ok && kb + 8 * g < K) {
-                        float *dst = part_c + (split * N + n) * ns;
-                        if (sb == 4) {
-                            dst[k >> 2] = tc[g][0] + tc[g][1];
-                        } else {
-                            dst[k >> 1] = tc[g][0];
-                            dst[(k >> 1) + 1] = tc[g][1];
-                        }
+                    const uint32_t k = kb + 8 * g + 4 * lh;
+                    const uint32_t drop = n_drop | past(k);
+                    if (sb == 4) {
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(tc[g][0] + tc[g][1]), rpc,
+                                                              (int)(((nl * ns32 + (k >> 2)) * 4u) | drop), 0, 0);
+                    } else {
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(tc[g][0]), rpc,
+                                                              (int)(((nl * ns32 + (k >> 1)) * 4u) | drop), 0, 0);
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(tc[g][1]), rpc,
+                                                              (int)(((nl * ns32 + (k >> 1) + 1) * 4u) | drop), 0, 0);
                     }
                 });
             } else {
@@ -591,32 +647,35 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
                     s8[g] = tc[g][0] + tc[g][1];
                     s8[g] += __shfl_xor(s8[g], 32, 64);
                 });
-                if (lh == 0 && n_ok) {
-                    float *dst = part_c + (split * N + n) * ns;
-                    if (sb == 8) {
-                        static_for<4>([&](auto g) {
-                            if (kb + 8 * g < K) dst[(kb >> 3) + g] = s8[g];
-                        });
-                    } else if (sb == 16) {
-                        if (kb < K) dst[kb >> 4] = s8[0] + s8[1];
-                        if (kb + 16 < K) dst[(kb >> 4) + 1] = s8[2] + s8[3];
-                    } else {
-                        if (kb < K) dst[kb >> 5] = (s8[0] + s8[1]) + (s8[2] + s8[3]);
-                    }
+                const uint32_t drop = n_drop | lh_drop;
+                if (sb == 8) {
+                    static_for<4>([&](auto g) {
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s8[g]), rpc,
+                                                              (int)(((nl * ns32 + (kb >> 3) + g) * 4u) | drop | past(kb + 8 * g)), 0, 0);
+                    });
+                } else if (sb == 16) {
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s8[0] + s8[1]), rpc,
+                                                          (int)(((nl * ns32 + (kb >> 4)) * 4u) | drop | past(kb)), 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s8[2] + s8[3]), rpc,
+                                                          (int)(((nl * ns32 + (kb >> 4) + 1) * 4u) | drop | past(kb + 16)), 0, 0);
+                } else {
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint((s8[0] + s8[1]) + (s8[2] + s8[3])), rpc,
+                                                          (int)(((nl * ns32 + (kb >> 5)) * 4u) | drop | past(kb)), 0, 0);
                 }
             }
             // ---- block sums of G (q - m u) ----
             float h0 = ts[0] + ts[1], h1 = ts[2] + ts[3];
             h0 += __shfl_xor(h0, 32, 64);
             h1 += __shfl_xor(h1, 32, 64);
-            if (lh == 0 && n_ok) {
-                float *dst = part_s + (split * N + n) * nb;
-                if (B == 32) {
-                    if (kb < K) dst[kb >> 5] = h0 + h1;
-                } else {
-                    if (kb < K) dst[kb >> 4] = h0;
-                    if (kb + 16 < K) dst[(kb >> 4) + 1] = h1;
-                }
+            const uint32_t drop = n_drop | lh_drop;
+            if constexpr (B == 32) {
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h0 + h1), rps,
+                                                      (int)(((nl * nb32 + (kb >> 5)) * 4u) | drop | past(kb)), 0, 0);
+            } else {
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h0), rps,
+                                                      (int)(((nl * nb32 + (kb >> 4)) * 4u) | drop | past(kb)), 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h1), rps,
+                                                      (int)(((nl * nb32 + (kb >> 4) + 1) * 4u) | drop | past(kb + 16)), 0, 0);
             }
         });
     });
@@ -634,7 +693,7 @@ bool mfma_fwd_supported(int64_t M, int64_t N, int64_t K) {
 
 bool mfma_bwd_supported(int64_t M, int64_t N, int64_t K) {
     return N % 8 == 0 && K % 16 == 0 && N > 0 && K > 0 && M >= 0 && int64_t(kBwdStep) * N * 2 < (int64_t(1) << 31) &&
-           int64_t(kBwdStep) * K * 2 < (int64_t(1) << 31);
+           int64_t(kBwdStep) * K * 2 < (int64_t(1) << 31) && int64_t(kTile) * K * 4 < (int64_t(1) << 31);
 }
 
 hipError_t launch_fwd_mfma(const void *X, const void *W, int64_t M, int64_t N, int64_t K, const void *Yref, void *dY,
