@@ -78,7 +78,7 @@ size_t focus_workspace_size(int call, const focus_qconfig *q, int64_t M, int64_t
     switch (call) {
         case FOCUS_CALL_SCALES_INIT:
         case FOCUS_CALL_FAKEQUANT_FWD:
-            return kWsHeader + kAbsmaxParts * sizeof(float);
+            return kWsHeader + (kAbsmaxParts + 64) * sizeof(float);  // partial maxima + tensor scale slot
         case FOCUS_CALL_FAKEQUANT_BWD:
         case FOCUS_CALL_EXPORT_PACKED:
             return kWsHeader;

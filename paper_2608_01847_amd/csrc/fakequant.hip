@@ -38,19 +38,21 @@ fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int
     const int sb = 1 << sb_log2;
     const int64_t nb = K / B, ns = K >> sb_log2;
     bool bad = false;
+    // rows are contiguous: chunk t starts at element e0 = row0 K + 8 t, its block's scale is
+    // s_fp[e0 / B] and its first sub-block coefficient c[e0 >> log2 sb]
+    (void)cpr, (void)nb, (void)ns;
+    const int64_t e_row0 = row0 * K;
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
-        const uint32_t r = t / cpr, j = t - r * cpr;
-        const int64_t row = row0 + r, k0 = (int64_t)j * 8;
-        const int64_t e0 = row * K + k0;
+        const int64_t e0 = e_row0 + (int64_t)t * 8;
         float v[8];
         load8(W, IN, e0, v);
         uint32_t byte;
-        const float sdq = weight_sdq(FMT, s_fp[row * nb + k0 / B], alpha, byte, bad);
+        const float sdq = weight_sdq(FMT, s_fp[e0 / B], alpha, byte, bad);
         float cv[4] = {1.0f, 1.0f, 1.0f, 1.0f};
         const int ncoef = sb >= 8 ? 1 : 8 >> sb_log2;
         if (c) {
             for (int i = 0; i < ncoef; i++) {
-                cv[i] = c[row * ns + (k0 >> sb_log2) + i];
+                cv[i] = c[(e0 >> sb_log2) + i];
                 bad |= bad_coeff(cv[i]);
             }
         }
@@ -66,7 +68,7 @@ fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int
         }
         if (w_hat) store8(w_hat, OUT, e0, out);
         if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
-        if (scale_bytes && (k0 % B) == 0) scale_bytes[row * nb + k0 / B] = (uint8_t)byte;
+        if (scale_bytes && (e0 % B) == 0) scale_bytes[e0 / B] = (uint8_t)byte;
     }
     if (bad) raise_domain_flag(flag);
     (void)ste_clip;
@@ -81,12 +83,13 @@ __global__ void __launch_bounds__(256)
 fq_act_mx_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
                  void *__restrict__ x_hat, uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes,
                  uint32_t *flag) {
-    const int64_t nb = K / 32;
+    // Rows are contiguous, so chunk t (8 elements) starts at element row0 K + 8 t and its block's
+    // scale byte is element / 32. Launched with one chunk per thread (the loop is a guard).
+    (void)cpr;
+    const int64_t e_row0 = row0 * K;
     bool bad = false;
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
-        const uint32_t r = t / cpr, j = t - r * cpr;
-        const int64_t row = row0 + r, k0 = (int64_t)j * 8;
-        const int64_t e0 = row * K + k0;
+        const int64_t e0 = e_row0 + (int64_t)t * 8;
         float v[8];
         load8(X, IN, e0, v);
         float amax = 0.0f;
@@ -95,19 +98,22 @@ fq_act_mx_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
         amax = group_max(amax, 4);
         const int e = e8m0_ceil_exp(amax / 6.0f, bad);
         const float S = exp2i(e), inv = exp2i(-e);
+        // u = x 2^-e has the sign of x, so the hardware code's sign bit is the code's; element i
+        // lands in nibble i
+        uint32_t packed = e2m1_code2<0>(0u, v[0] * inv, v[1] * inv);
+        packed = e2m1_code2<1>(packed, v[2] * inv, v[3] * inv);
+        packed = e2m1_code2<2>(packed, v[4] * inv, v[5] * inv);
+        packed = e2m1_code2<3>(packed, v[6] * inv, v[7] * inv);
         float out[8];
-        uint32_t packed = 0;
+        e2m1_value2<0>(packed, out[0], out[1]);
+        e2m1_value2<1>(packed, out[2], out[3]);
+        e2m1_value2<2>(packed, out[4], out[5]);
+        e2m1_value2<3>(packed, out[6], out[7]);
 #pragma unroll
-        for (int i = 0; i < 8; i++) {
-            const uint32_t sign = __float_as_uint(v[i]) & 0x80000000u;
-            const uint32_t idx = e2m1_index(__builtin_fabsf(v[i] * inv));
-            const float q = __uint_as_float(e2m1_magnitude_bits(idx) | sign);
-            out[i] = q * S;
-            packed |= ((sign >> 28) | idx) << (4 * i);
-        }
+        for (int i = 0; i < 8; i++) out[i] *= S;
         if (x_hat) store8(x_hat, OUT, e0, out);
         if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
-        if (scale_bytes && (k0 % 32) == 0) scale_bytes[row * nb + k0 / 32] = (uint8_t)(e + 127);
+        if (scale_bytes && (t & 3u) == 0) scale_bytes[e0 / 32] = (uint8_t)(e + 127);
     }
     if (bad) raise_domain_flag(flag);
 }
@@ -151,23 +157,32 @@ __device__ float tensor_alpha_from_partials(const float *__restrict__ partial, i
     return A > 0.0f ? A / 2688.0f : 1.0f;
 }
 
+// pass 2 of the NVFP4 tensor scale: one workgroup folds the partial maxima once, into a workspace
+// slot that the elementwise kernels read (and into alpha_out when given)
+__global__ void __launch_bounds__(256)
+tensor_alpha_kernel(const float *__restrict__ partial, int npart, float *__restrict__ alpha_slot,
+                    float *__restrict__ alpha_out) {
+    const float a = tensor_alpha_from_partials(partial, npart);
+    if (threadIdx.x == 0) {
+        *alpha_slot = a;
+        if (alpha_out) *alpha_out = a;
+    }
+}
+
 // K2 (NVFP4) pass 2: block of 16 = 2 lanes; Delta = Q_E4M3(fl32(amax / fl32(alpha * 6))),
 // S = fl32(alpha * Delta), u = fl32(x / S) (a true division: S is not a power of two).
 template <int IN, int OUT>
 __global__ void __launch_bounds__(256)
 fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
-                 const float *__restrict__ partial, int npart, void *__restrict__ x_hat,
-                 uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes,
-                 float *__restrict__ alpha_out, uint32_t *flag) {
-    const float alpha = tensor_alpha_from_partials(partial, npart);
-    if (alpha_out && blockIdx.x == 0 && threadIdx.x == 0) *alpha_out = alpha;
+                 const float *__restrict__ alpha_slot, void *__restrict__ x_hat, uint8_t *__restrict__ codes,
+                 uint8_t *__restrict__ scale_bytes, uint32_t *flag) {
+    const float alpha = *alpha_slot;
     const float alpha6 = alpha * 6.0f;
-    const int64_t nb = K / 16;
+    (void)cpr;
+    const int64_t e_row0 = row0 * K;  // rows are contiguous: chunk t starts at e_row0 + 8 t
     bool bad = false;
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
-        const uint32_t r = t / cpr, j = t - r * cpr;
-        const int64_t row = row0 + r, k0 = (int64_t)j * 8;
-        const int64_t e0 = row * K + k0;
+        const int64_t e0 = e_row0 + (int64_t)t * 8;
         float v[8];
         load8(X, IN, e0, v);
         float amax = 0.0f;
@@ -186,7 +201,7 @@ fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
         }
         if (x_hat) store8(x_hat, OUT, e0, out);
         if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
-        if (scale_bytes && (k0 % 16) == 0) scale_bytes[row * nb + k0 / 16] = (uint8_t)byte;
+        if (scale_bytes && (t & 1u) == 0) scale_bytes[e0 / 16] = (uint8_t)byte;
     }
     if (bad) raise_domain_flag(flag);
 }
@@ -197,32 +212,28 @@ fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
 template <int FMT, int IN>
 __global__ void __launch_bounds__(256)
 scales_init_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
-                   const float *__restrict__ partial, int npart, float *__restrict__ s_fp,
-                   float *__restrict__ c, int sb_log2, float *__restrict__ alpha_out) {
+                   const float *__restrict__ alpha_slot, float *__restrict__ s_fp, float *__restrict__ c,
+                   int sb_log2, float *__restrict__ alpha_out) {
     constexpr int B = block_of(FMT);
     float alpha = 1.0f;
-    if (FMT == kFmtNV) {
-        alpha = tensor_alpha_from_partials(partial, npart);
-        if (alpha_out && blockIdx.x == 0 && threadIdx.x == 0) *alpha_out = alpha;
-    } else if (alpha_out && blockIdx.x == 0 && threadIdx.x == 0) {
-        *alpha_out = 1.0f;
-    }
+    if (FMT == kFmtNV) alpha = *alpha_slot;  // alpha_out was written with the slot
+    else if (alpha_out && blockIdx.x == 0 && threadIdx.x == 0) *alpha_out = 1.0f;
     const int sb = 1 << sb_log2;
-    const int64_t nb = K / B, ns = K >> sb_log2;
+    (void)cpr;
+    const int64_t e_row0 = row0 * K;  // rows are contiguous: chunk t starts at e_row0 + 8 t
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
-        const uint32_t r = t / cpr, j = t - r * cpr;
-        const int64_t row = row0 + r, k0 = (int64_t)j * 8;
+        const int64_t e0 = e_row0 + (int64_t)t * 8;
         float v[8];
-        load8(W, IN, row * K + k0, v);
+        load8(W, IN, e0, v);
         float amax = 0.0f;
 #pragma unroll
         for (int i = 0; i < 8; i++) amax = fmaxf(amax, __builtin_fabsf(v[i]));
         amax = group_max(amax, B / 8);
-        if ((k0 % B) == 0) s_fp[row * nb + k0 / B] = FMT == kFmtMX ? amax / 6.0f : amax / (alpha * 6.0f);
+        if ((e0 % B) == 0) s_fp[e0 / B] = FMT == kFmtMX ? amax / 6.0f : amax / (alpha * 6.0f);
         if (sb >= 8) {
-            if ((k0 % sb) == 0) c[row * ns + (k0 >> sb_log2)] = 1.0f;
+            if ((e0 % sb) == 0) c[e0 >> sb_log2] = 1.0f;
         } else {
-            for (int i = 0; i < (8 >> sb_log2); i++) c[row * ns + (k0 >> sb_log2) + i] = 1.0f;
+            for (int i = 0; i < (8 >> sb_log2); i++) c[(e0 >> sb_log2) + i] = 1.0f;
         }
     }
 }
@@ -241,20 +252,20 @@ fq_bwd_kernel(const float *__restrict__ G, uint32_t nchunks, uint32_t cpr, int64
     const int sb = 1 << sb_log2;
     const int64_t nb = K / B, ns = K >> sb_log2;
     bool bad = false;
+    (void)cpr, (void)nb, (void)ns;
+    const int64_t e_row0 = row0 * K;  // rows are contiguous: chunk t starts at e_row0 + 8 t
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
-        const uint32_t r = t / cpr, j = t - r * cpr;
-        const int64_t row = row0 + r, k0 = (int64_t)j * 8;
-        const int64_t e0 = row * K + k0;
+        const int64_t e0 = e_row0 + (int64_t)t * 8;
         float w[8], g[8];
         load8(W, WDT, e0, w);
         load8(G, kF32, e0, g);
         uint32_t byte;
-        const float sdq = weight_sdq(FMT, s_fp[row * nb + k0 / B], alpha, byte, bad);
+        const float sdq = weight_sdq(FMT, s_fp[e0 / B], alpha, byte, bad);
         float cv[4] = {1.0f, 1.0f, 1.0f, 1.0f};
         const int ncoef = sb >= 8 ? 1 : 8 >> sb_log2;
         if (c) {
             for (int i = 0; i < ncoef; i++) {
-                cv[i] = c[row * ns + (k0 >> sb_log2) + i];
+                cv[i] = c[(e0 >> sb_log2) + i];
                 bad |= bad_coeff(cv[i]);
             }
         }
@@ -272,13 +283,12 @@ fq_bwd_kernel(const float *__restrict__ G, uint32_t nchunks, uint32_t cpr, int64
         }
         if (sb >= 8) {
             const float s = group_sum(tc[0], sb / 8);
-            if ((k0 % sb) == 0) grad_c[row * ns + (k0 >> sb_log2)] = -s / (cv[0] * cv[0]);
+            if ((e0 % sb) == 0) grad_c[e0 >> sb_log2] = -s / (cv[0] * cv[0]);
         } else {
-            for (int i = 0; i < ncoef; i++)
-                grad_c[row * ns + (k0 >> sb_log2) + i] = -tc[i] / (cv[i] * cv[i]);
+            for (int i = 0; i < ncoef; i++) grad_c[(e0 >> sb_log2) + i] = -tc[i] / (cv[i] * cv[i]);
         }
         const float s = group_sum(ts, B / 8);
-        if ((k0 % B) == 0) grad_s[row * nb + k0 / B] = FMT == kFmtNV ? s * alpha : s;
+        if ((e0 % B) == 0) grad_s[e0 / B] = FMT == kFmtNV ? s * alpha : s;
     }
     if (bad) raise_domain_flag(flag);
 }
@@ -295,7 +305,8 @@ static hipError_t for_row_ranges(int64_t rows, int64_t K, F &&launch) {
     for (int64_t r0 = 0; r0 < rows; r0 += max_rows) {
         const int64_t nr = std::min(max_rows, rows - r0);
         const uint32_t nchunks = (uint32_t)(nr * cpr);
-        const uint32_t grid = (uint32_t)std::min<int64_t>((nchunks + 255) / 256, kStreamGridCap);
+        // one chunk per thread: a full grid streams HBM faster than a capped grid-stride loop
+        const uint32_t grid = (uint32_t)((nchunks + 255) / 256);
         launch(r0, nchunks, (uint32_t)cpr, grid);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -326,10 +337,13 @@ hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64
     });
 }
 
-static hipError_t launch_absmax(int in_dt, const void *X, int64_t n, float *partial, hipStream_t st) {
+// NVFP4 tensor scale: kAbsmaxParts partial maxima, then alpha into partial[kAbsmaxParts]
+static hipError_t launch_tensor_alpha(int in_dt, const void *X, int64_t n, float *partial, float *alpha_out,
+                                      hipStream_t st) {
     const uint64_t nchunks = (uint64_t)n / 8;
     if (in_dt == kBF16) absmax_partial_kernel<kBF16><<<kAbsmaxParts, 256, 0, st>>>(X, nchunks, partial);
     else absmax_partial_kernel<kF32><<<kAbsmaxParts, 256, 0, st>>>(X, nchunks, partial);
+    tensor_alpha_kernel<<<1, 256, 0, st>>>(partial, kAbsmaxParts, partial + kAbsmaxParts, alpha_out);
     return hipGetLastError();
 }
 
@@ -344,10 +358,11 @@ hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t 
 #undef FQA
         });
     }
-    hipError_t e = launch_absmax(in_dt, X, rows * K, partial, st);
+    hipError_t e = launch_tensor_alpha(in_dt, X, rows * K, partial, alpha_out, st);
     if (e != hipSuccess) return e;
+    const float *slot = partial + kAbsmaxParts;
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-#define FQN(I, O) fq_act_nv_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, partial, kAbsmaxParts, x_hat, codes, scale_bytes, r0 == 0 ? alpha_out : nullptr, flag)
+#define FQN(I, O) fq_act_nv_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, slot, x_hat, codes, scale_bytes, flag)
         if (in_dt == kBF16) { if (out_dt == kBF16) FQN(kBF16, kBF16); else FQN(kBF16, kF32); }
         else { if (out_dt == kBF16) FQN(kF32, kBF16); else FQN(kF32, kF32); }
 #undef FQN
@@ -358,12 +373,13 @@ hipError_t launch_scales_init(int fmt, int in_dt, const void *W, int64_t rows, i
                               float *c, int sb, float *alpha_out, float *partial, hipStream_t st) {
     const int sbl = log2i(sb);
     if (fmt == kFmtNV) {
-        hipError_t e = launch_absmax(in_dt, W, rows * K, partial, st);
+        hipError_t e = launch_tensor_alpha(in_dt, W, rows * K, partial, alpha_out, st);
         if (e != hipSuccess) return e;
     }
+    const float *slot = partial + kAbsmaxParts;
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-        float *ao = r0 == 0 ? alpha_out : nullptr;
-#define SI(F, I) scales_init_kernel<F, I><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, partial, kAbsmaxParts, s_fp, c, sbl, ao)
+        float *ao = r0 == 0 && fmt == kFmtMX ? alpha_out : nullptr;
+#define SI(F, I) scales_init_kernel<F, I><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, slot, s_fp, c, sbl, ao)
         if (fmt == kFmtMX) { if (in_dt == kBF16) SI(kFmtMX, kBF16); else SI(kFmtMX, kF32); }
         else { if (in_dt == kBF16) SI(kFmtNV, kBF16); else SI(kFmtNV, kF32); }
 #undef SI

@@ -19,23 +19,37 @@ constexpr int kBF16 = 1;
 __host__ __device__ constexpr int block_of(int fmt) { return fmt == kFmtMX ? 32 : 16; }
 
 // ---- E2M1 --------------------------------------------------------------------------------------
-// Nearest magnitude index of a = |u| with ties to the even index and saturation at 6: the grid's
-// midpoints are 0.25, 0.75, 1.25, 1.75, 2.5, 3.5 and 5; a midpoint goes to the even neighbour, so
-// the comparison is strict where the lower neighbour has an even index and inclusive otherwise.
-// A NaN compares false everywhere and maps to index 0.
-__device__ __forceinline__ uint32_t e2m1_index(float a) {
-    return (uint32_t)(a > 0.25f) + (uint32_t)(a >= 0.75f) + (uint32_t)(a > 1.25f) +
-           (uint32_t)(a >= 1.75f) + (uint32_t)(a > 2.5f) + (uint32_t)(a >= 3.5f) +
-           (uint32_t)(a > 5.0f);
+// A code is sign << 3 | magnitude index (grid 0, 0.5, 1, 1.5, 2, 3, 4, 6). Q_E2M1 rounds |u| to the
+// nearest grid value, a midpoint (0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5) going to the even index, and
+// saturates at 6; a NaN takes index 0 with its sign bit. gfx950's FP4 conversion rounds and
+// saturates exactly so (pinned against the threshold form over every bf16 value and the fp32
+// neighbourhoods of every midpoint by a GPU test); it gives a NaN the largest magnitude, so NaNs are
+// replaced by a signed zero first.
+__device__ __forceinline__ float e2m1_nan_to_zero(float u) {
+    return u == u ? u : __uint_as_float(__float_as_uint(u) & 0x80000000u);
 }
 
-// fp32 bit pattern of the magnitude with index idx: for idx >= 2 it is (1 + (idx & 1) / 2) *
-// 2^((idx >> 1) - 1); index 1 is 0.5 and index 0 is 0.
-__device__ __forceinline__ uint32_t e2m1_magnitude_bits(uint32_t idx) {
-    const uint32_t hi = (((idx >> 1) + 126u) << 23) | ((idx & 1u) << 22);
-    // integer masks instead of a select chain, which the compiler turns into a divergent branch
-    const uint32_t ge2 = 0u - (uint32_t)(idx >= 2u), is1 = 0u - (uint32_t)(idx == 1u);
-    return (hi & ge2) | (0x3F000000u & is1);
+// Codes of u0, u1 written into byte `sel` of `word` (u0 in the low nibble).
+template <int SEL>
+__device__ __forceinline__ uint32_t e2m1_code2(uint32_t word, float u0, float u1) {
+    return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, e2m1_nan_to_zero(u0), e2m1_nan_to_zero(u1), 1.0f, SEL);
+}
+
+__device__ __forceinline__ uint32_t e2m1_code(float u) { return e2m1_code2<0>(0u, u, 0.0f) & 0xFu; }
+
+// Grid values of the two codes in byte SEL of `word` (low nibble first), signed.
+template <int SEL>
+__device__ __forceinline__ void e2m1_value2(uint32_t word, float &v0, float &v1) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    const f32x2 v = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(word, 1.0f, SEL);
+    v0 = v.x;
+    v1 = v.y;
+}
+
+__device__ __forceinline__ float e2m1_value(uint32_t code) {
+    float v0, v1;
+    e2m1_value2<0>(code, v0, v1);
+    return v0;
 }
 
 // ---- E8M0 (scale rounded up to a power of two) ---------------------------------------------------
@@ -144,16 +158,15 @@ struct Quantized {
 __device__ __forceinline__ Quantized quantize_element(float x, float sq, float sdq, bool ste_clip) {
     // both cases are computed and the result masked: no divergent branch per element
     Quantized r;
+    const uint32_t keep = 0u - (uint32_t)!(sdq == 0.0f || sq == 0.0f);  // all ones unless a scale is zero
+    const float u = x / (keep ? sq : 1.0f);
     const uint32_t sign = __float_as_uint(x) & 0x80000000u;
-    const bool zero = sdq == 0.0f || sq == 0.0f;
-    const uint32_t keep = 0u - (uint32_t)!zero;  // all ones unless the scale is zero
-    const float u = x / (zero ? 1.0f : sq);
-    const float a = __builtin_fabsf(u);
-    const uint32_t idx = e2m1_index(a) & keep;    // index 0 for a zero scale
+    // a zero scale gives index 0: the code keeps only the sign
+    const uint32_t code = e2m1_code(u) & (keep | 8u);
     r.u = __uint_as_float(__float_as_uint(u) & keep);
-    r.q = __uint_as_float(e2m1_magnitude_bits(idx) | sign);
-    r.code = (sign >> 28) | idx;
-    r.m = !zero && (ste_clip ? (a <= 6.0f) : true);
+    r.code = (code & 7u) | (sign >> 28);
+    r.q = __uint_as_float(__float_as_uint(e2m1_value(r.code & 7u)) | sign);
+    r.m = keep && (ste_clip ? (__builtin_fabsf(u) <= 6.0f) : true);
     r.xhat = r.q * sdq;
     return r;
 }
