@@ -31,8 +31,8 @@ def parse():
     p.add_argument("--workload", default="block2560_mxfp4")
     p.add_argument("--tokens", type=int, default=0, help="override the token count (0 = the workload's)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-sample-tokens", type=int, default=16384)
-    p.add_argument("--cpu-sample-rows", type=int, default=128)
+    p.add_argument("--cpu-sample-tokens", type=int, default=32768)
+    p.add_argument("--cpu-sample-rows", type=int, default=512)
     p.add_argument("--copy-calibration", action="store_true",
                    help="run an untimed 1 GiB device copy first (a known-size reference for HBM counters)")
     return p.parse_args()
