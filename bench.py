@@ -20,6 +20,7 @@ sys.path.insert(0, REPO)
 
 METRIC = "ms per fwd+bwd scale-learning step per decoder block; fake-quant GB/s"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP4_TFLOPS = 10100.0   # MI355X dense MXFP4 MFMA
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 
 
@@ -33,6 +34,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=32768)
     p.add_argument("--cpu-sample-rows", type=int, default=512)
+    p.add_argument("--fwd-operands", choices=("bf16", "mxfp4"), default="bf16",
+                   help="forward reconstruction GEMM from bf16 X_hat / W_hat, or (MXFP4 workloads) from their "
+                        "packed FP4 codes and E8M0 scales on the block-scaled FP4 MFMA")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run an untimed 1 GiB device copy first (a known-size reference for HBM counters)")
     return p.parse_args()
@@ -121,6 +125,18 @@ def main():
                            gs=torch.empty_like(s), gc=torch.empty_like(c),
                            loss=torch.empty(1, dtype=torch.float64, device=dev)))
     x_hat = {src: torch.empty_like(x) for src, x in acts.items()}
+    mx_primary = args.fwd_operands == "mxfp4"
+    if mx_primary and fmt != 0:
+        print("--fwd-operands mxfp4 needs an MXFP4 workload", file=sys.stderr)
+        sys.exit(2)
+    mx_possible = fmt == 0 and all(l.K % 128 == 0 and l.N % 8 == 0 for l in w.linears)
+    if mx_possible:  # packed operands of an MXFP4 forward: codes [rows][K/2] and E8M0 bytes [rows][K/32]
+        x_codes = {src: torch.empty(M, x.shape[1] // 2, dtype=torch.uint8, device=dev) for src, x in acts.items()}
+        x_scales = {src: torch.empty(M, x.shape[1] // 32, dtype=torch.uint8, device=dev) for src, x in acts.items()}
+        for L in layers:
+            N_, K_ = L["W"].shape
+            L["Wc"] = torch.empty(N_, K_ // 2, dtype=torch.uint8, device=dev)
+            L["Ws"] = torch.empty(N_, K_ // 32, dtype=torch.uint8, device=dev)
     max_n = max(l.N for l in w.linears)
     dY_buf = torch.empty(M * max_n, dtype=acts[w.linears[0].source].dtype, device=dev)
     q = F.qconfig(fmt, sb)
@@ -129,83 +145,121 @@ def main():
     ws_bwd = F.workspace(max(F.workspace_size(F.CALL_RECON_GEMM_BWD, q, M, l.N, l.K) for l in w.linears))
     torch.cuda.synchronize()
 
-    def step(timer):
+    def step(timer, mx_fwd):
         for src, x in acts.items():
             rows, K = x.shape
-            timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src]), rows * K)
+            if mx_fwd:
+                timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src],
+                                                                   codes_out=x_codes[src], scales_out=x_scales[src]),
+                          rows * K)
+            else:
+                timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src]), rows * K)
         for L in layers:
             lin = L["lin"]
             xh = x_hat[lin.source]
             dY = dY_buf[:M * lin.N].view(M, lin.N)
-            timer.run("fakequant_weight",
-                      lambda: F.fakequant_fwd(L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws_fq, out=L["W_hat"]),
-                      lin.N * lin.K)
-            timer.run("recon_gemm_fwd",
-                      lambda: F.recon_gemm_fwd(xh, L["W_hat"], L["Y"], ws=ws_fwd, out=dY, loss=L["loss"]),
-                      2 * M * lin.N * lin.K)
+            if mx_fwd:
+                # the forward's weight operand is the deployable export: codes + E8M0 bytes, no bf16 W_hat
+                timer.run("fakequant_weight",
+                          lambda: F.export_packed(L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws_fq,
+                                                  out=(L["Wc"], L["Ws"])), lin.N * lin.K)
+                timer.run("recon_gemm_fwd",
+                          lambda: F.recon_gemm_fwd_mxfp4(x_codes[lin.source], x_scales[lin.source], L["Wc"], L["Ws"],
+                                                         L["Y"], ws=ws_fwd, out=dY, loss=L["loss"]),
+                          2 * M * lin.N * lin.K)
+            else:
+                timer.run("fakequant_weight",
+                          lambda: F.fakequant_fwd(L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws_fq, out=L["W_hat"]),
+                          lin.N * lin.K)
+                timer.run("recon_gemm_fwd",
+                          lambda: F.recon_gemm_fwd(xh, L["W_hat"], L["Y"], ws=ws_fwd, out=dY, loss=L["loss"]),
+                          2 * M * lin.N * lin.K)
             timer.run("recon_gemm_bwd",
                       lambda: F.recon_gemm_bwd(dY, xh, L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws_bwd,
                                                out=(L["gs"], L["gc"])),
                       2 * M * lin.N * lin.K)
 
-    for _ in range(args.warmup):
-        step(Timer(torch))
-    torch.cuda.synchronize()
-    if F.check_flags(ws_fq) != F.OK:
-        raise RuntimeError("domain error in the warm-up steps")
+    def run(mx_fwd):
+        """Warm-up, then exactly args.steps timed steps; -> (ms per step, per-family summary)."""
+        for _ in range(args.warmup):
+            step(Timer(torch), mx_fwd)
+        torch.cuda.synchronize()
+        if F.check_flags(ws_fq) != F.OK:
+            raise RuntimeError("domain error in the warm-up steps")
+        timer = Timer(torch)
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            step(timer, mx_fwd)
+        end.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / args.steps, timer.summary()
 
-    timer = Timer(torch)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
-        step(timer)
-    end.record()
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
-    ms_per_step = total_ms / args.steps
-    kern = timer.summary()
+    mx_fwd = mx_primary
+    ms_per_step, kern = run(mx_fwd)
     block_loss = float(sum(L["loss"].item() for L in layers))
 
     # ---- algorithmic work ----
     # fake quantisation bytes per element: activations read 2 + write 2 (bf16) (+2 for the NVFP4
-    # tensor-absmax pass); weights read W 2 + S_fp 4/B + c 4/sb, write W_hat 2
+    # tensor-absmax pass, + 0.5 + 1/32 for the codes and scale bytes of an MXFP4 forward); weights
+    # read W 2 + S_fp 4/B + c 4/sb, write W_hat 2 (or, for an MXFP4 forward, codes 0.5 + bytes 1/32)
     esz = 2 if w.dtype == "bf16" else 4
-    act_b = (2 * esz + (esz if fmt == 1 else 0))
-    wt_b = 2 * esz + 4.0 / B + 4.0 / sb
+    act_b = (2 * esz + (esz if fmt == 1 else 0)) + (0.5 + 1.0 / 32 if mx_fwd else 0.0)
+    wt_b = esz + 4.0 / B + 4.0 / sb + ((0.5 + 1.0 / 32) if mx_fwd else esz)
     fq_bytes = kern["fakequant_act"]["units"] * act_b + kern["fakequant_weight"]["units"] * wt_b
     fq_ms = kern["fakequant_act"]["total_ms"] + kern["fakequant_weight"]["total_ms"]
     gemm_flops = kern["recon_gemm_fwd"]["units"] + kern["recon_gemm_bwd"]["units"]
     gemm_ms = kern["recon_gemm_fwd"]["total_ms"] + kern["recon_gemm_bwd"]["total_ms"]
 
+    peaks = {"recon_gemm_fwd": PEAK_FP4_TFLOPS if mx_fwd else PEAK_BF16_TFLOPS, "recon_gemm_bwd": PEAK_BF16_TFLOPS}
+    gemm = {k: {"TFLOPs": round(kern[k]["units"] / (kern[k]["total_ms"] * 1e-3) / 1e12, 1), "peak": peaks[k],
+                "frac": round(kern[k]["units"] / (kern[k]["total_ms"] * 1e-3) / 1e12 / peaks[k], 4)}
+            for k in ("recon_gemm_fwd", "recon_gemm_bwd")}
     dominant = max(("recon_gemm_fwd", "recon_gemm_bwd"), key=lambda k: kern[k]["total_ms"])
     d = kern[dominant]
     per_launch_flops = d["units"] / d["launches"]
     achieved = per_launch_flops / (d["avg_ms"] * 1e-3) / 1e12
     src_hash = kernel_source_hash()
-    kname = {"recon_gemm_fwd": "fwd_mfma_kernel", "recon_gemm_bwd": "bwd_mfma_kernel"}[dominant]
-    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_from_profile(kname, src_hash),
+    kname = {"recon_gemm_fwd": "fwd_mfma_kernel_mx" if mx_fwd else "fwd_mfma_kernel",
+             "recon_gemm_bwd": "bwd_mfma_kernel"}[dominant]
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peaks[dominant], "unit": "TFLOP/s",
+                "frac": round(achieved / peaks[dominant], 4), "traffic": traffic_from_profile(kname, src_hash),
                 "kernel": kname, "avg_launch_ms": round(d["avg_ms"], 4), "launches": d["launches"],
                 "flops_per_launch": per_launch_flops}
 
     result = {
         "metric": METRIC, "value": round(ms_per_step, 4), "unit": "ms per step", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if esz == 2 else "f32",
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": ("bf16+mxfp4" if mx_fwd else "bf16") if esz == 2 else "f32",
         "data": "synthetic (seeded; shapes and distributions of the calibration workload)",
         "config": {"workload": w.name, "tokens": M, "format": "mxfp4" if fmt == 0 else "nvfp4", "sub_block": sb,
-                   "linears": {l.name: [l.N, l.K] for l in w.linears}},
+                   "fwd_operands": args.fwd_operands, "linears": {l.name: [l.N, l.K] for l in w.linears}},
         "roofline": roofline,
         "fakequant_GBps": round(fq_bytes / (fq_ms * 1e-3) / 1e9, 1),
         "fakequant_frac_hbm": round(fq_bytes / (fq_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
         "gemm_TFLOPs": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
         "gemm_frac_bf16": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "gemm": gemm,
         "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "total_ms_per_step": round(v["total_ms"] / args.steps, 4),
                         "launches_per_step": v["launches"] // args.steps} for k, v in kern.items()},
         "block_loss": block_loss,
         "source_hash": src_hash,
     }
+    if mx_possible and not mx_primary:
+        # the same step with the forward on the packed MXFP4 operands (block-scaled FP4 MFMA: exact
+        # products, fp32 sums, the bf16 path's result up to the accumulation order), same inputs
+        mx_ms, mx_kern = run(True)
+        mx_loss = float(sum(L["loss"].item() for L in layers))
+        f = mx_kern["recon_gemm_fwd"]
+        result["mxfp4_forward"] = {
+            "ms_per_step": round(mx_ms, 4), "block_loss": mx_loss,
+            "recon_gemm_fwd": {"TFLOPs": round(f["units"] / (f["total_ms"] * 1e-3) / 1e12, 1),
+                               "peak_fp4": PEAK_FP4_TFLOPS,
+                               "frac_fp4": round(f["units"] / (f["total_ms"] * 1e-3) / 1e12 / PEAK_FP4_TFLOPS, 4)},
+            "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "total_ms_per_step": round(v["total_ms"] / args.steps, 4)}
+                        for k, v in mx_kern.items()}}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens, args.cpu_sample_rows)
     print(json.dumps(result), flush=True)

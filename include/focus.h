@@ -137,6 +137,21 @@ focus_status focus_recon_gemm_fwd(const void *X_hat, const void *W_hat, int op_d
                                   double *loss_out, double *col_sq_opt,
                                   void *ws, size_t ws_bytes, focus_stream stream);
 
+/* Reconstruction GEMM forward from packed MXFP4 operands, with the same epilogue and outputs as
+ * focus_recon_gemm_fwd (Y_ref and dY bf16). Under MXFP4, X_hat and W_hat are exactly FP4 codes
+ * times E8M0 block scales along K (Sec. 3.1, Eq. 1 and 3), so Y_hat = X_hat W_hat^T is computed from
+ * that representation with the block-scaled FP4 MFMA: every product is exact and the sums are
+ * accumulated in fp32, i.e. the same result as the bf16 path up to the accumulation order.
+ *   X_codes [M][K/2], W_codes [N][K/2]: two E2M1 codes per byte, even k in the low nibble (the
+ *     codes_opt / packed layout of focus_fakequant_fwd and focus_export_packed), 16-byte aligned;
+ *   X_scales [M][K/32], W_scales [N][K/32]: E8M0 bytes (e + 127), 4-byte aligned.
+ *   Requires K % 128 == 0 and N % 8 == 0 (FOCUS_ERR_SHAPE otherwise). The workspace is that of
+ *   FOCUS_CALL_RECON_GEMM_FWD. */
+focus_status focus_recon_gemm_fwd_mxfp4(const uint8_t *X_codes, const uint8_t *X_scales, const uint8_t *W_codes,
+                                        const uint8_t *W_scales, int64_t M, int64_t N, int64_t K,
+                                        const void *Y_ref, void *dY, double *loss_out, double *col_sq_opt,
+                                        void *ws, size_t ws_bytes, focus_stream stream);
+
 /* Reconstruction GEMM backward with the fused straight-through epilogue.
  *   G = dY^T X_hat ([N][K], the reduction runs over the M tokens, fp32 accumulation) is formed
  *   tile by tile and reduced at once into grad_s [N][K/B] and grad_c [N][K/sub_block] exactly as

@@ -163,6 +163,25 @@ focus_status focus_recon_gemm_fwd(const void *X_hat, const void *W_hat, int op_d
                                        (hipStream_t)stream));
 }
 
+focus_status focus_recon_gemm_fwd_mxfp4(const uint8_t *X_codes, const uint8_t *X_scales, const uint8_t *W_codes,
+                                        const uint8_t *W_scales, int64_t M, int64_t N, int64_t K,
+                                        const void *Y_ref, void *dY, double *loss_out, double *col_sq_opt,
+                                        void *ws, size_t ws_bytes, focus_stream stream) {
+    if (!X_codes || !X_scales || !W_codes || !W_scales || !dY) return FOCUS_ERR_NULL;
+    if (Y_ref && !loss_out) return FOCUS_ERR_NULL;
+    if (M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return FOCUS_ERR_SHAPE;
+    if (K % 128 != 0 || N % 8 != 0) return FOCUS_ERR_SHAPE;
+    if ((M > 0 && K > kMaxElems / M) || (N > 0 && K > kMaxElems / N) || (M > 0 && N > kMaxElems / M))
+        return FOCUS_ERR_SHAPE;
+    if (!all_aligned({X_codes, W_codes, Y_ref, dY})) return FOCUS_ERR_SHAPE;
+    if ((reinterpret_cast<uintptr_t>(X_scales) | reinterpret_cast<uintptr_t>(W_scales)) & 3u) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, fwd_ws(M, N, K)));
+    if (M == 0 || N == 0) return FOCUS_OK;
+    if (!mfma_fwd_mx_supported(M, N, K)) return FOCUS_ERR_SHAPE;
+    return hip_status(launch_recon_fwd_mx(X_codes, X_scales, W_codes, W_scales, M, N, K, Y_ref, dY, loss_out,
+                                          col_sq_opt, ws, (hipStream_t)stream));
+}
+
 focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const void *X_hat, int op_dtype,
                                   int64_t M, int64_t N, int64_t K, const void *W, int w_dtype,
                                   const float *s_fp, const float *c, const float *alpha, float *grad_s,

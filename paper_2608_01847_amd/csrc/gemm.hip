@@ -289,9 +289,26 @@ hipError_t launch_recon_fwd(const FwdPlan &p, int op_dt, const void *X, const vo
         if (e != hipSuccess) return e;
     }
     if (!Yref) return hipSuccess;
-    colsum_kernel<<<(unsigned)cdiv(N, 16), 256, 0, st>>>(colpart, p.mtiles, N, col_sq);
+    return launch_fwd_finish(p.mtiles, M, N, colpart, col_sq, loss_out, st);
+}
+
+hipError_t launch_fwd_finish(int64_t mtiles, int64_t M, int64_t N, const double *colpart, double *col_sq,
+                             double *loss_out, hipStream_t st) {
+    colsum_kernel<<<(unsigned)cdiv(N, 16), 256, 0, st>>>(colpart, mtiles, N, col_sq);
     if (loss_out) loss_kernel<<<1, 256, 0, st>>>(col_sq, N, 1.0 / ((double)M * (double)N), loss_out);
     return hipGetLastError();
+}
+
+hipError_t launch_recon_fwd_mx(const void *Xc, const void *Xs, const void *Wc, const void *Ws, int64_t M, int64_t N,
+                               int64_t K, const void *Yref, void *dY, double *loss_out, double *col_sq_opt, void *ws,
+                               hipStream_t st) {
+    const int64_t mtiles = cdiv(M, kMfmaTileM);
+    double *colpart = reinterpret_cast<double *>(reinterpret_cast<char *>(ws) + kWsHeader);
+    double *col_sq = col_sq_opt ? col_sq_opt : colpart + mtiles * N;
+    const float dscale = (float)(2.0 / ((double)M * (double)N));
+    hipError_t e = launch_fwd_mfma_mx(Xc, Xs, Wc, Ws, M, N, K, Yref, dY, dscale, colpart, st);
+    if (e != hipSuccess || !Yref) return e;
+    return launch_fwd_finish(mtiles, M, N, colpart, col_sq, loss_out, st);
 }
 
 hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int ste_clip, const void *dY,

@@ -79,26 +79,27 @@ __device__ __forceinline__ uint32_t fwd_off(uint32_t row, uint32_t chunk) {
 // A direct-to-LDS load writes lane L's 16 bytes at LDS byte 16 L from the instruction's base, so
 // each wave fills 1 KB blocks: lane L of block q lands in row 16 q + L / 4, physical chunk L % 4,
 // which must hold logical chunk (L % 4) ^ fwd_key(row). The key depends on row bits 1-3 only,
-// i.e. on L alone, so one k offset serves all four blocks. Each thread's byte offsets at k0 = 0
-// are fixed for the whole tile.
+// i.e. on L alone, so one step offset serves all four blocks. Offsets are in bytes of a row of
+// `pitch` bytes (2 K for bf16 operands, K / 2 for packed FP4 codes); each thread's offsets at the
+// first step are fixed for the whole tile.
 struct FwdDma {
     uint32_t lane_off[4];
-    uint32_t kk;  // k offset of this lane's chunk inside a step
-    __device__ __forceinline__ void init(int64_t K, int wave, int lane) {
-        kk = (uint32_t)(((uint32_t)(lane & 3) ^ fwd_key((uint32_t)lane >> 2)) * 8);
+    uint32_t cb;  // byte offset of this lane's chunk inside a step's 64 bytes of a row
+    __device__ __forceinline__ void init(int64_t pitch, int wave, int lane) {
+        cb = ((uint32_t)(lane & 3) ^ fwd_key((uint32_t)lane >> 2)) * 16u;
 #pragma unroll
         for (int i = 0; i < 4; i++) {
             const uint32_t row = (wave * 4 + i) * 16 + (lane >> 2);
-            lane_off[i] = (row * (uint32_t)K + kk) * 2u;
+            lane_off[i] = row * (uint32_t)pitch + cb;
         }
     }
-    // Offset bits of the step starting at k0: chunks at or past K get bit 31 set, so they are out
-    // of range and read as zeros (an arithmetic mask, not a branch).
-    __device__ __forceinline__ uint32_t step_bad(int64_t K, int64_t k0) const {
-        const int32_t lim = (int32_t)(K - k0);
-        return ((uint32_t)(lim - 1 - (int32_t)kk) >> 31) << 31;
+    // Offset bits of the step whose row bytes start at b0: chunks at or past the row end get bit
+    // 31 set, so they are out of range and read as zeros (an arithmetic mask, not a branch).
+    __device__ __forceinline__ uint32_t step_bad(int64_t pitch, int64_t b0) const {
+        const int32_t lim = (int32_t)(pitch - b0);
+        return ((uint32_t)(lim - 1 - (int32_t)cb) >> 31) << 31;
     }
-    // Load i (0..3) of this wave for the step starting at k0 (base = 2 k0).
+    // Load i (0..3) of this wave for the step whose row bytes start at b0 = base.
     __device__ __forceinline__ void issue_one(__amdgpu_buffer_rsrc_t rs, uint32_t base, uint32_t bad,
                                               lds_char *dst, int wave, int i) const {
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst + (wave * 4 + i) * 1024, 16,
@@ -267,13 +268,27 @@ __device__ __forceinline__ void static_for(F &&f) {
 }  // namespace
 
 // ------------------------------------------------------------------------------------------------
-template <bool MSE>  // MSE epilogue against Y_ref, or the plain product
+// Forward reconstruction GEMM, Y_hat = X_hat W_hat^T with the MSE epilogue (or the plain product).
+// Operands are bf16 (MX == false) or packed MXFP4 (MX == true): codes [rows][K / 2] (two per byte,
+// even k in the low nibble) and E8M0 scale bytes [rows][K / 32], exactly the values X_hat and W_hat
+// hold under MXFP4, multiplied by the block-scaled FP4 MFMA. Both modes stage 64 bytes of each
+// operand row per step (32 bf16 or 128 FP4 k), so the LDS geometry, swizzle, pipeline and epilogue
+// are shared.
+template <bool MSE, bool MX>
 __global__ void __launch_bounds__(kThreads, 1)
-fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, int64_t M, int64_t N, int64_t K,
+fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const uint8_t *__restrict__ Xs,
+                const uint8_t *__restrict__ Ws, int64_t M, int64_t N, int64_t K,
                 const uint16_t *__restrict__ Yref, uint16_t *__restrict__ dY, float dscale,
                 double *__restrict__ colpart, int tiles_n) {
-    __shared__ __attribute__((aligned(16))) char smem[kFwdStages * kFwdStageBytes];
+    constexpr int S = MX ? 4 : kFwdStages;                          // LDS stages
+    constexpr int kLoads = MX ? 10 : 8;                             // loads per slot per thread
+    constexpr int kKStep = MX ? 128 : kFwdStep;                     // k per step
+    constexpr int kScaleBytes = MX ? 2048 : 0;                      // per stage: [256][4] bytes X, then W
+    constexpr int kStage = kFwdStageBytes + kScaleBytes;
+    static_assert(S * kStage <= kLdsBytes, "forward stages fit the LDS");
+    __shared__ __attribute__((aligned(16))) char smem[S * kStage];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
+    const int lr = lane & 31, lh = lane >> 5;
     uint32_t tm, tn;
     grouped_tile(xcd_tile(blockIdx.x, gridDim.x), gridDim.x / tiles_n, tiles_n, tm, tn);
     const int64_t m0 = (int64_t)tm * kTile, n0 = (int64_t)tn * kTile;
@@ -285,38 +300,53 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
 #pragma unroll
         for (int j = 0; j < 4; j++) acc[i][j] = zero;
 
-    // S = kFwdStages LDS stages of 32 of K. Load "slot" j fills stage j % S: for j < nk it is
-    // step j of the operands; slots nk .. nk + 3 bring the four 64-row quarters of the Y_ref tile
-    // (zeros in the plain mode), so the epilogue's input arrives while the last steps' MFMAs run.
-    // Every slot is 8 loads per thread, which is what the vmcnt waits below count on.
-    constexpr int S = kFwdStages;
+    // S LDS stages, one step each. Load "slot" j fills stage j % S: for j < nk it is step j of the
+    // operands; slots nk .. nk + 3 bring the four 64-row quarters of the Y_ref tile (zeros in the
+    // plain mode), so the epilogue's input arrives while the last steps' MFMAs run. Every slot is
+    // kLoads loads per thread, which is what the vmcnt waits below count on.
     lds_char *const lsm = (lds_char *)smem;
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-    FwdDma dma;  // X and W panels have the same row length K, so one set of offsets serves both
-    dma.init(K, wave_u, lane);
-    const __amdgpu_buffer_rsrc_t ra = make_rsrc(X + m0 * K, (M - m0) * K * 2);
-    const __amdgpu_buffer_rsrc_t rb = make_rsrc(W + n0 * K, (N - n0) * K * 2);
+    const int64_t pitch = MX ? K / 2 : K * 2;  // bytes of an operand row
+    FwdDma dma;  // X and W rows have the same length, so one set of offsets serves both
+    dma.init(pitch, wave_u, lane);
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(static_cast<const char *>(X) + m0 * pitch, (M - m0) * pitch);
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc(static_cast<const char *>(W) + n0 * pitch, (N - n0) * pitch);
+    const int64_t spitch = K / 32;             // scale bytes of a row (a multiple of 4 in MX mode)
+    const __amdgpu_buffer_rsrc_t rxs = make_rsrc(MX ? Xs + m0 * spitch : Xs, MX ? (M - m0) * spitch : 0);
+    const __amdgpu_buffer_rsrc_t rws = make_rsrc(MX ? Ws + n0 * spitch : Ws, MX ? (N - n0) * spitch : 0);
+    const __amdgpu_buffer_rsrc_t r_none = make_rsrc(dY, 0);
     const __amdgpu_buffer_rsrc_t rs_y = make_rsrc(MSE ? Yref + m0 * N : dY, MSE ? (M - m0) * N * 2 : 0);
     const __amdgpu_buffer_rsrc_t rs_d = make_rsrc(dY + m0 * N, (M - m0) * N * 2);
     const uint32_t N32 = (uint32_t)N;  // offsets are below 256 * N * 2 < 2^31 (checked when chosen)
-    const int64_t nk = (K + kFwdStep - 1) / kFwdStep;
+    const int64_t nk = (K + kKStep - 1) / kKStep;
     // Quarter q of the output tile holds tile rows q*32 + 0..31 and 128 + q*32 + 0..31 (local rows
     // 0..63), i.e. accumulator block i == q of every wave. In LDS a quarter is 64 rows of 512 bytes;
     // the two 64-byte halves of each 128-byte span are swapped on rows with bit 2 set, so the lanes
     // reading rows r and r + 4 of one column group use different banks.
     auto q_row = [](uint32_t rl, uint32_t q) { return (rl >> 5) * 128u + q * 32u + (rl & 31u); };
     auto q_off = [](uint32_t rl, uint32_t chunk) { return rl * 512u + ((chunk ^ (((rl >> 2) & 1u) << 2)) << 4); };
-    auto stage = [&](int sidx) { return lsm + sidx * kFwdStageBytes; };
-    // Load i (0..7) of slot j into stage st: loads 0-3 bring X rows, 4-7 W rows of an operand
-    // step; a Y_ref quarter is 32 one-KB blocks of two rows each, this wave filling blocks
-    // 8 wave .. 8 wave + 7 (lane L of block b lands in local row 2 b + L / 32, physical chunk L % 32).
+    auto stage = [&](int sidx) { return lsm + sidx * kStage; };
+    // Load i of slot j into stage st: loads 0-3 bring X rows, 4-7 W rows of an operand step, and in
+    // MX mode 8 / 9 the step's X / W scale bytes (4 bytes of each of 256 rows; this wave's 64 rows,
+    // lane L's 4 bytes landing at byte 4 L). A Y_ref quarter is 32 one-KB blocks of two rows
+    // each, this wave filling blocks 8 wave .. 8 wave + 7 (lane L of block b lands in local row
+    // 2 b + L / 32, physical chunk L % 32); in MX mode its loads 8 and 9 are empty and only write
+    // zeros into the stage's scale bytes.
     auto issue_op = [&](lds_char *st, int64_t j, int i) {
-        const int64_t k0 = j * kFwdStep;
-        const uint32_t base = (uint32_t)k0 * 2u, bad = dma.step_bad(K, k0);
+        const uint32_t base = (uint32_t)j * 64u, bad = dma.step_bad(pitch, base);  // 64 row bytes per step
         if (i < 4) dma.issue_one(ra, base, bad, st, wave_u, i);
-        else dma.issue_one(rb, base, bad, st + kFwdOpBytes, wave_u, i - 4);
+        else if (i < 8) dma.issue_one(rb, base, bad, st + kFwdOpBytes, wave_u, i - 4);
+        else {
+            const uint32_t so = (uint32_t)(wave_u * 64 + lane) * (uint32_t)spitch + (uint32_t)j * 4u;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(i == 8 ? rxs : rws, st + kFwdStageBytes + (i - 8) * 1024 + wave_u * 256, 4,
+                                                     (int)so, 0, 0, 0);
+        }
     };
     auto issue_y = [&](lds_char *st, int64_t j, int i) {
+        if (MX && i >= 8) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(r_none, st + kFwdStageBytes + (i - 8) * 1024 + wave_u * 256, 4, 0, 0, 0, 0);
+            return;
+        }
         const uint32_t q = (uint32_t)((j - nk) & 3);
         const uint32_t blk = wave_u * 8 + i, rl = 2 * blk + (lane >> 5);
         const uint32_t chunk = (uint32_t)(lane & 31) ^ (((rl >> 2) & 1u) << 2);
@@ -329,10 +359,33 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
         lds_char *st = stage((int)(j % S));
         if (j < nk) {
 #pragma unroll
-            for (int i = 0; i < 8; i++) issue_op(st, j, i);
+            for (int i = 0; i < kLoads; i++) issue_op(st, j, i);
         } else {
 #pragma unroll
-            for (int i = 0; i < 8; i++) issue_y(st, j, i);
+            for (int i = 0; i < kLoads; i++) issue_y(st, j, i);
+        }
+    };
+    // MX mode: this lane's scale words (rows of its X / W fragments) of a stage, shifted so that
+    // byte 0 / 2 holds the scale of the first / second 64 k it covers (lane half lh takes the odd
+    // 32-k block of each 64)
+    auto load_scales = [&](const char *st, uint32_t (&sa)[4], uint32_t (&sb)[4]) {
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            sa[i] = *reinterpret_cast<const uint32_t *>(st + kFwdStageBytes + (wm * 128 + i * 32 + lr) * 4) >> (8 * lh);
+            sb[i] = *reinterpret_cast<const uint32_t *>(st + kFwdStageBytes + 1024 + (wn * 128 + i * 32 + lr) * 4) >> (8 * lh);
+        }
+    };
+    auto mfma = [&](auto i, auto j, const Frags &fr, const uint32_t (&sa)[4], const uint32_t (&sb)[4], auto half) {
+        if constexpr (MX) {
+            typedef int v4i __attribute__((ext_vector_type(4)));
+            typedef int v8i __attribute__((ext_vector_type(8)));
+            const v4i a4 = __builtin_bit_cast(v4i, fr.a[i]), b4 = __builtin_bit_cast(v4i, fr.b[j]);
+            const v8i a8 = {a4[0], a4[1], a4[2], a4[3], 0, 0, 0, 0}, b8 = {b4[0], b4[1], b4[2], b4[3], 0, 0, 0, 0};
+            constexpr int ops = decltype(half)::value * 2;
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, acc[i][j], 4, 4, ops, (int)sa[i], ops,
+                                                                        (int)sb[j]);
+        } else {
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr.a[i], fr.b[j], acc[i][j], 0, 0, 0);
         }
     };
 #pragma unroll
@@ -342,34 +395,45 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
     // fragments of step kt + 1 can be read while step kt's MFMAs run, and stage (kt - 1) % S,
     // last read in step kt - 1, can be refilled with slot kt + S - 1. A bare s_barrier:
     // __syncthreads would also wait for the loads still in flight.
-    FOCUS_WAIT_VMCNT(8 * (S - 3));
+    FOCUS_WAIT_VMCNT(kLoads * (S - 3));
     asm volatile("s_barrier" ::: "memory");
     Frags f, g;
+    uint32_t sa[4], sb[4], na[4], nb[4];
     load_frags_fwd(f, smem, smem + kFwdOpBytes, 0, wm, wn, lane);
-    // One step (sc = kt % S). The 8 loads of slot kt + S - 1 go out one after every second MFMA
-    // of the first half: issued back to back they would fill the texture unit's queue, and a wave
-    // stalled on a full queue issues no MFMA. The scheduling barriers keep the compiler from
-    // regrouping them.
+    if constexpr (MX) load_scales(smem, na, nb);
+    // One step (sc = kt % S). The loads of slot kt + S - 1 go out between the MFMAs of the first
+    // half (8 after every second one, MX's scale loads after the first and the ninth): issued back
+    // to back they would fill the texture unit's queue, and a wave stalled on a full queue issues
+    // no MFMA. The scheduling barriers keep the compiler from regrouping them.
     auto step = [&](int64_t kt, int sc, auto y_slot) {
-        FOCUS_WAIT_VMCNT(8 * (S - 3));
+        FOCUS_WAIT_VMCNT(kLoads * (S - 3));
         asm volatile("s_barrier" ::: "memory");
         const int sn = sc == S - 1 ? 0 : sc + 1, sl = sc == 0 ? S - 1 : sc - 1;
-        const char *As = smem + sc * kFwdStageBytes, *Bs = As + kFwdOpBytes;
-        const char *An = smem + sn * kFwdStageBytes, *Bn = An + kFwdOpBytes;
+        const char *As = smem + sc * kStage, *Bs = As + kFwdOpBytes;
+        const char *An = smem + sn * kStage, *Bn = An + kFwdOpBytes;
         lds_char *st = stage(sl);
+        if constexpr (MX) {
+#pragma unroll
+            for (int i = 0; i < 4; i++) sa[i] = na[i], sb[i] = nb[i];
+        }
         load_frags_fwd(g, As, Bs, 1, wm, wn, lane);
         static_for<16>([&](auto idx) {
             constexpr int i = idx / 4, jj = idx % 4;
-            acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[jj], acc[i][jj], 0, 0, 0);
-            if constexpr (idx % 2 == 1) {
+            mfma(std::integral_constant<int, i>{}, std::integral_constant<int, jj>{}, f, sa, sb, std::integral_constant<int, 0>{});
+            if constexpr (idx % 2 == 1 || (MX && (idx == 0 || idx == 8))) {
+                constexpr int li = idx % 2 == 1 ? idx / 2 : 8 + idx / 8;
                 __builtin_amdgcn_sched_barrier(0);
-                if constexpr (decltype(y_slot)::value) issue_y(st, kt + S - 1, idx / 2);
-                else issue_op(st, kt + S - 1, idx / 2);
+                if constexpr (decltype(y_slot)::value) issue_y(st, kt + S - 1, li);
+                else issue_op(st, kt + S - 1, li);
                 __builtin_amdgcn_sched_barrier(0);
             }
         });
         load_frags_fwd(f, An, Bn, 0, wm, wn, lane);
-        mma_frags(g, acc);
+        if constexpr (MX) load_scales(An, na, nb);
+        static_for<16>([&](auto idx) {
+            constexpr int i = idx / 4, jj = idx % 4;
+            mfma(std::integral_constant<int, i>{}, std::integral_constant<int, jj>{}, g, sa, sb, std::integral_constant<int, 1>{});
+        });
     };
     const int64_t n_op = nk > S - 1 ? nk - (S - 1) : 0;  // steps whose slot kt + S - 1 is an operand step
     int64_t kt = 0;
@@ -389,11 +453,10 @@ fwd_mfma_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, 
     // past M and columns past N hold zero accumulators and read Y_ref as zero, so they add nothing
     // to the column sums; their stores fall outside the resource and are dropped. D^2 is summed per
     // accumulator tile in fp32 (16 terms), then into the column's fp64 total.
-    const int lr = lane & 31, lh = lane >> 5;
     double csum[4] = {0.0, 0.0, 0.0, 0.0};
     static_for<4>([&](auto q) {
         if (q == 0) {
-            FOCUS_WAIT_VMCNT(24);  // this thread's loads of quarter 0 have landed
+            FOCUS_WAIT_VMCNT(3 * kLoads);  // this thread's loads of quarter 0 have landed
             asm volatile("s_barrier" ::: "memory");
         }
         lds_char *qb = stage((int)((nk + q) % S));
@@ -700,11 +763,28 @@ hipError_t launch_fwd_mfma(const void *X, const void *W, int64_t M, int64_t N, i
                            float dscale, double *colpart, hipStream_t st) {
     const int tiles_m = (int)((M + kTile - 1) / kTile), tiles_n = (int)((N + kTile - 1) / kTile);
     const dim3 grid((unsigned)tiles_m * tiles_n);
-    const uint16_t *x = static_cast<const uint16_t *>(X), *w = static_cast<const uint16_t *>(W);
     const uint16_t *y = static_cast<const uint16_t *>(Yref);
     uint16_t *d = static_cast<uint16_t *>(dY);
-    if (Yref) fwd_mfma_kernel<true><<<grid, kThreads, 0, st>>>(x, w, M, N, K, y, d, dscale, colpart, tiles_n);
-    else fwd_mfma_kernel<false><<<grid, kThreads, 0, st>>>(x, w, M, N, K, y, d, dscale, colpart, tiles_n);
+    if (Yref) fwd_mfma_kernel<true, false><<<grid, kThreads, 0, st>>>(X, W, nullptr, nullptr, M, N, K, y, d, dscale, colpart, tiles_n);
+    else fwd_mfma_kernel<false, false><<<grid, kThreads, 0, st>>>(X, W, nullptr, nullptr, M, N, K, y, d, dscale, colpart, tiles_n);
+    return hipGetLastError();
+}
+
+bool mfma_fwd_mx_supported(int64_t M, int64_t N, int64_t K) {
+    return M > 0 && N > 0 && N % 8 == 0 && K % 128 == 0 && int64_t(kTile) * K / 2 < (int64_t(1) << 31) &&
+           int64_t(kTile) * N * 2 < (int64_t(1) << 31) &&
+           (M + kTile - 1) / kTile * ((N + kTile - 1) / kTile) < (int64_t(1) << 31);
+}
+
+hipError_t launch_fwd_mfma_mx(const void *Xc, const void *Xs, const void *Wc, const void *Ws, int64_t M, int64_t N,
+                              int64_t K, const void *Yref, void *dY, float dscale, double *colpart, hipStream_t st) {
+    const int tiles_m = (int)((M + kTile - 1) / kTile), tiles_n = (int)((N + kTile - 1) / kTile);
+    const dim3 grid((unsigned)tiles_m * tiles_n);
+    const uint8_t *xs = static_cast<const uint8_t *>(Xs), *ws = static_cast<const uint8_t *>(Ws);
+    const uint16_t *y = static_cast<const uint16_t *>(Yref);
+    uint16_t *d = static_cast<uint16_t *>(dY);
+    if (Yref) fwd_mfma_kernel<true, true><<<grid, kThreads, 0, st>>>(Xc, Wc, xs, ws, M, N, K, y, d, dscale, colpart, tiles_n);
+    else fwd_mfma_kernel<false, true><<<grid, kThreads, 0, st>>>(Xc, Wc, xs, ws, M, N, K, y, d, dscale, colpart, tiles_n);
     return hipGetLastError();
 }
 

@@ -46,6 +46,13 @@ BwdPlan plan_bwd(int op_dt, int fmt, int sb, int64_t M, int64_t N, int64_t K, bo
 hipError_t launch_recon_fwd(const FwdPlan &p, int op_dt, const void *X, const void *W, int64_t M,
                             int64_t N, int64_t K, const void *Yref, void *dY, double *loss_out,
                             double *col_sq_opt, void *ws, hipStream_t st);
+// column sums of D^2 from the per-m-tile partials, then the loss
+hipError_t launch_fwd_finish(int64_t mtiles, int64_t M, int64_t N, const double *colpart, double *col_sq,
+                             double *loss_out, hipStream_t st);
+// the forward from packed MXFP4 operands (MFMA path only)
+hipError_t launch_recon_fwd_mx(const void *Xc, const void *Xs, const void *Wc, const void *Ws, int64_t M, int64_t N,
+                               int64_t K, const void *Yref, void *dY, double *loss_out, double *col_sq_opt, void *ws,
+                               hipStream_t st);
 hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int ste_clip, const void *dY,
                             const void *X, int64_t M, int64_t N, int64_t K, const void *W, int w_dt,
                             const float *s_fp, const float *c, const float *alpha, float *grad_s,

@@ -21,8 +21,8 @@ CALL_RECON_GEMM_FWD, CALL_RECON_GEMM_BWD, CALL_EXPORT_PACKED = 3, 4, 5
 OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_CONFIG, ERR_WORKSPACE, ERR_DOMAIN, ERR_HIP = range(8)
 
 EXPORTED = ("focus_workspace_size", "focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd",
-            "focus_recon_gemm_fwd", "focus_recon_gemm_bwd", "focus_export_packed", "focus_check_flags",
-            "focus_status_string")
+            "focus_recon_gemm_fwd", "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd", "focus_export_packed",
+            "focus_check_flags", "focus_status_string")
 
 
 class QConfig(ctypes.Structure):
@@ -54,6 +54,7 @@ def lib() -> ctypes.CDLL:
         L.focus_fakequant_fwd.argtypes = [q, p, i32, i64, i64, p, p, p, p, i32, p, p, p, p, sz, p]
         L.focus_fakequant_bwd.argtypes = [q, p, i64, i64, p, i32, p, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_fwd.argtypes = [p, p, i32, i64, i64, i64, p, p, p, p, p, sz, p]
+        L.focus_recon_gemm_fwd_mxfp4.argtypes = [p, p, p, p, i64, i64, i64, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_bwd.argtypes = [q, p, p, i32, i64, i64, i64, p, i32, p, p, p, p, p, p, p, sz, p]
         L.focus_export_packed.argtypes = [q, p, i32, i64, i64, p, p, p, p, p, p, sz, p]
         L.focus_check_flags.argtypes = [p, p]
@@ -139,16 +140,23 @@ def scales_init(W: torch.Tensor, fmt: int, sub_block: int, ws=None, out=None):
 
 def fakequant_fwd(X: torch.Tensor, fmt: int, sub_block: int = 8, s_fp=None, c=None, alpha=None,
                   out_dtype=None, want_codes: bool = False, want_scale_bytes: bool = False,
-                  want_alpha: bool = False, ste_clip: int = 1, ws=None, out=None):
+                  want_alpha: bool = False, ste_clip: int = 1, ws=None, out=None, codes_out=None,
+                  scales_out=None):
     """Fake quantisation forward. Weight mode when s_fp is given, dynamic activation mode otherwise.
+    codes_out / scales_out: preallocated code and scale-byte outputs (they imply want_codes /
+    want_scale_bytes).
 
     Returns (x_hat, packed_codes or None, scale_bytes or None, alpha_x or None)."""
     rows, K = X.shape
     q = qconfig(fmt, sub_block, ste_clip)
     out_dtype = out_dtype or X.dtype
     x_hat = out if out is not None else torch.empty(rows, K, dtype=out_dtype, device=X.device)
-    codes = torch.empty(rows, K // 2, dtype=torch.uint8, device=X.device) if want_codes else None
-    sbytes = torch.empty(rows, K // block_size(fmt), dtype=torch.uint8, device=X.device) if want_scale_bytes else None
+    codes = codes_out
+    if codes is None and want_codes:
+        codes = torch.empty(rows, K // 2, dtype=torch.uint8, device=X.device)
+    sbytes = scales_out
+    if sbytes is None and want_scale_bytes:
+        sbytes = torch.empty(rows, K // block_size(fmt), dtype=torch.uint8, device=X.device)
     alpha_out = torch.empty(1, dtype=torch.float32, device=X.device) if want_alpha else None
     ws = _ws(ws, CALL_FAKEQUANT_FWD, q, 0, rows, K, X.device)
     _check(lib().focus_fakequant_fwd(ctypes.byref(q), _ptr(X), _dt(X), rows, K, _ptr(s_fp), _ptr(c), _ptr(alpha),
@@ -186,6 +194,25 @@ def recon_gemm_fwd(X_hat: torch.Tensor, W_hat: torch.Tensor, Y_ref=None, want_co
     _check(lib().focus_recon_gemm_fwd(_ptr(X_hat), _ptr(W_hat), _dt(X_hat), M, N, K, _ptr(Y_ref), _ptr(dY),
                                       _ptr(loss_t), _ptr(col_sq), _ptr(ws), ws.numel(), _stream()),
            "focus_recon_gemm_fwd")
+    return dY, loss_t, col_sq
+
+
+def recon_gemm_fwd_mxfp4(X_codes: torch.Tensor, X_scales: torch.Tensor, W_codes: torch.Tensor, W_scales: torch.Tensor,
+                         Y_ref=None, want_col_sq: bool = False, ws=None, out=None, loss=None):
+    """The forward from packed MXFP4 operands (codes [rows][K/2], E8M0 bytes [rows][K/32]) -> as recon_gemm_fwd."""
+    M, K = X_codes.shape[0], X_codes.shape[1] * 2
+    N = W_codes.shape[0]
+    dev = X_codes.device
+    dY = out if out is not None else torch.empty(M, N, dtype=torch.bfloat16, device=dev)
+    loss_t = None
+    if Y_ref is not None:
+        loss_t = loss if loss is not None else torch.empty(1, dtype=torch.float64, device=dev)
+    col_sq = torch.empty(N, dtype=torch.float64, device=dev) if want_col_sq else None
+    ws = _ws(ws, CALL_RECON_GEMM_FWD, qconfig(MXFP4, 8), M, N, K, dev)
+    _check(lib().focus_recon_gemm_fwd_mxfp4(_ptr(X_codes), _ptr(X_scales), _ptr(W_codes), _ptr(W_scales), M, N, K,
+                                            _ptr(Y_ref), _ptr(dY), _ptr(loss_t), _ptr(col_sq), _ptr(ws), ws.numel(),
+                                            _stream()),
+           "focus_recon_gemm_fwd_mxfp4")
     return dY, loss_t, col_sq
 
 

@@ -19,7 +19,7 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))
 def declared_functions():
     text = open(HEADER).read()
     # declarations: a return type at the start of a line, then the function name and "("
-    return sorted(set(re.findall(r"^(?:focus_status|size_t|const char \*)\s*(focus_[a-z_]+)\(", text, re.M)))
+    return sorted(set(re.findall(r"^(?:focus_status|size_t|const char \*)\s*(focus_[a-z0-9_]+)\(", text, re.M)))
 
 
 @pytest.fixture(scope="module")
@@ -103,6 +103,20 @@ def test_argument_checks(L, cpu_only):
                                   None) == focus.ERR_NULL  # MSE mode needs loss_out
     assert L.focus_recon_gemm_fwd(BOGUS, BOGUS, 3, 8, 8, 32, None, BOGUS, None, None, BOGUS, 1 << 30,
                                   None) == focus.ERR_DTYPE
+    # forward GEMM from packed MXFP4 operands
+    mxf = L.focus_recon_gemm_fwd_mxfp4
+    assert mxf(BOGUS, BOGUS, BOGUS, BOGUS, 8, 8, 64, None, BOGUS, None, None, BOGUS, 1 << 30,
+               None) == focus.ERR_SHAPE   # K not a multiple of 128
+    assert mxf(BOGUS, BOGUS, BOGUS, BOGUS, 8, 12, 128, None, BOGUS, None, None, BOGUS, 1 << 30,
+               None) == focus.ERR_SHAPE   # N not a multiple of 8
+    assert mxf(BOGUS, None, BOGUS, BOGUS, 8, 8, 128, None, BOGUS, None, None, BOGUS, 1 << 30,
+               None) == focus.ERR_NULL
+    assert mxf(BOGUS, BOGUS, BOGUS, BOGUS, 8, 8, 128, BOGUS, BOGUS, None, None, BOGUS, 1 << 30,
+               None) == focus.ERR_NULL    # MSE mode needs loss_out
+    assert mxf(BOGUS, ctypes.c_void_p((1 << 20) + 2), BOGUS, BOGUS, 8, 8, 128, None, BOGUS, None, None, BOGUS,
+               1 << 30, None) == focus.ERR_SHAPE  # scale bytes not 4-byte aligned
+    assert mxf(BOGUS, BOGUS, BOGUS, BOGUS, 8, 8, 128, None, BOGUS, None, None, BOGUS, 16,
+               None) == focus.ERR_WORKSPACE
     # export and init
     assert L.focus_export_packed(ctypes.byref(mx), BOGUS, 1, 4, 64, BOGUS, None, None, None, BOGUS, BOGUS,
                                  1 << 20, None) == focus.ERR_NULL
