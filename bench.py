@@ -129,14 +129,15 @@ def main():
     if mx_primary and fmt != 0:
         print("--fwd-operands mxfp4 needs an MXFP4 workload", file=sys.stderr)
         sys.exit(2)
-    mx_possible = fmt == 0 and all(l.K % 128 == 0 and l.N % 8 == 0 for l in w.linears)
+    mx_possible = fmt == 0 and M % 4 == 0 and all(l.K % 128 == 0 and l.N % 8 == 0 for l in w.linears)
     if mx_possible:  # packed operands of an MXFP4 forward: codes [rows][K/2] and E8M0 bytes [rows][K/32]
+        # (scale bytes block-major, [K/32][rows], the layout the MXFP4 forward reads)
         x_codes = {src: torch.empty(M, x.shape[1] // 2, dtype=torch.uint8, device=dev) for src, x in acts.items()}
-        x_scales = {src: torch.empty(M, x.shape[1] // 32, dtype=torch.uint8, device=dev) for src, x in acts.items()}
+        x_scales = {src: torch.empty(x.shape[1] // 32, M, dtype=torch.uint8, device=dev) for src, x in acts.items()}
         for L in layers:
             N_, K_ = L["W"].shape
             L["Wc"] = torch.empty(N_, K_ // 2, dtype=torch.uint8, device=dev)
-            L["Ws"] = torch.empty(N_, K_ // 32, dtype=torch.uint8, device=dev)
+            L["Ws"] = torch.empty(K_ // 32, N_, dtype=torch.uint8, device=dev)
     max_n = max(l.N for l in w.linears)
     dY_buf = torch.empty(M * max_n, dtype=acts[w.linears[0].source].dtype, device=dev)
     q = F.qconfig(fmt, sb)
@@ -150,7 +151,8 @@ def main():
             rows, K = x.shape
             if mx_fwd:
                 timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src],
-                                                                   codes_out=x_codes[src], scales_out=x_scales[src]),
+                                                                   codes_out=x_codes[src], scales_out=x_scales[src],
+                                                                   scale_layout=F.SCALES_BLOCK_MAJOR),
                           rows * K)
             else:
                 timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src]), rows * K)
@@ -162,7 +164,8 @@ def main():
                 # the forward's weight operand is the deployable export: codes + E8M0 bytes, no bf16 W_hat
                 timer.run("fakequant_weight",
                           lambda: F.export_packed(L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws_fq,
-                                                  out=(L["Wc"], L["Ws"])), lin.N * lin.K)
+                                                  out=(L["Wc"], L["Ws"]), scale_layout=F.SCALES_BLOCK_MAJOR),
+                          lin.N * lin.K)
                 timer.run("recon_gemm_fwd",
                           lambda: F.recon_gemm_fwd_mxfp4(x_codes[lin.source], x_scales[lin.source], L["Wc"], L["Ws"],
                                                          L["Y"], ws=ws_fwd, out=dY, loss=L["loss"]),

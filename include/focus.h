@@ -45,7 +45,7 @@ typedef enum {
     FOCUS_ERR_SHAPE = 2,     /* bad sizes (negative, too large, K not a multiple of the block size)
                                 or a tensor pointer that is not 16-byte aligned */
     FOCUS_ERR_DTYPE = 3,     /* unknown dtype or unsupported dtype combination */
-    FOCUS_ERR_CONFIG = 4,    /* bad focus_qconfig (format, sub_block, ste_clip, reserved) */
+    FOCUS_ERR_CONFIG = 4,    /* bad focus_qconfig (format, sub_block, ste_clip, scale_layout) */
     FOCUS_ERR_WORKSPACE = 5, /* workspace NULL, misaligned or smaller than focus_workspace_size() */
     FOCUS_ERR_DOMAIN = 6,    /* focus_check_flags: a kernel met a NaN scale or a c <= 0 / non-finite */
     FOCUS_ERR_HIP = 7        /* the HIP runtime reported an error */
@@ -61,12 +61,15 @@ typedef enum { FOCUS_F32 = 0, FOCUS_BF16 = 1 } focus_dtype;
  *               coefficient per block (Sec. 3.3 Eq. 6-7); the paper's default is 8.
  *   ste_clip  : 1 -> the straight-through derivative of Q_E2M1 is the clamp's, m = [|u| <= 6];
  *               0 -> m = 1 everywhere.
- *   reserved  : must be 0. */
+ *   scale_layout : layout of the scale bytes that focus_fakequant_fwd and focus_export_packed write:
+ *               FOCUS_SCALES_ROW_MAJOR (0) [rows][K/B], the deployable layout; FOCUS_SCALES_BLOCK_MAJOR
+ *               (1) [K/B][rows], the layout focus_recon_gemm_fwd_mxfp4 reads. Other calls ignore it. */
+typedef enum { FOCUS_SCALES_ROW_MAJOR = 0, FOCUS_SCALES_BLOCK_MAJOR = 1 } focus_scale_layout;
 typedef struct {
     int32_t format;
     int32_t sub_block;
     int32_t ste_clip;
-    int32_t reserved;
+    int32_t scale_layout;
 } focus_qconfig;
 
 typedef void *focus_stream; /* a hipStream_t */
@@ -144,9 +147,10 @@ focus_status focus_recon_gemm_fwd(const void *X_hat, const void *W_hat, int op_d
  * accumulated in fp32, i.e. the same result as the bf16 path up to the accumulation order.
  *   X_codes [M][K/2], W_codes [N][K/2]: two E2M1 codes per byte, even k in the low nibble (the
  *     codes_opt / packed layout of focus_fakequant_fwd and focus_export_packed), 16-byte aligned;
- *   X_scales [M][K/32], W_scales [N][K/32]: E8M0 bytes (e + 127), 4-byte aligned.
- *   Requires K % 128 == 0 and N % 8 == 0 (FOCUS_ERR_SHAPE otherwise). The workspace is that of
- *   FOCUS_CALL_RECON_GEMM_FWD. */
+ *   X_scales [K/32][M], W_scales [K/32][N]: E8M0 bytes (e + 127) in the block-major layout
+ *     (FOCUS_SCALES_BLOCK_MAJOR of focus_fakequant_fwd / focus_export_packed), 4-byte aligned.
+ *   Requires K % 128 == 0, M % 4 == 0 and N % 8 == 0 (FOCUS_ERR_SHAPE otherwise). The workspace is
+ *   that of FOCUS_CALL_RECON_GEMM_FWD. */
 focus_status focus_recon_gemm_fwd_mxfp4(const uint8_t *X_codes, const uint8_t *X_scales, const uint8_t *W_codes,
                                         const uint8_t *W_scales, int64_t M, int64_t N, int64_t K,
                                         const void *Y_ref, void *dY, double *loss_out, double *col_sq_opt,

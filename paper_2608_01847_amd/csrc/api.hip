@@ -20,7 +20,7 @@ focus_status check_q(const focus_qconfig *q) {
     const int B = block_of(q->format), sb = q->sub_block;
     if (!(sb == 2 || sb == 4 || sb == 8 || sb == 16 || sb == 32) || B % sb != 0) return FOCUS_ERR_CONFIG;
     if (q->ste_clip != 0 && q->ste_clip != 1) return FOCUS_ERR_CONFIG;
-    if (q->reserved != 0) return FOCUS_ERR_CONFIG;
+    if (q->scale_layout != FOCUS_SCALES_ROW_MAJOR && q->scale_layout != FOCUS_SCALES_BLOCK_MAJOR) return FOCUS_ERR_CONFIG;
     return FOCUS_OK;
 }
 
@@ -125,9 +125,9 @@ focus_status focus_fakequant_fwd(const focus_qconfig *q, const void *X, int x_dt
     hipStream_t st = (hipStream_t)stream;
     if (weight_mode)
         return hip_status(launch_fq_weight(q->format, x_dtype, xhat_dtype, X, rows, K, s_fp, c, q->sub_block,
-                                           alpha, X_hat, codes_opt, scale_bytes_opt, flag_of(ws), st));
+                                           alpha, X_hat, codes_opt, scale_bytes_opt, q->scale_layout, flag_of(ws), st));
     return hip_status(launch_fq_act(q->format, x_dtype, xhat_dtype, X, rows, K, X_hat, codes_opt,
-                                    scale_bytes_opt, alpha_out_opt, partials_of(ws), flag_of(ws), st));
+                                    scale_bytes_opt, q->scale_layout, alpha_out_opt, partials_of(ws), flag_of(ws), st));
 }
 
 focus_status focus_fakequant_bwd(const focus_qconfig *q, const float *G, int64_t N, int64_t K, const void *W,
@@ -170,7 +170,7 @@ focus_status focus_recon_gemm_fwd_mxfp4(const uint8_t *X_codes, const uint8_t *X
     if (!X_codes || !X_scales || !W_codes || !W_scales || !dY) return FOCUS_ERR_NULL;
     if (Y_ref && !loss_out) return FOCUS_ERR_NULL;
     if (M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return FOCUS_ERR_SHAPE;
-    if (K % 128 != 0 || N % 8 != 0) return FOCUS_ERR_SHAPE;
+    if (K % 128 != 0 || N % 8 != 0 || M % 4 != 0) return FOCUS_ERR_SHAPE;
     if ((M > 0 && K > kMaxElems / M) || (N > 0 && K > kMaxElems / N) || (M > 0 && N > kMaxElems / M))
         return FOCUS_ERR_SHAPE;
     if (!all_aligned({X_codes, W_codes, Y_ref, dY})) return FOCUS_ERR_SHAPE;
@@ -215,7 +215,7 @@ focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dt
     FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_EXPORT_PACKED, q, 0, N, K)));
     if (N == 0 || K == 0) return FOCUS_OK;
     return hip_status(launch_fq_weight(q->format, w_dtype, w_dtype, W, N, K, s_fp, c, q->sub_block, alpha,
-                                       nullptr, packed, scale_bytes, flag_of(ws), (hipStream_t)stream));
+                                       nullptr, packed, scale_bytes, q->scale_layout, flag_of(ws), (hipStream_t)stream));
 }
 
 focus_status focus_check_flags(void *ws, focus_stream stream) {

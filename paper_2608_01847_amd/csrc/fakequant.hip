@@ -25,6 +25,16 @@ __device__ __forceinline__ float group_sum(float v, int lanes) {
     return v;
 }
 
+// Index of the scale byte of the block holding element e0 of a [rows_total][K] tensor: row-major
+// [rows][K/B] (e0 / B, rows being contiguous) or block-major [K/B][rows_total].
+template <int B>
+__device__ __forceinline__ int64_t scale_index(int64_t e0, uint32_t t, uint32_t cpr, int64_t row0,
+                                               int64_t rows_total, int block_major) {
+    if (!block_major) return e0 / B;
+    const uint32_t r = t / cpr, j = t - r * cpr;
+    return (int64_t)(j * 8 / B) * rows_total + row0 + r;
+}
+
 // ------------------------------------------------------------------------------------------------
 // K1 / K7: weight fake quantisation with learned scales (Eq. 4, 6-8) and export (Fig. 3(d)).
 template <int FMT, int IN, int OUT>
@@ -32,7 +42,8 @@ __global__ void __launch_bounds__(256)
 fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
                  const float *__restrict__ s_fp, const float *__restrict__ c, int sb_log2,
                  const float *__restrict__ alpha_ptr, int ste_clip, void *__restrict__ w_hat,
-                 uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes, uint32_t *flag) {
+                 uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes, int64_t rows_total,
+                 int block_major, uint32_t *flag) {
     constexpr int B = block_of(FMT);
     const float alpha = FMT == kFmtNV ? *alpha_ptr : 1.0f;
     const int sb = 1 << sb_log2;
@@ -68,7 +79,8 @@ fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int
         }
         if (w_hat) store8(w_hat, OUT, e0, out);
         if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
-        if (scale_bytes && (e0 % B) == 0) scale_bytes[e0 / B] = (uint8_t)byte;
+        if (scale_bytes && (e0 % B) == 0)
+            scale_bytes[scale_index<B>(e0, t, cpr, row0, rows_total, block_major)] = (uint8_t)byte;
     }
     if (bad) raise_domain_flag(flag);
     (void)ste_clip;
@@ -82,10 +94,9 @@ template <int IN, int OUT>
 __global__ void __launch_bounds__(256)
 fq_act_mx_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
                  void *__restrict__ x_hat, uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes,
-                 uint32_t *flag) {
-    // Rows are contiguous, so chunk t (8 elements) starts at element row0 K + 8 t and its block's
-    // scale byte is element / 32. Launched with one chunk per thread (the loop is a guard).
-    (void)cpr;
+                 int64_t rows_total, int block_major, uint32_t *flag) {
+    // Rows are contiguous, so chunk t (8 elements) starts at element row0 K + 8 t. Launched with one
+    // chunk per thread (the loop is a guard).
     const int64_t e_row0 = row0 * K;
     bool bad = false;
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
@@ -113,7 +124,8 @@ fq_act_mx_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
         for (int i = 0; i < 8; i++) out[i] *= S;
         if (x_hat) store8(x_hat, OUT, e0, out);
         if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
-        if (scale_bytes && (t & 3u) == 0) scale_bytes[e0 / 32] = (uint8_t)(e + 127);
+        if (scale_bytes && (t & 3u) == 0)
+            scale_bytes[scale_index<32>(e0, t, cpr, row0, rows_total, block_major)] = (uint8_t)(e + 127);
     }
     if (bad) raise_domain_flag(flag);
 }
@@ -175,10 +187,9 @@ template <int IN, int OUT>
 __global__ void __launch_bounds__(256)
 fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
                  const float *__restrict__ alpha_slot, void *__restrict__ x_hat, uint8_t *__restrict__ codes,
-                 uint8_t *__restrict__ scale_bytes, uint32_t *flag) {
+                 uint8_t *__restrict__ scale_bytes, int64_t rows_total, int block_major, uint32_t *flag) {
     const float alpha = *alpha_slot;
     const float alpha6 = alpha * 6.0f;
-    (void)cpr;
     const int64_t e_row0 = row0 * K;  // rows are contiguous: chunk t starts at e_row0 + 8 t
     bool bad = false;
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
@@ -201,7 +212,8 @@ fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
         }
         if (x_hat) store8(x_hat, OUT, e0, out);
         if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
-        if (scale_bytes && (t & 1u) == 0) scale_bytes[e0 / 16] = (uint8_t)byte;
+        if (scale_bytes && (t & 1u) == 0)
+            scale_bytes[scale_index<16>(e0, t, cpr, row0, rows_total, block_major)] = (uint8_t)byte;
     }
     if (bad) raise_domain_flag(flag);
 }
@@ -322,10 +334,10 @@ static int log2i(int v) {
 
 hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64_t rows, int64_t K,
                             const float *s_fp, const float *c, int sb, const float *alpha, void *w_hat,
-                            uint8_t *codes, uint8_t *scale_bytes, uint32_t *flag, hipStream_t st) {
+                            uint8_t *codes, uint8_t *scale_bytes, int block_major, uint32_t *flag, hipStream_t st) {
     const int sbl = log2i(sb);
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-#define FQW(F, I, O) fq_weight_kernel<F, I, O><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, s_fp, c, sbl, alpha, 1, w_hat, codes, scale_bytes, flag)
+#define FQW(F, I, O) fq_weight_kernel<F, I, O><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, s_fp, c, sbl, alpha, 1, w_hat, codes, scale_bytes, rows, block_major, flag)
         if (fmt == kFmtMX) {
             if (in_dt == kBF16) { if (out_dt == kBF16) FQW(kFmtMX, kBF16, kBF16); else FQW(kFmtMX, kBF16, kF32); }
             else { if (out_dt == kBF16) FQW(kFmtMX, kF32, kBF16); else FQW(kFmtMX, kF32, kF32); }
@@ -348,11 +360,11 @@ static hipError_t launch_tensor_alpha(int in_dt, const void *X, int64_t n, float
 }
 
 hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t rows, int64_t K,
-                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, float *alpha_out,
+                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, float *alpha_out,
                          float *partial, uint32_t *flag, hipStream_t st) {
     if (fmt == kFmtMX) {
         return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-#define FQA(I, O) fq_act_mx_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, x_hat, codes, scale_bytes, flag)
+#define FQA(I, O) fq_act_mx_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, x_hat, codes, scale_bytes, rows, block_major, flag)
             if (in_dt == kBF16) { if (out_dt == kBF16) FQA(kBF16, kBF16); else FQA(kBF16, kF32); }
             else { if (out_dt == kBF16) FQA(kF32, kBF16); else FQA(kF32, kF32); }
 #undef FQA
@@ -362,7 +374,7 @@ hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t 
     if (e != hipSuccess) return e;
     const float *slot = partial + kAbsmaxParts;
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-#define FQN(I, O) fq_act_nv_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, slot, x_hat, codes, scale_bytes, flag)
+#define FQN(I, O) fq_act_nv_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, slot, x_hat, codes, scale_bytes, rows, block_major, flag)
         if (in_dt == kBF16) { if (out_dt == kBF16) FQN(kBF16, kBF16); else FQN(kBF16, kF32); }
         else { if (out_dt == kBF16) FQN(kF32, kBF16); else FQN(kF32, kF32); }
 #undef FQN

@@ -311,9 +311,10 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     dma.init(pitch, wave_u, lane);
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(static_cast<const char *>(X) + m0 * pitch, (M - m0) * pitch);
     const __amdgpu_buffer_rsrc_t rb = make_rsrc(static_cast<const char *>(W) + n0 * pitch, (N - n0) * pitch);
-    const int64_t spitch = K / 32;             // scale bytes of a row (a multiple of 4 in MX mode)
-    const __amdgpu_buffer_rsrc_t rxs = make_rsrc(MX ? Xs + m0 * spitch : Xs, MX ? (M - m0) * spitch : 0);
-    const __amdgpu_buffer_rsrc_t rws = make_rsrc(MX ? Ws + n0 * spitch : Ws, MX ? (N - n0) * spitch : 0);
+    // block-major scale bytes [K/32][rows]: a step's 4 blocks of the tile's 256 rows are 4 runs of 256
+    // contiguous bytes per operand
+    const __amdgpu_buffer_rsrc_t rxs = make_rsrc(Xs, MX ? (K / 32) * M : 0);
+    const __amdgpu_buffer_rsrc_t rws = make_rsrc(Ws, MX ? (K / 32) * N : 0);
     const __amdgpu_buffer_rsrc_t r_none = make_rsrc(dY, 0);
     const __amdgpu_buffer_rsrc_t rs_y = make_rsrc(MSE ? Yref + m0 * N : dY, MSE ? (M - m0) * N * 2 : 0);
     const __amdgpu_buffer_rsrc_t rs_d = make_rsrc(dY + m0 * N, (M - m0) * N * 2);
@@ -327,17 +328,19 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     auto q_off = [](uint32_t rl, uint32_t chunk) { return rl * 512u + ((chunk ^ (((rl >> 2) & 1u) << 2)) << 4); };
     auto stage = [&](int sidx) { return lsm + sidx * kStage; };
     // Load i of slot j into stage st: loads 0-3 bring X rows, 4-7 W rows of an operand step, and in
-    // MX mode 8 / 9 the step's X / W scale bytes (4 bytes of each of 256 rows; this wave's 64 rows,
-    // lane L's 4 bytes landing at byte 4 L). A Y_ref quarter is 32 one-KB blocks of two rows
-    // each, this wave filling blocks 8 wave .. 8 wave + 7 (lane L of block b lands in local row
-    // 2 b + L / 32, physical chunk L % 32); in MX mode its loads 8 and 9 are empty and only write
-    // zeros into the stage's scale bytes.
+    // MX mode 8 / 9 the scale bytes of block 4 j + wave of the tile's 256 X / W rows (a [4][256]
+    // byte array per operand in the stage; lane L's 4 bytes, rows 4 L .. 4 L + 3, land at byte 4 L
+    // of the wave's run). A Y_ref quarter is 32 one-KB blocks of two rows each, this wave filling
+    // blocks 8 wave .. 8 wave + 7 (lane L of block b lands in local row 2 b + L / 32, physical chunk
+    // L % 32); in MX mode its loads 8 and 9 are empty and only write zeros into the stage's scale
+    // bytes. Scale rows past M or N belong to the next block (or past the array) and meet zero codes.
     auto issue_op = [&](lds_char *st, int64_t j, int i) {
         const uint32_t base = (uint32_t)j * 64u, bad = dma.step_bad(pitch, base);  // 64 row bytes per step
         if (i < 4) dma.issue_one(ra, base, bad, st, wave_u, i);
         else if (i < 8) dma.issue_one(rb, base, bad, st + kFwdOpBytes, wave_u, i - 4);
         else {
-            const uint32_t so = (uint32_t)(wave_u * 64 + lane) * (uint32_t)spitch + (uint32_t)j * 4u;
+            const uint32_t blk = (uint32_t)j * 4u + wave_u;
+            const uint32_t so = blk * (uint32_t)(i == 8 ? M : N) + (uint32_t)(i == 8 ? m0 : n0) + 4u * lane;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(i == 8 ? rxs : rws, st + kFwdStageBytes + (i - 8) * 1024 + wave_u * 256, 4,
                                                      (int)so, 0, 0, 0);
         }
@@ -365,14 +368,16 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
             for (int i = 0; i < kLoads; i++) issue_y(st, j, i);
         }
     };
-    // MX mode: this lane's scale words (rows of its X / W fragments) of a stage, shifted so that
-    // byte 0 / 2 holds the scale of the first / second 64 k it covers (lane half lh takes the odd
-    // 32-k block of each 64)
+    // MX mode: this lane's scales (rows of its X / W fragments) of a stage, byte 0 / 2 holding the
+    // scale of the first / second 64 k it covers (lane half lh takes the odd 32-k block of each 64)
     auto load_scales = [&](const char *st, uint32_t (&sa)[4], uint32_t (&sb)[4]) {
+        const uint8_t *sx = reinterpret_cast<const uint8_t *>(st + kFwdStageBytes) + lh * 256;
+        const uint8_t *sw = sx + 1024;
 #pragma unroll
         for (int i = 0; i < 4; i++) {
-            sa[i] = *reinterpret_cast<const uint32_t *>(st + kFwdStageBytes + (wm * 128 + i * 32 + lr) * 4) >> (8 * lh);
-            sb[i] = *reinterpret_cast<const uint32_t *>(st + kFwdStageBytes + 1024 + (wn * 128 + i * 32 + lr) * 4) >> (8 * lh);
+            const int ra_ = wm * 128 + i * 32 + lr, rb_ = wn * 128 + i * 32 + lr;
+            sa[i] = (uint32_t)sx[ra_] | ((uint32_t)sx[512 + ra_] << 16);
+            sb[i] = (uint32_t)sw[rb_] | ((uint32_t)sw[512 + rb_] << 16);
         }
     };
     auto mfma = [&](auto i, auto j, const Frags &fr, const uint32_t (&sa)[4], const uint32_t (&sb)[4], auto half) {
@@ -771,7 +776,8 @@ hipError_t launch_fwd_mfma(const void *X, const void *W, int64_t M, int64_t N, i
 }
 
 bool mfma_fwd_mx_supported(int64_t M, int64_t N, int64_t K) {
-    return M > 0 && N > 0 && N % 8 == 0 && K % 128 == 0 && int64_t(kTile) * K / 2 < (int64_t(1) << 31) &&
+    return M > 0 && N > 0 && N % 8 == 0 && M % 4 == 0 && K % 128 == 0 && int64_t(kTile) * K / 2 < (int64_t(1) << 31) &&
+           (K / 32) * std::max(M, N) < (int64_t(1) << 31) &&
            int64_t(kTile) * N * 2 < (int64_t(1) << 31) &&
            (M + kTile - 1) / kTile * ((N + kTile - 1) / kTile) < (int64_t(1) << 31);
 }

@@ -14,9 +14,9 @@ constexpr size_t kWsHeader = 256;     // workspace bytes reserved for the domain
 
 hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64_t rows, int64_t K,
                             const float *s_fp, const float *c, int sb, const float *alpha, void *w_hat,
-                            uint8_t *codes, uint8_t *scale_bytes, uint32_t *flag, hipStream_t st);
+                            uint8_t *codes, uint8_t *scale_bytes, int block_major, uint32_t *flag, hipStream_t st);
 hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t rows, int64_t K,
-                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, float *alpha_out,
+                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, float *alpha_out,
                          float *partial, uint32_t *flag, hipStream_t st);
 hipError_t launch_scales_init(int fmt, int in_dt, const void *W, int64_t rows, int64_t K, float *s_fp,
                               float *c, int sb, float *alpha_out, float *partial, hipStream_t st);

@@ -27,7 +27,7 @@ EXPORTED = ("focus_workspace_size", "focus_scales_init", "focus_fakequant_fwd", 
 
 class QConfig(ctypes.Structure):
     _fields_ = [("format", ctypes.c_int32), ("sub_block", ctypes.c_int32),
-                ("ste_clip", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("ste_clip", ctypes.c_int32), ("scale_layout", ctypes.c_int32)]
 
 
 class FocusError(RuntimeError):
@@ -71,8 +71,11 @@ def status_string(status: int) -> str:
     return lib().focus_status_string(status).decode()
 
 
-def qconfig(fmt: int, sub_block: int, ste_clip: int = 1) -> QConfig:
-    return QConfig(fmt, sub_block, ste_clip, 0)
+SCALES_ROW_MAJOR, SCALES_BLOCK_MAJOR = 0, 1
+
+
+def qconfig(fmt: int, sub_block: int, ste_clip: int = 1, scale_layout: int = SCALES_ROW_MAJOR) -> QConfig:
+    return QConfig(fmt, sub_block, ste_clip, scale_layout)
 
 
 def block_size(fmt: int) -> int:
@@ -141,14 +144,14 @@ def scales_init(W: torch.Tensor, fmt: int, sub_block: int, ws=None, out=None):
 def fakequant_fwd(X: torch.Tensor, fmt: int, sub_block: int = 8, s_fp=None, c=None, alpha=None,
                   out_dtype=None, want_codes: bool = False, want_scale_bytes: bool = False,
                   want_alpha: bool = False, ste_clip: int = 1, ws=None, out=None, codes_out=None,
-                  scales_out=None):
+                  scales_out=None, scale_layout: int = SCALES_ROW_MAJOR):
     """Fake quantisation forward. Weight mode when s_fp is given, dynamic activation mode otherwise.
     codes_out / scales_out: preallocated code and scale-byte outputs (they imply want_codes /
-    want_scale_bytes).
+    want_scale_bytes). scale_layout: [rows][K/B] (row-major) or [K/B][rows] (block-major).
 
     Returns (x_hat, packed_codes or None, scale_bytes or None, alpha_x or None)."""
     rows, K = X.shape
-    q = qconfig(fmt, sub_block, ste_clip)
+    q = qconfig(fmt, sub_block, ste_clip, scale_layout)
     out_dtype = out_dtype or X.dtype
     x_hat = out if out is not None else torch.empty(rows, K, dtype=out_dtype, device=X.device)
     codes = codes_out
@@ -156,7 +159,8 @@ def fakequant_fwd(X: torch.Tensor, fmt: int, sub_block: int = 8, s_fp=None, c=No
         codes = torch.empty(rows, K // 2, dtype=torch.uint8, device=X.device)
     sbytes = scales_out
     if sbytes is None and want_scale_bytes:
-        sbytes = torch.empty(rows, K // block_size(fmt), dtype=torch.uint8, device=X.device)
+        shape = (rows, K // block_size(fmt)) if scale_layout == SCALES_ROW_MAJOR else (K // block_size(fmt), rows)
+        sbytes = torch.empty(*shape, dtype=torch.uint8, device=X.device)
     alpha_out = torch.empty(1, dtype=torch.float32, device=X.device) if want_alpha else None
     ws = _ws(ws, CALL_FAKEQUANT_FWD, q, 0, rows, K, X.device)
     _check(lib().focus_fakequant_fwd(ctypes.byref(q), _ptr(X), _dt(X), rows, K, _ptr(s_fp), _ptr(c), _ptr(alpha),
@@ -199,7 +203,8 @@ def recon_gemm_fwd(X_hat: torch.Tensor, W_hat: torch.Tensor, Y_ref=None, want_co
 
 def recon_gemm_fwd_mxfp4(X_codes: torch.Tensor, X_scales: torch.Tensor, W_codes: torch.Tensor, W_scales: torch.Tensor,
                          Y_ref=None, want_col_sq: bool = False, ws=None, out=None, loss=None):
-    """The forward from packed MXFP4 operands (codes [rows][K/2], E8M0 bytes [rows][K/32]) -> as recon_gemm_fwd."""
+    """The forward from packed MXFP4 operands (codes [rows][K/2], block-major E8M0 bytes [K/32][rows])
+    -> as recon_gemm_fwd."""
     M, K = X_codes.shape[0], X_codes.shape[1] * 2
     N = W_codes.shape[0]
     dev = X_codes.device
@@ -235,13 +240,15 @@ def recon_gemm_bwd(dY: torch.Tensor, X_hat: torch.Tensor, W: torch.Tensor, fmt: 
     return grad_s, grad_c, G
 
 
-def export_packed(W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha=None, ws=None, out=None):
-    """Deployable export -> (packed codes [N][K/2], scale bytes [N][K/B])."""
+def export_packed(W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha=None, ws=None, out=None,
+                  scale_layout: int = SCALES_ROW_MAJOR):
+    """Deployable export -> (packed codes [N][K/2], scale bytes [N][K/B] or, block-major, [K/B][N])."""
     N, K = W.shape
-    q = qconfig(fmt, sub_block)
+    q = qconfig(fmt, sub_block, 1, scale_layout)
     if out is None:
         packed = torch.empty(N, K // 2, dtype=torch.uint8, device=W.device)
-        sbytes = torch.empty(N, K // block_size(fmt), dtype=torch.uint8, device=W.device)
+        shape = (N, K // block_size(fmt)) if scale_layout == SCALES_ROW_MAJOR else (K // block_size(fmt), N)
+        sbytes = torch.empty(*shape, dtype=torch.uint8, device=W.device)
     else:
         packed, sbytes = out
     ws = _ws(ws, CALL_EXPORT_PACKED, q, 0, N, K, W.device)

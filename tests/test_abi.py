@@ -77,7 +77,7 @@ def test_argument_checks(L, cpu_only):
     assert fq_fwd(L, focus.qconfig(focus.MXFP4, 3)) == focus.ERR_CONFIG
     assert fq_fwd(L, focus.qconfig(focus.NVFP4, 32)) == focus.ERR_CONFIG  # sub-block larger than the block
     assert fq_fwd(L, focus.qconfig(focus.MXFP4, 8, 2)) == focus.ERR_CONFIG
-    assert fq_fwd(L, focus.QConfig(0, 8, 1, 5)) == focus.ERR_CONFIG
+    assert fq_fwd(L, focus.QConfig(0, 8, 1, 5)) == focus.ERR_CONFIG  # no such scale layout
     assert fq_fwd(L, mx, X=None) == focus.ERR_NULL
     assert fq_fwd(L, mx, x_dt=7) == focus.ERR_DTYPE
     assert fq_fwd(L, mx, K=48) == focus.ERR_SHAPE          # not a multiple of 32
@@ -109,6 +109,8 @@ def test_argument_checks(L, cpu_only):
                None) == focus.ERR_SHAPE   # K not a multiple of 128
     assert mxf(BOGUS, BOGUS, BOGUS, BOGUS, 8, 12, 128, None, BOGUS, None, None, BOGUS, 1 << 30,
                None) == focus.ERR_SHAPE   # N not a multiple of 8
+    assert mxf(BOGUS, BOGUS, BOGUS, BOGUS, 6, 8, 128, None, BOGUS, None, None, BOGUS, 1 << 30,
+               None) == focus.ERR_SHAPE   # M not a multiple of 4
     assert mxf(BOGUS, None, BOGUS, BOGUS, 8, 8, 128, None, BOGUS, None, None, BOGUS, 1 << 30,
                None) == focus.ERR_NULL
     assert mxf(BOGUS, BOGUS, BOGUS, BOGUS, 8, 8, 128, BOGUS, BOGUS, None, None, BOGUS, 1 << 30,

@@ -10,6 +10,8 @@ that the library's fake quantisation returns. Checked here:
   * against the bf16 forward on the same operands: the two compute the same sums and differ only
     in the fp32 accumulation order (1e-4 on the loss and column sums);
   * the plain product mode (no Y_ref) returns Y_hat;
+  * the block-major scale bytes the forward reads are the transpose of the row-major ones, for
+    activations (MXFP4 and NVFP4), weights and the export;
   * at full size (hidden-2560 gate_proj, 65,536 tokens) on sampled output rows.
 """
 import zlib
@@ -45,9 +47,11 @@ def perturb(seed, s_fp, c):
 
 
 def device_operands(F, X, W, sb, s_d, c_d, a_d):
-    """bf16 X_hat, W_hat and the packed codes + scale bytes of both, from the library."""
-    x_hat, xc, xs, _ = F.fakequant_fwd(X, MX, sb, want_codes=True, want_scale_bytes=True)
-    w_hat, wc, ws, _ = F.fakequant_fwd(W, MX, sb, s_d, c_d, a_d, want_codes=True, want_scale_bytes=True)
+    """bf16 X_hat, W_hat and the packed codes + block-major scale bytes of both, from the library."""
+    bm = F.SCALES_BLOCK_MAJOR
+    x_hat, xc, xs, _ = F.fakequant_fwd(X, MX, sb, want_codes=True, want_scale_bytes=True, scale_layout=bm)
+    w_hat, wc, ws, _ = F.fakequant_fwd(W, MX, sb, s_d, c_d, a_d, want_codes=True, want_scale_bytes=True,
+                                       scale_layout=bm)
     return x_hat, w_hat, xc, xs, wc, ws
 
 
@@ -79,7 +83,7 @@ def check_layer(F, O, X, W, Y, sb, state, tag, rows=None):
     assert_close(col_sq.cpu().numpy()[res.rows], res.col_sq, TOL, f"col_sq {tag}")
 
 
-SHAPES = [(300, 264, 256), (64, 8, 128), (513, 520, 384), (1000, 1024, 2560)]
+SHAPES = [(300, 264, 256), (64, 8, 128), (516, 520, 384), (1000, 1024, 2560)]
 
 
 @pytest.mark.parametrize("M,N,K", SHAPES)
@@ -132,3 +136,22 @@ def test_mx_forward_fullsize_gate(F, O):
     rng = np.random.default_rng(7)
     rows = np.array(sorted({0, lin.N - 1} | set(rng.choice(lin.N, 24, replace=False).tolist()) | set(outl[:6])))
     check_layer(F, O, X, W, Y, w.sub_block, "perturbed", "fullsize gate", rows=rows)
+
+
+def test_block_major_scales_are_the_transpose(F):
+    announce("block-major scale bytes")
+    g = torch.Generator().manual_seed(9)
+    X = torch.randn(300, 640, generator=g).to(torch.bfloat16).cuda()
+    W = (torch.randn(72, 640, generator=g) * 0.02).to(torch.bfloat16).cuda()
+    bm = F.SCALES_BLOCK_MAJOR
+    for fmt in (0, 1):
+        _, c0, s0, _ = F.fakequant_fwd(X, fmt, 8, want_codes=True, want_scale_bytes=True)
+        _, c1, s1, _ = F.fakequant_fwd(X, fmt, 8, want_codes=True, want_scale_bytes=True, scale_layout=bm)
+        assert torch.equal(c0, c1) and torch.equal(s0.t().contiguous(), s1), f"activation fmt {fmt}"
+        s, c, a = F.scales_init(W, fmt, 8)
+        _, w0, t0, _ = F.fakequant_fwd(W, fmt, 8, s, c, a, want_codes=True, want_scale_bytes=True)
+        _, w1, t1, _ = F.fakequant_fwd(W, fmt, 8, s, c, a, want_codes=True, want_scale_bytes=True, scale_layout=bm)
+        assert torch.equal(w0, w1) and torch.equal(t0.t().contiguous(), t1), f"weight fmt {fmt}"
+        p0, e0 = F.export_packed(W, fmt, 8, s, c, a)
+        p1, e1 = F.export_packed(W, fmt, 8, s, c, a, scale_layout=bm)
+        assert torch.equal(p0, p1) and torch.equal(e0.t().contiguous(), e1), f"export fmt {fmt}"
