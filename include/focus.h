@@ -81,7 +81,8 @@ typedef enum {
     FOCUS_CALL_FAKEQUANT_BWD = 2,
     FOCUS_CALL_RECON_GEMM_FWD = 3,
     FOCUS_CALL_RECON_GEMM_BWD = 4,
-    FOCUS_CALL_EXPORT_PACKED = 5
+    FOCUS_CALL_EXPORT_PACKED = 5,
+    FOCUS_CALL_ADAMW = 6
 } focus_call;
 
 /* Workspace bytes a call needs for the given sizes (M = tokens, N = rows / out features,
@@ -177,9 +178,43 @@ focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dt
                                  uint8_t *packed, uint8_t *scale_bytes,
                                  void *ws, size_t ws_bytes, focus_stream stream);
 
+/* AdamW hyper-parameters (Sec. 4.1: AdamW with a constant learning rate; MXFP4 uses 2e-2 for the
+ * block scales and 5e-2 for the coefficients c, NVFP4 5e-3 and 1e-3).
+ *   lr           : learning rate, >= 0.
+ *   beta1, beta2 : decay rates of the first and second moment, in [0, 1).
+ *   eps          : added to the bias-corrected root of the second moment, > 0.
+ *   weight_decay : decoupled weight decay, >= 0 (the parameter is scaled by 1 - lr * weight_decay
+ *                  before the moment step).
+ *   log2_domain  : 0 -> the step is taken on the parameter p itself; 1 -> on theta = log2(p), with
+ *                  dL/dtheta = dL/dp * p * ln 2, the moments kept for theta and p written back as
+ *                  2^theta (p must be positive and finite: the scales S_fp / Delta_fp). */
+typedef struct {
+    float lr;
+    float beta1;
+    float beta2;
+    float eps;
+    float weight_decay;
+    int32_t log2_domain;
+} focus_adamw_config;
+
+/* One AdamW step on n fp32 parameters (Loshchilov & Hutter's AdamW with bias-corrected moments), in
+ * place. With g the gradient (of theta in the log2 domain) and t >= 1 the 1-based step count:
+ *   theta = theta - lr*weight_decay*theta;  m = beta1*m + (1-beta1)*g;  v = beta2*v + (1-beta2)*g^2
+ *   theta = theta - (lr / (1-beta1^t)) * m / (sqrt(v) / sqrt(1-beta2^t) + eps)
+ * (the bias corrections are formed in double on the host and rounded to fp32 once).
+ *   param, exp_avg, exp_avg_sq [n] fp32 device, read and written; grad [n] fp32 device, read.
+ *   The moments start at zero (caller-owned, e.g. the same shapes as S_fp and c). All four
+ *   pointers 16-byte aligned; n <= 2^40.
+ * Errors: FOCUS_ERR_CONFIG (bad hyper-parameters or t < 1), FOCUS_ERR_NULL, FOCUS_ERR_SHAPE, FOCUS_ERR_WORKSPACE
+ * (ws needs focus_workspace_size(FOCUS_CALL_ADAMW, ...) bytes). In the log2 domain a parameter
+ * that is not positive and finite is left unchanged and raises the domain flag. */
+focus_status focus_adamw_step(const focus_adamw_config *cfg, int64_t t, int64_t n, float *param, const float *grad,
+                              float *exp_avg, float *exp_avg_sq, void *ws, size_t ws_bytes, focus_stream stream);
+
 /* Synchronises `stream`, reads and clears the workspace's sticky domain flag. Returns
  * FOCUS_ERR_DOMAIN if any call on this workspace met a NaN scale or a coefficient c that is
- * <= 0 or not finite since the last check (outputs of such blocks are unspecified), FOCUS_OK
+ * <= 0 or not finite, or a log2-domain AdamW step met a parameter that is not positive and
+ * finite, since the last check (outputs of such blocks are unspecified), FOCUS_OK
  * otherwise, FOCUS_ERR_HIP on a runtime error. */
 focus_status focus_check_flags(void *ws, focus_stream stream);
 

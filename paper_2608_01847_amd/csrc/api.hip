@@ -5,6 +5,7 @@
 #include "gemm_common.h"
 #include "internal.h"
 
+#include <cmath>
 #include <initializer_list>
 
 using namespace focus;
@@ -73,6 +74,7 @@ size_t bwd_ws(int fmt, int sb, int64_t M, int64_t N, int64_t K) {
 extern "C" {
 
 size_t focus_workspace_size(int call, const focus_qconfig *q, int64_t M, int64_t N, int64_t K) {
+    if (call == FOCUS_CALL_ADAMW) return kWsHeader;  // the domain flag only; q may be NULL
     if (check_q(q) != FOCUS_OK) return 0;
     const int B = block_of(q->format);
     switch (call) {
@@ -216,6 +218,23 @@ focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dt
     if (N == 0 || K == 0) return FOCUS_OK;
     return hip_status(launch_fq_weight(q->format, w_dtype, w_dtype, W, N, K, s_fp, c, q->sub_block, alpha,
                                        nullptr, packed, scale_bytes, q->scale_layout, flag_of(ws), (hipStream_t)stream));
+}
+
+focus_status focus_adamw_step(const focus_adamw_config *cfg, int64_t t, int64_t n, float *param, const float *grad,
+                              float *exp_avg, float *exp_avg_sq, void *ws, size_t ws_bytes, focus_stream stream) {
+    if (!cfg) return FOCUS_ERR_NULL;
+    const bool finite = std::isfinite(cfg->lr) && std::isfinite(cfg->eps) && std::isfinite(cfg->weight_decay);
+    if (!finite || !(cfg->lr >= 0.f) || !(cfg->beta1 >= 0.f && cfg->beta1 < 1.f) ||
+        !(cfg->beta2 >= 0.f && cfg->beta2 < 1.f) || !(cfg->eps > 0.f) || !(cfg->weight_decay >= 0.f) ||
+        (cfg->log2_domain != 0 && cfg->log2_domain != 1) || t < 1)
+        return FOCUS_ERR_CONFIG;
+    if (n < 0 || n > (int64_t(1) << 40)) return FOCUS_ERR_SHAPE;  // keeps the grid below 2^31 workgroups
+    if (!param || !grad || !exp_avg || !exp_avg_sq) return FOCUS_ERR_NULL;
+    if (!all_aligned({param, grad, exp_avg, exp_avg_sq})) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, kWsHeader));
+    if (n == 0) return FOCUS_OK;
+    return hip_status(launch_adamw(cfg->lr, cfg->beta1, cfg->beta2, cfg->eps, cfg->weight_decay, cfg->log2_domain,
+                                   t, n, param, grad, exp_avg, exp_avg_sq, flag_of(ws), (hipStream_t)stream));
 }
 
 focus_status focus_check_flags(void *ws, focus_stream stream) {

@@ -58,4 +58,8 @@ hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int st
                             const float *s_fp, const float *c, const float *alpha, float *grad_s,
                             float *grad_c, float *G_out, void *ws, uint32_t *flag, hipStream_t st);
 
+hipError_t launch_adamw(float lr, float beta1, float beta2, float eps, float weight_decay, int log2_domain,
+                        int64_t t, int64_t n, float *param, const float *grad, float *exp_avg, float *exp_avg_sq,
+                        uint32_t *flag, hipStream_t st);
+
 }  // namespace focus

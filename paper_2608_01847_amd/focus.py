@@ -16,18 +16,23 @@ LIBRARY = Path(__file__).resolve().parent / "libfocus.so"
 MXFP4, NVFP4 = 0, 1
 F32, BF16 = 0, 1
 CALL_SCALES_INIT, CALL_FAKEQUANT_FWD, CALL_FAKEQUANT_BWD = 0, 1, 2
-CALL_RECON_GEMM_FWD, CALL_RECON_GEMM_BWD, CALL_EXPORT_PACKED = 3, 4, 5
+CALL_RECON_GEMM_FWD, CALL_RECON_GEMM_BWD, CALL_EXPORT_PACKED, CALL_ADAMW = 3, 4, 5, 6
 
 OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_CONFIG, ERR_WORKSPACE, ERR_DOMAIN, ERR_HIP = range(8)
 
 EXPORTED = ("focus_workspace_size", "focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd",
             "focus_recon_gemm_fwd", "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd", "focus_export_packed",
-            "focus_check_flags", "focus_status_string")
+            "focus_adamw_step", "focus_check_flags", "focus_status_string")
 
 
 class QConfig(ctypes.Structure):
     _fields_ = [("format", ctypes.c_int32), ("sub_block", ctypes.c_int32),
                 ("ste_clip", ctypes.c_int32), ("scale_layout", ctypes.c_int32)]
+
+
+class AdamWConfig(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float), ("log2_domain", ctypes.c_int32)]
 
 
 class FocusError(RuntimeError):
@@ -57,11 +62,13 @@ def lib() -> ctypes.CDLL:
         L.focus_recon_gemm_fwd_mxfp4.argtypes = [p, p, p, p, i64, i64, i64, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_bwd.argtypes = [q, p, p, i32, i64, i64, i64, p, i32, p, p, p, p, p, p, p, sz, p]
         L.focus_export_packed.argtypes = [q, p, i32, i64, i64, p, p, p, p, p, p, sz, p]
+        L.focus_adamw_step.argtypes = [ctypes.POINTER(AdamWConfig), i64, i64, p, p, p, p, p, sz, p]
         L.focus_check_flags.argtypes = [p, p]
         L.focus_status_string.argtypes = [i32]
         L.focus_status_string.restype = ctypes.c_char_p
         for name in ("focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd", "focus_recon_gemm_fwd",
-                     "focus_recon_gemm_bwd", "focus_export_packed", "focus_check_flags"):
+                     "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd", "focus_export_packed",
+                     "focus_adamw_step", "focus_check_flags"):
             getattr(L, name).restype = ctypes.c_int
         _LIB = L
     return _LIB
@@ -256,6 +263,19 @@ def export_packed(W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha
                                      _ptr(packed), _ptr(sbytes), _ptr(ws), ws.numel(), _stream()),
            "focus_export_packed")
     return packed, sbytes
+
+
+def adamw_step(param: torch.Tensor, grad: torch.Tensor, exp_avg: torch.Tensor, exp_avg_sq: torch.Tensor, t: int,
+               lr: float, betas=(0.9, 0.999), eps: float = 1e-8, weight_decay: float = 0.0,
+               log2_domain: bool = False, ws=None) -> None:
+    """One in-place AdamW step on fp32 `param` (moments in exp_avg / exp_avg_sq, t the 1-based step)."""
+    for x in (param, grad, exp_avg, exp_avg_sq):
+        assert x.dtype == torch.float32 and x.is_contiguous() and x.numel() == param.numel()
+    cfg = AdamWConfig(lr, betas[0], betas[1], eps, weight_decay, int(log2_domain))
+    if ws is None:
+        ws = workspace(256, param.device)
+    _check(lib().focus_adamw_step(ctypes.byref(cfg), t, param.numel(), _ptr(param), _ptr(grad), _ptr(exp_avg),
+                                  _ptr(exp_avg_sq), _ptr(ws), ws.numel(), _stream()), "focus_adamw_step")
 
 
 def check_flags(ws: torch.Tensor) -> int:

@@ -48,7 +48,7 @@ class Workload:
     w_sigma: float = 0.02
     w_outlier_p: float = 0.001
     w_outlier_f: float = 10.0
-    x_kind: str = "normal"          # "normal" or "student_t3"
+    x_kind: str = "normal"          # "normal", "student_t3" or "lowrank"
     x_outlier_p: float = 0.01
     x_outlier_f: float = 30.0
     seed: int = 0
@@ -160,6 +160,45 @@ def activation(w: Workload, source: str, M: int | None = None, device="cpu") -> 
     if count:
         ch = torch.randperm(K, generator=g, device=device)[:count]
         X[:, ch] *= w.x_outlier_f
+    return X.to(_torch_dtype(w.dtype)).contiguous()
+
+
+LOWRANK_RANK = 32
+LOWRANK_NOISE = 0.1
+
+
+def _lowrank(w: Workload, source: str, M: int, K: int, g: torch.Generator, device) -> torch.Tensor:
+    """Correlated channels: X = Z A + 0.1 E with a fixed mixing matrix A [32][K] (entries N(0, 1/32),
+    drawn once per input tensor), fresh latent factors Z [M][32] and noise E, both N(0, 1). Every
+    channel has about unit variance and the channels are strongly correlated, so X^T X is far from
+    diagonal, as in the inputs of real decoder layers."""
+    A = torch.randn(LOWRANK_RANK, K, generator=_generator(w.name, source + ".mixing", w.seed, device),
+                    device=device) / LOWRANK_RANK ** 0.5
+    Z = torch.randn(M, LOWRANK_RANK, generator=g, device=device)
+    return Z @ A + LOWRANK_NOISE * torch.randn(M, K, generator=g, device=device)
+
+
+def activation_batch(w: Workload, source: str, step: int, M: int | None = None, device="cpu") -> torch.Tensor:
+    """Batch `step` of a calibration epoch for one activation tensor of the block: fresh tokens from
+    a stream keyed by the step, the same outlier channels (same scale factor) in every batch, as
+    tokens of one layer input drawn from a fixed distribution."""
+    K = w.inputs[source]
+    M = M or w.M
+    g = _generator(w.name, f"{source}.act.batch{step}", w.seed, device)
+    if w.x_kind == "lowrank":
+        X = _lowrank(w, source, M, K, g, device)
+    elif w.x_kind == "student_t3":
+        z = torch.randn(M, K, generator=g, device=device)
+        chi2 = torch.zeros(M, K, device=device)
+        for _ in range(3):
+            chi2 += torch.randn(M, K, generator=g, device=device) ** 2
+        X = z / torch.sqrt(chi2 / 3.0)
+    else:
+        X = torch.randn(M, K, generator=g, device=device)
+    count = int(round(w.x_outlier_p * K))
+    if count:
+        ch = torch.randperm(K, generator=_generator(w.name, source + ".channels", w.seed, device), device=device)
+        X[:, ch[:count]] *= w.x_outlier_f
     return X.to(_torch_dtype(w.dtype)).contiguous()
 
 

@@ -126,4 +126,21 @@ def test_argument_checks(L, cpu_only):
                                None) == focus.ERR_NULL
     assert L.focus_fakequant_bwd(ctypes.byref(mx), BOGUS, 4, 64, BOGUS, 0, BOGUS, None, None, BOGUS, BOGUS,
                                  BOGUS, 8, None) == focus.ERR_WORKSPACE
+    # AdamW
+    def adam(cfg, t=1, n=16, ptr=BOGUS, ws=BOGUS, ws_bytes=256):
+        return L.focus_adamw_step(ctypes.byref(cfg), t, n, ptr, BOGUS, BOGUS, BOGUS, ws, ws_bytes, None)
+    good = focus.AdamWConfig(1e-2, 0.9, 0.999, 1e-8, 0.0, 1)
+    assert adam(good, t=0) == focus.ERR_CONFIG
+    assert adam(focus.AdamWConfig(-1e-2, 0.9, 0.999, 1e-8, 0.0, 0)) == focus.ERR_CONFIG
+    assert adam(focus.AdamWConfig(1e-2, 1.0, 0.999, 1e-8, 0.0, 0)) == focus.ERR_CONFIG
+    assert adam(focus.AdamWConfig(1e-2, 0.9, 0.999, 0.0, 0.0, 0)) == focus.ERR_CONFIG
+    assert adam(focus.AdamWConfig(float("nan"), 0.9, 0.999, 1e-8, 0.0, 0)) == focus.ERR_CONFIG
+    assert adam(focus.AdamWConfig(1e-2, 0.9, 0.999, 1e-8, 0.0, 2)) == focus.ERR_CONFIG
+    assert L.focus_adamw_step(None, 1, 16, BOGUS, BOGUS, BOGUS, BOGUS, BOGUS, 256, None) == focus.ERR_NULL
+    assert adam(good, n=-1) == focus.ERR_SHAPE
+    assert adam(good, n=(1 << 40) + 1) == focus.ERR_SHAPE
+    assert adam(good, ptr=None) == focus.ERR_NULL
+    assert adam(good, ptr=ctypes.c_void_p((1 << 20) + 4)) == focus.ERR_SHAPE  # not 16-byte aligned
+    assert adam(good, ws_bytes=8) == focus.ERR_WORKSPACE
+    assert focus.workspace_size(focus.CALL_ADAMW, focus.qconfig(focus.MXFP4, 8)) == 256
     assert L.focus_check_flags(None, None) == focus.ERR_WORKSPACE
