@@ -190,17 +190,20 @@ def main():
         if F.check_flags(ws_fq) != F.OK:
             raise RuntimeError("domain error in the warm-up steps")
         timer = Timer(torch)
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         torch.cuda.synchronize()
-        start.record()
-        for _ in range(args.steps):
+        marks[0].record()
+        for i in range(args.steps):
             step(timer, mx_fwd)
-        end.record()
+            marks[i + 1].record()
         torch.cuda.synchronize()
-        return start.elapsed_time(end) / args.steps, timer.summary()
+        per_step = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
+        run.per_step = per_step
+        return marks[0].elapsed_time(marks[-1]) / args.steps, timer.summary()
 
     mx_fwd = mx_primary
     ms_per_step, kern = run(mx_fwd)
+    per_step = sorted(run.per_step)
     block_loss = float(sum(L["loss"].item() for L in layers))
 
     # ---- algorithmic work ----
@@ -247,6 +250,8 @@ def main():
         "gemm": gemm,
         "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "total_ms_per_step": round(v["total_ms"] / args.steps, 4),
                         "launches_per_step": v["launches"] // args.steps} for k, v in kern.items()},
+        "step_ms": {"median": round(per_step[len(per_step) // 2], 4), "min": round(per_step[0], 4),
+                    "max": round(per_step[-1], 4)},
         "block_loss": block_loss,
         "source_hash": src_hash,
     }
@@ -263,9 +268,87 @@ def main():
                                "frac_fp4": round(f["units"] / (f["total_ms"] * 1e-3) / 1e12 / PEAK_FP4_TFLOPS, 4)},
             "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "total_ms_per_step": round(v["total_ms"] / args.steps, 4)}
                         for k, v in mx_kern.items()}}
+    result["optimizer"] = optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws_fq)
+    result["attainable"] = attainable(torch, ms_gemm=gemm_flops / (gemm_ms * 1e-3) / 1e12,
+                                      fq_GBps=fq_bytes / (fq_ms * 1e-3) / 1e9)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens, args.cpu_sample_rows)
     print(json.dumps(result), flush=True)
+
+
+def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, reps=5):
+    """Outside the step (as the optimizer and the export are): one AdamW step on every linear's S_fp
+    and c (log2 domain, the paper's learning rates), and the deployable export of every linear.
+    AdamW moves 28 B per parameter (p, g, m, v read; p, m, v written); the export reads W, S_fp and
+    c and writes the packed codes and scale bytes."""
+    lr_s, lr_c = {0: (2e-2, 5e-2), 1: (5e-3, 1e-3)}[fmt]
+    moms = [(torch.zeros_like(L["s"]), torch.zeros_like(L["s"]), torch.zeros_like(L["c"]), torch.zeros_like(L["c"]))
+            for L in layers]
+    outs = [(torch.empty(L["W"].shape[0], L["W"].shape[1] // 2, dtype=torch.uint8, device=L["W"].device),
+             torch.empty(L["W"].shape[0], L["W"].shape[1] // B, dtype=torch.uint8, device=L["W"].device))
+            for L in layers]
+    s0 = [(L["s"].clone(), L["c"].clone()) for L in layers]
+
+    def adam_all(t):
+        for L, (ms, vs, mc, vc) in zip(layers, moms):
+            F.adamw_step(L["s"], L["gs"], ms, vs, t, lr_s, log2_domain=True, ws=ws)
+            F.adamw_step(L["c"], L["gc"], mc, vc, t, lr_c, log2_domain=True, ws=ws)
+
+    def export_all():
+        for L, o in zip(layers, outs):
+            F.export_packed(L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws, out=o)
+
+    res = {}
+    for name, fn in (("adamw", lambda t: adam_all(t)), ("export", lambda t: export_all())):
+        fn(1)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for t in range(reps):
+            fn(t + 2)
+        b.record()
+        torch.cuda.synchronize()
+        res[name] = a.elapsed_time(b) / reps
+    if F.check_flags(ws) != F.OK:
+        raise RuntimeError("domain error in the optimizer step")
+    for L, (s, c) in zip(layers, s0):  # leave the timed state as it was
+        L["s"].copy_(s)
+        L["c"].copy_(c)
+    n_params = sum(L["s"].numel() + L["c"].numel() for L in layers)
+    n_w = sum(L["W"].numel() for L in layers)
+    adam_bytes = 28 * n_params
+    exp_bytes = n_w * (esz + 4.0 / B + 4.0 / sb + 0.5 + 1.0 / B)
+    return {"adamw": {"ms_per_block": round(res["adamw"], 4), "params": n_params, "launches": 2 * len(layers),
+                      "GBps": round(adam_bytes / (res["adamw"] * 1e-3) / 1e9, 1),
+                      "frac_hbm": round(adam_bytes / (res["adamw"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
+            "export": {"ms_per_block": round(res["export"], 4), "weights": n_w,
+                       "GBps": round(exp_bytes / (res["export"] * 1e-3) / 1e9, 1),
+                       "frac_hbm": round(exp_bytes / (res["export"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}}
+
+
+def attainable(torch, ms_gemm, fq_GBps):
+    """Measured attainable rates on this GPU as secondary denominators (not the product's code): a
+    1 GiB device copy and a large bf16 library GEMM (torch.mm, 8192^3, random data)."""
+    src = torch.randn(1 << 28, device="cuda").to(torch.bfloat16)
+    dst = torch.empty_like(src)
+    a = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    bt = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)  # contiguous operands only
+    res = {}
+    for name, fn, work in (("copy", lambda: dst.copy_(src), 2 * src.numel() * 2),
+                           ("gemm", lambda: torch.mm(a, bt), 2 * 8192 ** 3)):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(10):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = work / (e0.elapsed_time(e1) / 10 * 1e-3)
+    del src, dst, a, bt
+    copy_GBps, gemm_TF = res["copy"] / 1e9, res["gemm"] / 1e12
+    return {"copy_GBps": round(copy_GBps, 1), "library_bf16_gemm_TFLOPs": round(gemm_TF, 1),
+            "gemm_frac_of_library": round(ms_gemm / gemm_TF, 4), "fakequant_frac_of_copy": round(fq_GBps / copy_GBps, 4)}
 
 
 def cpu_baseline(w, sample_tokens, sample_rows):
