@@ -37,6 +37,10 @@ def parse():
     p.add_argument("--fwd-operands", choices=("bf16", "mxfp4"), default="bf16",
                    help="forward reconstruction GEMM from bf16 X_hat / W_hat, or (MXFP4 workloads) from their "
                         "packed FP4 codes and E8M0 scales on the block-scaled FP4 MFMA")
+    p.add_argument("--sub-block", type=int, default=0, help="elements per coefficient c (0 = the workload's)")
+    p.add_argument("--no-coeff", action="store_true", help="the baseline mode: no coefficients (c = 1)")
+    p.add_argument("--e8m0", choices=("ceil", "floor"), default="ceil",
+                   help="MXFP4 scale rounding: up (the paper's) or the OCP floor rule")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run an untimed 1 GiB device copy first (a known-size reference for HBM counters)")
     return p.parse_args()
@@ -110,7 +114,8 @@ def main():
         w = synth.scaled(w, M=args.tokens, name=w.name)
     dev = "cuda"
     torch.cuda.set_device(0)
-    fmt, sb, M = w.fmt, w.sub_block, w.M
+    fmt, sb, M = w.fmt, args.sub_block or w.sub_block, w.M
+    rnd = 1 if args.e8m0 == "floor" else 0
     B = w.block
 
     # ---- inputs and state, resident in HBM before timing (untimed) ----
@@ -119,8 +124,8 @@ def main():
     for lin in w.linears:
         W = synth.weight(w, lin, device=dev)
         Y = synth.reference_output(acts[lin.source], W)
-        s, c, a = F.scales_init(W, fmt, sb)
-        layers.append(dict(lin=lin, W=W, Y=Y, s=s, c=c, a=a,
+        s, c, a = F.scales_init(W, fmt, sb, e8m0_rounding=rnd)
+        layers.append(dict(lin=lin, W=W, Y=Y, s=s, c=c, cf=None if args.no_coeff else c, a=a,
                            W_hat=torch.empty_like(W),
                            gs=torch.empty_like(s), gc=torch.empty_like(c),
                            loss=torch.empty(1, dtype=torch.float64, device=dev)))
@@ -150,12 +155,13 @@ def main():
         for src, x in acts.items():
             rows, K = x.shape
             if mx_fwd:
-                timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src],
+                timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src], e8m0_rounding=rnd,
                                                                    codes_out=x_codes[src], scales_out=x_scales[src],
                                                                    scale_layout=F.SCALES_BLOCK_MAJOR),
                           rows * K)
             else:
-                timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src]), rows * K)
+                timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src], e8m0_rounding=rnd),
+                          rows * K)
         for L in layers:
             lin = L["lin"]
             xh = x_hat[lin.source]
@@ -163,8 +169,9 @@ def main():
             if mx_fwd:
                 # the forward's weight operand is the deployable export: codes + E8M0 bytes, no bf16 W_hat
                 timer.run("fakequant_weight",
-                          lambda: F.export_packed(L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws_fq,
-                                                  out=(L["Wc"], L["Ws"]), scale_layout=F.SCALES_BLOCK_MAJOR),
+                          lambda: F.export_packed(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws_fq,
+                                                  out=(L["Wc"], L["Ws"]), scale_layout=F.SCALES_BLOCK_MAJOR,
+                                                  e8m0_rounding=rnd),
                           lin.N * lin.K)
                 timer.run("recon_gemm_fwd",
                           lambda: F.recon_gemm_fwd_mxfp4(x_codes[lin.source], x_scales[lin.source], L["Wc"], L["Ws"],
@@ -172,13 +179,15 @@ def main():
                           2 * M * lin.N * lin.K)
             else:
                 timer.run("fakequant_weight",
-                          lambda: F.fakequant_fwd(L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws_fq, out=L["W_hat"]),
+                          lambda: F.fakequant_fwd(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws_fq, out=L["W_hat"],
+                                                  e8m0_rounding=rnd),
                           lin.N * lin.K)
                 timer.run("recon_gemm_fwd",
                           lambda: F.recon_gemm_fwd(xh, L["W_hat"], L["Y"], ws=ws_fwd, out=dY, loss=L["loss"]),
                           2 * M * lin.N * lin.K)
             timer.run("recon_gemm_bwd",
-                      lambda: F.recon_gemm_bwd(dY, xh, L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws_bwd,
+                      lambda: F.recon_gemm_bwd(dY, xh, L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws_bwd,
+                                               e8m0_rounding=rnd,
                                                out=(L["gs"], L["gc"])),
                       2 * M * lin.N * lin.K)
 
@@ -212,7 +221,8 @@ def main():
     # read W 2 + S_fp 4/B + c 4/sb, write W_hat 2 (or, for an MXFP4 forward, codes 0.5 + bytes 1/32)
     esz = 2 if w.dtype == "bf16" else 4
     act_b = (2 * esz + (esz if fmt == 1 else 0)) + (0.5 + 1.0 / 32 if mx_fwd else 0.0)
-    wt_b = esz + 4.0 / B + 4.0 / sb + ((0.5 + 1.0 / 32) if mx_fwd else esz)
+    c_b = 0.0 if args.no_coeff else 4.0 / sb
+    wt_b = esz + 4.0 / B + c_b + ((0.5 + 1.0 / 32) if mx_fwd else esz)
     fq_bytes = kern["fakequant_act"]["units"] * act_b + kern["fakequant_weight"]["units"] * wt_b
     fq_ms = kern["fakequant_act"]["total_ms"] + kern["fakequant_weight"]["total_ms"]
     gemm_flops = kern["recon_gemm_fwd"]["units"] + kern["recon_gemm_bwd"]["units"]
@@ -241,6 +251,7 @@ def main():
         "dtype": ("bf16+mxfp4" if mx_fwd else "bf16") if esz == 2 else "f32",
         "data": "synthetic (seeded; shapes and distributions of the calibration workload)",
         "config": {"workload": w.name, "tokens": M, "format": "mxfp4" if fmt == 0 else "nvfp4", "sub_block": sb,
+                   "coefficients": not args.no_coeff, "e8m0": args.e8m0,
                    "fwd_operands": args.fwd_operands, "linears": {l.name: [l.N, l.K] for l in w.linears}},
         "roofline": roofline,
         "fakequant_GBps": round(fq_bytes / (fq_ms * 1e-3) / 1e9, 1),
@@ -268,7 +279,7 @@ def main():
                                "frac_fp4": round(f["units"] / (f["total_ms"] * 1e-3) / 1e12 / PEAK_FP4_TFLOPS, 4)},
             "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "total_ms_per_step": round(v["total_ms"] / args.steps, 4)}
                         for k, v in mx_kern.items()}}
-    result["optimizer"] = optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws_fq)
+    result["optimizer"] = optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws_fq, rnd, c_b)
     result["attainable"] = attainable(torch, ms_gemm=gemm_flops / (gemm_ms * 1e-3) / 1e12,
                                       fq_GBps=fq_bytes / (fq_ms * 1e-3) / 1e9)
     if not args.no_cpu_baseline:
@@ -276,7 +287,7 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, reps=5):
+def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, rnd, c_b, reps=5):
     """Outside the step (as the optimizer and the export are): one AdamW step on every linear's S_fp
     and c (log2 domain, the paper's learning rates), and the deployable export of every linear.
     AdamW moves 28 B per parameter (p, g, m, v read; p, m, v written); the export reads W, S_fp and
@@ -296,7 +307,7 @@ def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, reps=5):
 
     def export_all():
         for L, o in zip(layers, outs):
-            F.export_packed(L["W"], fmt, sb, L["s"], L["c"], L["a"], ws=ws, out=o)
+            F.export_packed(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws, out=o, e8m0_rounding=rnd)
 
     res = {}
     for name, fn in (("adamw", lambda t: adam_all(t)), ("export", lambda t: export_all())):
@@ -317,7 +328,7 @@ def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, reps=5):
     n_params = sum(L["s"].numel() + L["c"].numel() for L in layers)
     n_w = sum(L["W"].numel() for L in layers)
     adam_bytes = 28 * n_params
-    exp_bytes = n_w * (esz + 4.0 / B + 4.0 / sb + 0.5 + 1.0 / B)
+    exp_bytes = n_w * (esz + 4.0 / B + c_b + 0.5 + 1.0 / B)
     return {"adamw": {"ms_per_block": round(res["adamw"], 4), "params": n_params, "launches": 2 * len(layers),
                       "GBps": round(adam_bytes / (res["adamw"] * 1e-3) / 1e9, 1),
                       "frac_hbm": round(adam_bytes / (res["adamw"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},

@@ -45,7 +45,7 @@ typedef enum {
     FOCUS_ERR_SHAPE = 2,     /* bad sizes (negative, too large, K not a multiple of the block size)
                                 or a tensor pointer that is not 16-byte aligned */
     FOCUS_ERR_DTYPE = 3,     /* unknown dtype or unsupported dtype combination */
-    FOCUS_ERR_CONFIG = 4,    /* bad focus_qconfig (format, sub_block, ste_clip, scale_layout) */
+    FOCUS_ERR_CONFIG = 4,    /* bad focus_qconfig (format, sub_block, ste_clip, scale_layout, e8m0_rounding) */
     FOCUS_ERR_WORKSPACE = 5, /* workspace NULL, misaligned or smaller than focus_workspace_size() */
     FOCUS_ERR_DOMAIN = 6,    /* focus_check_flags: a kernel met a NaN scale or a c <= 0 / non-finite */
     FOCUS_ERR_HIP = 7        /* the HIP runtime reported an error */
@@ -63,13 +63,23 @@ typedef enum { FOCUS_F32 = 0, FOCUS_BF16 = 1 } focus_dtype;
  *               0 -> m = 1 everywhere.
  *   scale_layout : layout of the scale bytes that focus_fakequant_fwd and focus_export_packed write:
  *               FOCUS_SCALES_ROW_MAJOR (0) [rows][K/B], the deployable layout; FOCUS_SCALES_BLOCK_MAJOR
- *               (1) [K/B][rows], the layout focus_recon_gemm_fwd_mxfp4 reads. Other calls ignore it. */
+ *               (1) [K/B][rows], the layout focus_recon_gemm_fwd_mxfp4 reads. Other calls ignore it.
+ *   e8m0_rounding : MXFP4 only (NVFP4 requires 0). FOCUS_E8M0_CEIL (0): Q_E8M0 rounds up, 2^e the
+ *               smallest power of two >= s (Sec. 3.1 Eq. 3, "ceiling in practice"); activation blocks use
+ *               s = fl32(amax / 6) and focus_scales_init sets S_fp = fl32(amax / 6).
+ *               FOCUS_E8M0_FLOOR (1): the OCP MX rule, e = floor(log2 s) clamped to [-127, 127];
+ *               activation blocks take e = floor(log2 amax) - 2 (2 = exponent of E2M1's largest
+ *               value, elements above 6 S saturate) and focus_scales_init sets S_fp = fl32(amax / 4),
+ *               whose floor exponent is that same OCP exponent. The straight-through derivative of
+ *               Q_E8M0 is 1 in both modes. */
 typedef enum { FOCUS_SCALES_ROW_MAJOR = 0, FOCUS_SCALES_BLOCK_MAJOR = 1 } focus_scale_layout;
+typedef enum { FOCUS_E8M0_CEIL = 0, FOCUS_E8M0_FLOOR = 1 } focus_e8m0_rounding;
 typedef struct {
     int32_t format;
     int32_t sub_block;
     int32_t ste_clip;
     int32_t scale_layout;
+    int32_t e8m0_rounding;
 } focus_qconfig;
 
 typedef void *focus_stream; /* a hipStream_t */

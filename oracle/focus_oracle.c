@@ -92,6 +92,25 @@ static int e8m0_ceil_exponent(float s, int *domain_error) {
     return e;
 }
 
+/* Q_E8M0 rounded down, the OCP MX rule: e = floor(log2 s) - drop clamped to [-127, 127] (drop = 2 for
+   an activation block's amax, the exponent of E2M1's largest value 6 = 1.5 * 2^2; drop = 0 for a
+   learned scale). frexp gives s = m * 2^E with m in [0.5, 1), so floor(log2 s) = E - 1 exactly, for
+   subnormal s too. Non-positive s takes 2^-127, +inf 2^127; NaN is a domain error. */
+static int e8m0_floor_exponent(float s, int drop, int *domain_error) {
+    if (isnan(s)) {
+        *domain_error = 1;
+        return -127;
+    }
+    if (!(s > 0.0f)) return -127;
+    if (isinf(s)) return 127;
+    int E;
+    (void)frexp((double)s, &E);
+    int e = E - 1 - drop;
+    if (e < -127) e = -127;
+    if (e > 127) e = 127;
+    return e;
+}
+
 /* 2^e as an fp32 value; 2^-127 is an fp32 subnormal and is represented exactly */
 static float pow2f(int e) { return (float)ldexp(1.0, e); }
 
@@ -176,6 +195,12 @@ int oracle_e8m0_ceil_array(const float *s, int64_t n, uint8_t *byte) {
     return err;
 }
 
+int oracle_e8m0_floor_array(const float *s, int64_t n, uint8_t *byte) {
+    int err = 0;
+    for (int64_t i = 0; i < n; i++) byte[i] = (uint8_t)(e8m0_floor_exponent(s[i], 0, &err) + 127);
+    return err;
+}
+
 int oracle_e4m3_array(const float *x, int64_t n, uint8_t *byte) {
     int err = 0;
     e4m3_table_init();
@@ -195,9 +220,10 @@ static int block_size_of(int fmt) { return fmt == FMT_MXFP4 ? 32 : 16; }
 
 /* ------------------------------------------------------------------------------------------ */
 /* Scale initialisation by absmax (Sec. 3.2: "initialized via absmax"; Eq. 2 and Eq. 3).
-   MXFP4: S_fp = fl32(amax / 6).  NVFP4: alpha = fl32(max|W| / (6 * 448)) (alpha = 1 if W == 0),
+   MXFP4: S_fp = fl32(amax / 6), or fl32(amax / 4) under the OCP floor rule (whose E8M0 is then the
+   OCP exponent floor(log2 amax) - 2).  NVFP4: alpha = fl32(max|W| / (6 * 448)) (alpha = 1 if W == 0),
    Delta_fp = fl32(amax / fl32(alpha * 6)). Coefficients c start at 1 (Sec. 3.3, Sec. 3.4). */
-int oracle_init_scales(int fmt, int sb, const float *W, int64_t rows, int64_t K,
+int oracle_init_scales(int fmt, int sb, int e8m0_floor, const float *W, int64_t rows, int64_t K,
                        float *s_fp, float *c, float *alpha_out) {
     int B = block_size_of(fmt);
     int64_t nb = K / B, ns = K / sb;
@@ -212,7 +238,7 @@ int oracle_init_scales(int fmt, int sb, const float *W, int64_t rows, int64_t K,
         for (int64_t b = 0; b < nb; b++) {
             float amax = 0.0f;
             for (int j = 0; j < B; j++) amax = fmaxf(amax, fabsf(W[r * K + b * B + j]));
-            if (fmt == FMT_MXFP4) s_fp[r * nb + b] = amax / 6.0f;
+            if (fmt == FMT_MXFP4) s_fp[r * nb + b] = e8m0_floor ? amax / 4.0f : amax / 6.0f;
             else s_fp[r * nb + b] = amax / (alpha * 6.0f);
         }
         for (int64_t k = 0; k < ns; k++) c[r * ns + k] = 1.0f;
@@ -228,7 +254,7 @@ int oracle_init_scales(int fmt, int sb, const float *W, int64_t rows, int64_t K,
    Also returns what the straight-through backward needs: u, the clamp mask m = [|u| <= 6]
    (m = 1 everywhere when ste_clip == 0), S_dq per block and S_q per sub-block.
    Optional outputs may be NULL. Returns nonzero if a NaN scale or c <= 0 / non-finite c was seen. */
-int oracle_fq_weight(int fmt, int sb, int ste_clip, const float *W, int64_t rows, int64_t K,
+int oracle_fq_weight(int fmt, int sb, int ste_clip, int e8m0_floor, const float *W, int64_t rows, int64_t K,
                      const float *s_fp, const float *c, float alpha,
                      float *w_hat, uint8_t *codes, uint8_t *scale_bytes,
                      float *u_out, uint8_t *m_out, float *sdq_out, float *sq_out) {
@@ -241,7 +267,8 @@ int oracle_fq_weight(int fmt, int sb, int ste_clip, const float *W, int64_t rows
             float sdq;
             int byte;
             if (fmt == FMT_MXFP4) {
-                int e = e8m0_ceil_exponent(s_fp[r * nb + b], &err);
+                int e = e8m0_floor ? e8m0_floor_exponent(s_fp[r * nb + b], 0, &err)
+                                   : e8m0_ceil_exponent(s_fp[r * nb + b], &err);
                 sdq = pow2f(e);
                 byte = e + 127;
             } else {
@@ -286,11 +313,11 @@ int oracle_fq_weight(int fmt, int sb, int ste_clip, const float *W, int64_t rows
 /* Dynamic activation fake quantisation of X [rows][K] (Sec. 3.2: activation quantisation stays
    fully dynamic; Sec. 4.1: weights and activations of all linear layers are quantised). The
    scales are recomputed from X by the absmax rules of Eq. (2)-(3) with no coefficients (c = 1):
-     MXFP4: S = 2^E8M0(fl32(amax / 6))
+     MXFP4: S = 2^E8M0(fl32(amax / 6)), or under the OCP floor rule S = 2^(floor(log2 amax) - 2)
      NVFP4: alpha = fl32(max|X| / 2688) over the whole X (R7); Delta = Q_E4M3(fl32(amax / fl32(alpha*6)));
             S = fl32(alpha * Delta)
    then u = fl32(x / S), code = Q_E2M1(u), x_hat = fl32(q * S). Multithreaded over rows. */
-int oracle_fq_act(int fmt, const float *X, int64_t rows, int64_t K,
+int oracle_fq_act(int fmt, int e8m0_floor, const float *X, int64_t rows, int64_t K,
                   float *x_hat, uint8_t *codes, uint8_t *scale_bytes, float *alpha_out) {
     int B = block_size_of(fmt);
     int64_t nb = K / B;
@@ -313,7 +340,7 @@ int oracle_fq_act(int fmt, const float *X, int64_t rows, int64_t K,
             float S;
             int byte;
             if (fmt == FMT_MXFP4) {
-                int e = e8m0_ceil_exponent(amax / 6.0f, &err);
+                int e = e8m0_floor ? e8m0_floor_exponent(amax, 2, &err) : e8m0_ceil_exponent(amax / 6.0f, &err);
                 S = pow2f(e);
                 byte = e + 127;
             } else {

@@ -69,13 +69,14 @@ def _lib():
         lib.oracle_e4m3_array.argtypes = [p, i64, p]
         lib.oracle_e4m3_decode_array.argtypes = [p, i64, p]
         lib.oracle_bf16_round_array.argtypes = [p, i64, p]
-        lib.oracle_init_scales.argtypes = [i32, i32, p, i64, i64, p, p, p]
-        lib.oracle_fq_weight.argtypes = [i32, i32, i32, p, i64, i64, p, p, f32, p, p, p, p, p, p, p]
-        lib.oracle_fq_act.argtypes = [i32, p, i64, i64, p, p, p, p]
+        lib.oracle_init_scales.argtypes = [i32, i32, i32, p, i64, i64, p, p, p]
+        lib.oracle_fq_weight.argtypes = [i32, i32, i32, i32, p, i64, i64, p, p, f32, p, p, p, p, p, p, p]
+        lib.oracle_fq_act.argtypes = [i32, i32, p, i64, i64, p, p, p, p]
+        lib.oracle_e8m0_floor_array.argtypes = [p, i64, p]
         lib.oracle_pack_codes.argtypes = [p, i64, i64, p]
         lib.oracle_unpack_codes.argtypes = [p, i64, i64, p]
         lib.oracle_decode_packed.argtypes = [i32, p, p, f32, i64, i64, p]
-        for name in ("oracle_e8m0_ceil_array", "oracle_e4m3_array", "oracle_init_scales",
+        for name in ("oracle_e8m0_ceil_array", "oracle_e8m0_floor_array", "oracle_e4m3_array", "oracle_init_scales",
                      "oracle_fq_weight", "oracle_fq_act"):
             getattr(lib, name).restype = ctypes.c_int
         _LIB = lib
@@ -111,6 +112,14 @@ def e2m1_decode(code) -> np.ndarray:
     v = np.empty(code.shape, np.float32)
     _lib().oracle_e2m1_decode_array(_ptr(code), code.size, _ptr(v))
     return v
+
+
+def e8m0_floor(s) -> np.ndarray:
+    """Q_E8M0 rounded down (the OCP MX rule): the byte e + 127 of the largest 2^e <= s."""
+    s = _f32(s)
+    out = np.empty(s.shape, np.uint8)
+    _lib().oracle_e8m0_floor_array(_ptr(s), s.size, _ptr(out))
+    return out
 
 
 def e8m0_ceil(s) -> np.ndarray:
@@ -157,7 +166,7 @@ def bf16_to_f32(bits) -> np.ndarray:
 # Scale initialisation and fake quantisation
 # ---------------------------------------------------------------------------------------------
 
-def init_scales(W, fmt: int, sb: int):
+def init_scales(W, fmt: int, sb: int, e8m0_floor: bool = False):
     """Absmax initialisation (Sec. 3.2) -> (s_fp [N][K/B], c [N][K/sb] = 1, alpha)."""
     W = _f32(W)
     N, K = W.shape
@@ -165,7 +174,7 @@ def init_scales(W, fmt: int, sb: int):
     s_fp = np.empty((N, K // B), np.float32)
     c = np.empty((N, K // sb), np.float32)
     alpha = np.ones(1, np.float32)
-    _lib().oracle_init_scales(fmt, sb, _ptr(W), N, K, _ptr(s_fp), _ptr(c), _ptr(alpha))
+    _lib().oracle_init_scales(fmt, sb, int(e8m0_floor), _ptr(W), N, K, _ptr(s_fp), _ptr(c), _ptr(alpha))
     return s_fp, c, float(alpha[0])
 
 
@@ -184,7 +193,8 @@ class WeightFQ:
     c: np.ndarray | None     # fp32 [N][K/sb] the coefficients used (None means all ones)
 
 
-def fq_weight(W, fmt: int, sb: int, s_fp, c, alpha: float = 1.0, ste_clip: bool = True) -> WeightFQ:
+def fq_weight(W, fmt: int, sb: int, s_fp, c, alpha: float = 1.0, ste_clip: bool = True,
+              e8m0_floor: bool = False) -> WeightFQ:
     W = _f32(W)
     N, K = W.shape
     B = block_size(fmt)
@@ -195,13 +205,13 @@ def fq_weight(W, fmt: int, sb: int, s_fp, c, alpha: float = 1.0, ste_clip: bool 
                    np.empty((N, K), np.uint8), np.empty((N, K // B), np.float32),
                    np.empty((N, K // sb), np.float32), 0, W, c)
     out.domain_error = _lib().oracle_fq_weight(
-        fmt, sb, int(ste_clip), _ptr(W), N, K, _ptr(s_fp), _ptr(c), float(alpha),
+        fmt, sb, int(ste_clip), int(e8m0_floor), _ptr(W), N, K, _ptr(s_fp), _ptr(c), float(alpha),
         _ptr(out.w_hat), _ptr(out.codes), _ptr(out.scale_bytes), _ptr(out.u), _ptr(out.m),
         _ptr(out.s_dq), _ptr(out.s_q))
     return out
 
 
-def fq_act(X, fmt: int):
+def fq_act(X, fmt: int, e8m0_floor: bool = False):
     """Dynamic activation fake quantisation -> (x_hat fp32, codes, scale_bytes, alpha)."""
     X = _f32(X)
     M, K = X.shape
@@ -210,7 +220,7 @@ def fq_act(X, fmt: int):
     codes = np.empty((M, K), np.uint8)
     sb = np.empty((M, K // B), np.uint8)
     alpha = np.ones(1, np.float32)
-    _lib().oracle_fq_act(fmt, _ptr(X), M, K, _ptr(x_hat), _ptr(codes), _ptr(sb), _ptr(alpha))
+    _lib().oracle_fq_act(fmt, int(e8m0_floor), _ptr(X), M, K, _ptr(x_hat), _ptr(codes), _ptr(sb), _ptr(alpha))
     return x_hat, codes, sb, float(alpha[0])
 
 

@@ -22,8 +22,12 @@ focus_status check_q(const focus_qconfig *q) {
     if (!(sb == 2 || sb == 4 || sb == 8 || sb == 16 || sb == 32) || B % sb != 0) return FOCUS_ERR_CONFIG;
     if (q->ste_clip != 0 && q->ste_clip != 1) return FOCUS_ERR_CONFIG;
     if (q->scale_layout != FOCUS_SCALES_ROW_MAJOR && q->scale_layout != FOCUS_SCALES_BLOCK_MAJOR) return FOCUS_ERR_CONFIG;
+    if (q->e8m0_rounding != FOCUS_E8M0_CEIL && q->e8m0_rounding != FOCUS_E8M0_FLOOR) return FOCUS_ERR_CONFIG;
+    if (q->e8m0_rounding == FOCUS_E8M0_FLOOR && q->format != FOCUS_MXFP4) return FOCUS_ERR_CONFIG;
     return FOCUS_OK;
 }
+
+int floor_of(const focus_qconfig *q) { return q->e8m0_rounding == FOCUS_E8M0_FLOOR ? 1 : 0; }
 
 bool dtype_ok(int d) { return d == FOCUS_F32 || d == FOCUS_BF16; }
 
@@ -106,7 +110,7 @@ focus_status focus_scales_init(const focus_qconfig *q, const void *W, int w_dtyp
     if (!all_aligned({W})) return FOCUS_ERR_SHAPE;
     FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_SCALES_INIT, q, 0, N, K)));
     if (N == 0 || K == 0) return FOCUS_OK;
-    return hip_status(launch_scales_init(q->format, w_dtype, W, N, K, s_fp, c, q->sub_block, alpha_out,
+    return hip_status(launch_scales_init(q->format, w_dtype, W, N, K, s_fp, c, q->sub_block, floor_of(q), alpha_out,
                                          partials_of(ws), (hipStream_t)stream));
 }
 
@@ -127,9 +131,10 @@ focus_status focus_fakequant_fwd(const focus_qconfig *q, const void *X, int x_dt
     hipStream_t st = (hipStream_t)stream;
     if (weight_mode)
         return hip_status(launch_fq_weight(q->format, x_dtype, xhat_dtype, X, rows, K, s_fp, c, q->sub_block,
-                                           alpha, X_hat, codes_opt, scale_bytes_opt, q->scale_layout, flag_of(ws), st));
+                                           alpha, floor_of(q), X_hat, codes_opt, scale_bytes_opt, q->scale_layout, flag_of(ws), st));
     return hip_status(launch_fq_act(q->format, x_dtype, xhat_dtype, X, rows, K, X_hat, codes_opt,
-                                    scale_bytes_opt, q->scale_layout, alpha_out_opt, partials_of(ws), flag_of(ws), st));
+                                    scale_bytes_opt, q->scale_layout, floor_of(q), alpha_out_opt, partials_of(ws),
+                                    flag_of(ws), st));
 }
 
 focus_status focus_fakequant_bwd(const focus_qconfig *q, const float *G, int64_t N, int64_t K, const void *W,
@@ -144,7 +149,7 @@ focus_status focus_fakequant_bwd(const focus_qconfig *q, const float *G, int64_t
     FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_FAKEQUANT_BWD, q, 0, N, K)));
     if (N == 0 || K == 0) return FOCUS_OK;
     return hip_status(launch_fq_bwd(q->format, w_dtype, G, N, K, W, s_fp, c, q->sub_block, alpha, q->ste_clip,
-                                    grad_s, grad_c, flag_of(ws), (hipStream_t)stream));
+                                    floor_of(q), grad_s, grad_c, flag_of(ws), (hipStream_t)stream));
 }
 
 focus_status focus_recon_gemm_fwd(const void *X_hat, const void *W_hat, int op_dtype, int64_t M, int64_t N,
@@ -200,7 +205,7 @@ focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const 
     FOCUS_TRY(check_ws(ws, ws_bytes, bwd_ws(q->format, q->sub_block, M, N, K)));
     if (N == 0 || K == 0) return FOCUS_OK;
     const BwdPlan p = plan_bwd(op_dtype, q->format, q->sub_block, M, N, K, G_out_opt != nullptr);
-    return hip_status(launch_recon_bwd(p, op_dtype, q->format, q->sub_block, q->ste_clip, dY, X_hat, M, N, K, W,
+    return hip_status(launch_recon_bwd(p, op_dtype, q->format, q->sub_block, q->ste_clip, floor_of(q), dY, X_hat, M, N, K, W,
                                        w_dtype, s_fp, c, alpha, grad_s, grad_c, G_out_opt, ws, flag_of(ws),
                                        (hipStream_t)stream));
 }
@@ -217,7 +222,7 @@ focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dt
     FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_EXPORT_PACKED, q, 0, N, K)));
     if (N == 0 || K == 0) return FOCUS_OK;
     return hip_status(launch_fq_weight(q->format, w_dtype, w_dtype, W, N, K, s_fp, c, q->sub_block, alpha,
-                                       nullptr, packed, scale_bytes, q->scale_layout, flag_of(ws), (hipStream_t)stream));
+                                       floor_of(q), nullptr, packed, scale_bytes, q->scale_layout, flag_of(ws), (hipStream_t)stream));
 }
 
 focus_status focus_adamw_step(const focus_adamw_config *cfg, int64_t t, int64_t n, float *param, const float *grad,

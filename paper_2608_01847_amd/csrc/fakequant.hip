@@ -41,7 +41,7 @@ template <int FMT, int IN, int OUT>
 __global__ void __launch_bounds__(256)
 fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
                  const float *__restrict__ s_fp, const float *__restrict__ c, int sb_log2,
-                 const float *__restrict__ alpha_ptr, int ste_clip, void *__restrict__ w_hat,
+                 const float *__restrict__ alpha_ptr, int e8m0_floor, void *__restrict__ w_hat,
                  uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes, int64_t rows_total,
                  int block_major, uint32_t *flag) {
     constexpr int B = block_of(FMT);
@@ -58,7 +58,7 @@ fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int
         float v[8];
         load8(W, IN, e0, v);
         uint32_t byte;
-        const float sdq = weight_sdq(FMT, s_fp[e0 / B], alpha, byte, bad);
+        const float sdq = weight_sdq(FMT, s_fp[e0 / B], alpha, e8m0_floor, byte, bad);
         float cv[4] = {1.0f, 1.0f, 1.0f, 1.0f};
         const int ncoef = sb >= 8 ? 1 : 8 >> sb_log2;
         if (c) {
@@ -83,18 +83,18 @@ fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int
             scale_bytes[scale_index<B>(e0, t, cpr, row0, rows_total, block_major)] = (uint8_t)byte;
     }
     if (bad) raise_domain_flag(flag);
-    (void)ste_clip;
 }
 
 // ------------------------------------------------------------------------------------------------
 // K2 (MXFP4): dynamic activation fake quantisation, one pass. Block of 32 = 4 lanes.
-// S = 2^e with e = E8M0_up(fl32(amax / 6)); u = x / S is computed as x * 2^-e, which is the same
-// correctly rounded value because 2^-e is exact for every e in [-127, 127].
+// S = 2^e with e = E8M0_up(fl32(amax / 6)), or with e8m0_floor the OCP rule e = floor(log2 amax) - 2;
+// u = x / S is computed as x * 2^-e, which is the same correctly rounded value because 2^-e is exact
+// for every e in [-127, 127].
 template <int IN, int OUT>
 __global__ void __launch_bounds__(256)
 fq_act_mx_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
                  void *__restrict__ x_hat, uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes,
-                 int64_t rows_total, int block_major, uint32_t *flag) {
+                 int64_t rows_total, int block_major, int e8m0_floor, uint32_t *flag) {
     // Rows are contiguous, so chunk t (8 elements) starts at element row0 K + 8 t. Launched with one
     // chunk per thread (the loop is a guard).
     const int64_t e_row0 = row0 * K;
@@ -107,7 +107,7 @@ fq_act_mx_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
 #pragma unroll
         for (int i = 0; i < 8; i++) amax = fmaxf(amax, __builtin_fabsf(v[i]));
         amax = group_max(amax, 4);
-        const int e = e8m0_ceil_exp(amax / 6.0f, bad);
+        const int e = e8m0_floor ? e8m0_floor_exp(amax, 2, bad) : e8m0_ceil_exp(amax / 6.0f, bad);
         const float S = exp2i(e), inv = exp2i(-e);
         // u = x 2^-e has the sign of x, so the hardware code's sign bit is the code's; element i
         // lands in nibble i
@@ -219,13 +219,14 @@ fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
 }
 
 // ------------------------------------------------------------------------------------------------
-// K8: absmax initialisation (Sec. 3.2). MXFP4: s = fl32(amax / 6). NVFP4: Delta_fp =
+// K8: absmax initialisation (Sec. 3.2). MXFP4: s = fl32(amax / 6) (E8M0 rounded up), or fl32(amax / 4)
+// with the OCP floor rule, whose E8M0 is then floor(log2 amax) - 2. NVFP4: Delta_fp =
 // fl32(amax / fl32(alpha * 6)) with alpha from the partial maxima; c = 1.
 template <int FMT, int IN>
 __global__ void __launch_bounds__(256)
 scales_init_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
                    const float *__restrict__ alpha_slot, float *__restrict__ s_fp, float *__restrict__ c,
-                   int sb_log2, float *__restrict__ alpha_out) {
+                   int sb_log2, int e8m0_floor, float *__restrict__ alpha_out) {
     constexpr int B = block_of(FMT);
     float alpha = 1.0f;
     if (FMT == kFmtNV) alpha = *alpha_slot;  // alpha_out was written with the slot
@@ -241,7 +242,8 @@ scales_init_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, i
 #pragma unroll
         for (int i = 0; i < 8; i++) amax = fmaxf(amax, __builtin_fabsf(v[i]));
         amax = group_max(amax, B / 8);
-        if ((e0 % B) == 0) s_fp[e0 / B] = FMT == kFmtMX ? amax / 6.0f : amax / (alpha * 6.0f);
+        if ((e0 % B) == 0)
+            s_fp[e0 / B] = FMT == kFmtMX ? (e8m0_floor ? amax / 4.0f : amax / 6.0f) : amax / (alpha * 6.0f);
         if (sb >= 8) {
             if ((e0 % sb) == 0) c[e0 >> sb_log2] = 1.0f;
         } else {
@@ -257,7 +259,7 @@ template <int FMT, int WDT>
 __global__ void __launch_bounds__(256)
 fq_bwd_kernel(const float *__restrict__ G, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
               const void *__restrict__ W, const float *__restrict__ s_fp, const float *__restrict__ c,
-              int sb_log2, const float *__restrict__ alpha_ptr, int ste_clip,
+              int sb_log2, const float *__restrict__ alpha_ptr, int ste_clip, int e8m0_floor,
               float *__restrict__ grad_s, float *__restrict__ grad_c, uint32_t *flag) {
     constexpr int B = block_of(FMT);
     const float alpha = FMT == kFmtNV ? *alpha_ptr : 1.0f;
@@ -272,7 +274,7 @@ fq_bwd_kernel(const float *__restrict__ G, uint32_t nchunks, uint32_t cpr, int64
         load8(W, WDT, e0, w);
         load8(G, kF32, e0, g);
         uint32_t byte;
-        const float sdq = weight_sdq(FMT, s_fp[e0 / B], alpha, byte, bad);
+        const float sdq = weight_sdq(FMT, s_fp[e0 / B], alpha, e8m0_floor, byte, bad);
         float cv[4] = {1.0f, 1.0f, 1.0f, 1.0f};
         const int ncoef = sb >= 8 ? 1 : 8 >> sb_log2;
         if (c) {
@@ -333,11 +335,12 @@ static int log2i(int v) {
 }
 
 hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64_t rows, int64_t K,
-                            const float *s_fp, const float *c, int sb, const float *alpha, void *w_hat,
-                            uint8_t *codes, uint8_t *scale_bytes, int block_major, uint32_t *flag, hipStream_t st) {
+                            const float *s_fp, const float *c, int sb, const float *alpha, int e8m0_floor,
+                            void *w_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, uint32_t *flag,
+                            hipStream_t st) {
     const int sbl = log2i(sb);
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-#define FQW(F, I, O) fq_weight_kernel<F, I, O><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, s_fp, c, sbl, alpha, 1, w_hat, codes, scale_bytes, rows, block_major, flag)
+#define FQW(F, I, O) fq_weight_kernel<F, I, O><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, s_fp, c, sbl, alpha, e8m0_floor, w_hat, codes, scale_bytes, rows, block_major, flag)
         if (fmt == kFmtMX) {
             if (in_dt == kBF16) { if (out_dt == kBF16) FQW(kFmtMX, kBF16, kBF16); else FQW(kFmtMX, kBF16, kF32); }
             else { if (out_dt == kBF16) FQW(kFmtMX, kF32, kBF16); else FQW(kFmtMX, kF32, kF32); }
@@ -360,11 +363,11 @@ static hipError_t launch_tensor_alpha(int in_dt, const void *X, int64_t n, float
 }
 
 hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t rows, int64_t K,
-                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, float *alpha_out,
-                         float *partial, uint32_t *flag, hipStream_t st) {
+                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, int e8m0_floor,
+                         float *alpha_out, float *partial, uint32_t *flag, hipStream_t st) {
     if (fmt == kFmtMX) {
         return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-#define FQA(I, O) fq_act_mx_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, x_hat, codes, scale_bytes, rows, block_major, flag)
+#define FQA(I, O) fq_act_mx_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, x_hat, codes, scale_bytes, rows, block_major, e8m0_floor, flag)
             if (in_dt == kBF16) { if (out_dt == kBF16) FQA(kBF16, kBF16); else FQA(kBF16, kF32); }
             else { if (out_dt == kBF16) FQA(kF32, kBF16); else FQA(kF32, kF32); }
 #undef FQA
@@ -382,7 +385,7 @@ hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t 
 }
 
 hipError_t launch_scales_init(int fmt, int in_dt, const void *W, int64_t rows, int64_t K, float *s_fp,
-                              float *c, int sb, float *alpha_out, float *partial, hipStream_t st) {
+                              float *c, int sb, int e8m0_floor, float *alpha_out, float *partial, hipStream_t st) {
     const int sbl = log2i(sb);
     if (fmt == kFmtNV) {
         hipError_t e = launch_tensor_alpha(in_dt, W, rows * K, partial, alpha_out, st);
@@ -391,7 +394,7 @@ hipError_t launch_scales_init(int fmt, int in_dt, const void *W, int64_t rows, i
     const float *slot = partial + kAbsmaxParts;
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
         float *ao = r0 == 0 && fmt == kFmtMX ? alpha_out : nullptr;
-#define SI(F, I) scales_init_kernel<F, I><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, slot, s_fp, c, sbl, ao)
+#define SI(F, I) scales_init_kernel<F, I><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, slot, s_fp, c, sbl, e8m0_floor, ao)
         if (fmt == kFmtMX) { if (in_dt == kBF16) SI(kFmtMX, kBF16); else SI(kFmtMX, kF32); }
         else { if (in_dt == kBF16) SI(kFmtNV, kBF16); else SI(kFmtNV, kF32); }
 #undef SI
@@ -400,10 +403,10 @@ hipError_t launch_scales_init(int fmt, int in_dt, const void *W, int64_t rows, i
 
 hipError_t launch_fq_bwd(int fmt, int w_dt, const float *G, int64_t rows, int64_t K, const void *W,
                          const float *s_fp, const float *c, int sb, const float *alpha, int ste_clip,
-                         float *grad_s, float *grad_c, uint32_t *flag, hipStream_t st) {
+                         int e8m0_floor, float *grad_s, float *grad_c, uint32_t *flag, hipStream_t st) {
     const int sbl = log2i(sb);
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-#define FQB(F, WD) fq_bwd_kernel<F, WD><<<grid, 256, 0, st>>>(G, n, cpr, r0, K, W, s_fp, c, sbl, alpha, ste_clip, grad_s, grad_c, flag)
+#define FQB(F, WD) fq_bwd_kernel<F, WD><<<grid, 256, 0, st>>>(G, n, cpr, r0, K, W, s_fp, c, sbl, alpha, ste_clip, e8m0_floor, grad_s, grad_c, flag)
         if (fmt == kFmtMX) { if (w_dt == kBF16) FQB(kFmtMX, kBF16); else FQB(kFmtMX, kF32); }
         else { if (w_dt == kBF16) FQB(kFmtNV, kBF16); else FQB(kFmtNV, kF32); }
 #undef FQB

@@ -68,6 +68,23 @@ __device__ __forceinline__ int e8m0_ceil_exp(float s, bool &nan_seen) {
     return e;
 }
 
+// E8M0 rounded down, the OCP MX rule: e = floor(log2 s) - drop, clamped to [-127, 127] (drop = 2 for an
+// activation block's amax, the exponent of E2M1's largest value; drop = 0 for a learned scale).
+// Non-positive s (and -0) -> -127; +inf -> 127; NaN sets *nan_seen and gives -127. floor(log2 s) is
+// exact for subnormal s too (from the position of the leading mantissa bit).
+__device__ __forceinline__ int e8m0_floor_exp(float s, int drop, bool &nan_seen) {
+    const uint32_t b = __float_as_uint(s);
+    const bool nan = (b & 0x7FFFFFFFu) > 0x7F800000u;
+    const uint32_t E = b >> 23, man = b & 0x7FFFFFu;
+    int e = E != 0u ? (int)E - 127 : (31 - __builtin_clz(man | 1u)) - 149;
+    e -= drop;
+    e = e < -127 ? -127 : e;
+    e = e > 127 ? 127 : e;
+    e = (nan || (int32_t)b <= 0) ? -127 : e;
+    nan_seen = nan_seen || nan;
+    return e;
+}
+
 // 2^e as fp32 for e in [-127, 127]; 2^-127 is the subnormal 0x00400000.
 __device__ __forceinline__ float exp2i(int e) {
     return e >= -126 ? __uint_as_float((uint32_t)(e + 127) << 23) : __uint_as_float(0x00400000u);
@@ -171,11 +188,13 @@ __device__ __forceinline__ Quantized quantize_element(float x, float sq, float s
     return r;
 }
 
-// Dequantisation scale of one weight block from its learnable copy (Eq. 4): MXFP4 2^E8M0_up(s),
-// NVFP4 fl32(alpha * Q_E4M3(s)). Also returns the exported scale byte.
-__device__ __forceinline__ float weight_sdq(int fmt, float s, float alpha, uint32_t &byte, bool &nan_seen) {
+// Dequantisation scale of one weight block from its learnable copy (Eq. 4): MXFP4 2^E8M0(s), rounded
+// up (default) or down (e8m0_floor, the OCP rule), NVFP4 fl32(alpha * Q_E4M3(s)). Also returns the
+// exported scale byte.
+__device__ __forceinline__ float weight_sdq(int fmt, float s, float alpha, int e8m0_floor, uint32_t &byte,
+                                            bool &nan_seen) {
     if (fmt == kFmtMX) {
-        int e = e8m0_ceil_exp(s, nan_seen);
+        int e = e8m0_floor ? e8m0_floor_exp(s, 0, nan_seen) : e8m0_ceil_exp(s, nan_seen);
         byte = (uint32_t)(e + 127);
         return exp2i(e);
     }

@@ -83,7 +83,7 @@ template <int DT, int FMT, int WDT>
 __global__ void __launch_bounds__(256)
 bwd_valu_kernel(const void *__restrict__ dY, const void *__restrict__ X, int64_t M, int64_t N, int64_t K,
                 int64_t chunk, const void *__restrict__ W, const float *__restrict__ s_fp,
-                const float *__restrict__ c, int sb, const float *__restrict__ alpha_ptr, int ste_clip,
+                const float *__restrict__ c, int sb, const float *__restrict__ alpha_ptr, int ste_clip, int e8m0_floor,
                 float *__restrict__ part_s, float *__restrict__ part_c, float *__restrict__ G_out,
                 uint32_t *flag) {
     constexpr int B = block_of(FMT);
@@ -131,7 +131,7 @@ bwd_valu_kernel(const void *__restrict__ dY, const void *__restrict__ X, int64_t
             if (n < N && k < K) {
                 if (G_out) G_out[n * K + k] = acc[i][j];
                 uint32_t byte;
-                const float sdq = weight_sdq(FMT, s_fp[n * nb + k / B], alpha, byte, bad);
+                const float sdq = weight_sdq(FMT, s_fp[n * nb + k / B], alpha, e8m0_floor, byte, bad);
                 const float cv = c ? c[n * ns + k / sb] : 1.0f;
                 bad |= bad_coeff(cv);
                 ste_terms(acc[i][j], load1(W, WDT, n * K + k), sdq, cv, ste_clip != 0, tc, ts);
@@ -311,7 +311,7 @@ hipError_t launch_recon_fwd_mx(const void *Xc, const void *Xs, const void *Wc, c
     return launch_fwd_finish(mtiles, M, N, colpart, col_sq, loss_out, st);
 }
 
-hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int ste_clip, const void *dY,
+hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int ste_clip, int e8m0_floor, const void *dY,
                             const void *X, int64_t M, int64_t N, int64_t K, const void *W, int w_dt,
                             const float *s_fp, const float *c, const float *alpha, float *grad_s,
                             float *grad_c, float *G_out, void *ws, uint32_t *flag, hipStream_t st) {
@@ -320,11 +320,11 @@ hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int st
     float *part_c = part_s + p.splits * N * nb;
     if (p.path == 1) {
         hipError_t e = launch_bwd_mfma(fmt, w_dt, dY, X, M, N, K, p.chunk, p.splits, W, s_fp, c, sb,
-                                       alpha, ste_clip, part_s, part_c, flag, st);
+                                       alpha, ste_clip, e8m0_floor, part_s, part_c, flag, st);
         if (e != hipSuccess) return e;
     } else {
         dim3 grid((unsigned)cdiv(K, 64), (unsigned)cdiv(N, 64), (unsigned)p.splits);
-#define BV(D, F, WD) bwd_valu_kernel<D, F, WD><<<grid, 256, 0, st>>>(dY, X, M, N, K, p.chunk, W, s_fp, c, sb, alpha, ste_clip, part_s, part_c, G_out, flag)
+#define BV(D, F, WD) bwd_valu_kernel<D, F, WD><<<grid, 256, 0, st>>>(dY, X, M, N, K, p.chunk, W, s_fp, c, sb, alpha, ste_clip, e8m0_floor, part_s, part_c, G_out, flag)
         if (op_dt == kBF16) {
             if (fmt == kFmtMX) { if (w_dt == kBF16) BV(kBF16, kFmtMX, kBF16); else BV(kBF16, kFmtMX, kF32); }
             else { if (w_dt == kBF16) BV(kBF16, kFmtNV, kBF16); else BV(kBF16, kFmtNV, kF32); }

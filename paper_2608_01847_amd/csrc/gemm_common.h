@@ -43,7 +43,7 @@ hipError_t launch_fwd_mfma_mx(const void *Xc, const void *Xs, const void *Wc, co
                               int64_t K, const void *Yref, void *dY, float dscale, double *colpart, hipStream_t st);
 hipError_t launch_bwd_mfma(int fmt, int w_dt, const void *dY, const void *X, int64_t M, int64_t N, int64_t K,
                            int64_t chunk, int64_t splits, const void *W, const float *s_fp, const float *c,
-                           int sb, const float *alpha, int ste_clip, float *part_s, float *part_c,
-                           uint32_t *flag, hipStream_t st);
+                           int sb, const float *alpha, int ste_clip, int e8m0_floor, float *part_s,
+                           float *part_c, uint32_t *flag, hipStream_t st);
 
 }  // namespace focus

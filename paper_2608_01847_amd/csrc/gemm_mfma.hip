@@ -522,7 +522,7 @@ __global__ void __launch_bounds__(kThreads, 1)
 bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X, int64_t M, int64_t N, int64_t K,
                 int64_t chunk, const void *__restrict__ W, const float *__restrict__ s_fp,
                 const float *__restrict__ c, int sb_log2, const float *__restrict__ alpha_ptr, int ste_clip,
-                float *__restrict__ part_s, float *__restrict__ part_c, uint32_t *flag, int tiles_n) {
+                int e8m0_floor, float *__restrict__ part_s, float *__restrict__ part_c, uint32_t *flag, int tiles_n) {
     __shared__ __attribute__((aligned(16))) char smem[kBwdStages * kBwdStageBytes];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
     // linear id -> (split, tile): splits outermost, tiles of one split in grouped order, so that an
@@ -676,7 +676,7 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
             static_for<NBI>([&](auto h) {
                 bool nan = false;
                 uint32_t byte;
-                sdq[h] = weight_sdq(FMT, sv[i][h], alpha, byte, nan);
+                sdq[h] = weight_sdq(FMT, sv[i][h], alpha, e8m0_floor, byte, nan);
                 bad = bad || (n_ok && kb + h * B < K32 && nan);
             });
             float tc[4][2];  // per group of 8 k: this lane's sums of G m w over elements 0-1 / 2-3
@@ -796,14 +796,14 @@ hipError_t launch_fwd_mfma_mx(const void *Xc, const void *Xs, const void *Wc, co
 
 hipError_t launch_bwd_mfma(int fmt, int w_dt, const void *dY, const void *X, int64_t M, int64_t N, int64_t K,
                            int64_t chunk, int64_t splits, const void *W, const float *s_fp, const float *c, int sb,
-                           const float *alpha, int ste_clip, float *part_s, float *part_c, uint32_t *flag,
-                           hipStream_t st) {
+                           const float *alpha, int ste_clip, int e8m0_floor, float *part_s, float *part_c,
+                           uint32_t *flag, hipStream_t st) {
     const int tiles_k = (int)((K + kTile - 1) / kTile), tiles_n = (int)((N + kTile - 1) / kTile);
     int sbl = 0;
     while ((1 << sbl) < sb) sbl++;
     const dim3 grid((unsigned)tiles_k * tiles_n, (unsigned)splits);
     const uint16_t *dy = static_cast<const uint16_t *>(dY), *x = static_cast<const uint16_t *>(X);
-#define BM(F, WD) bwd_mfma_kernel<F, WD><<<grid, kThreads, 0, st>>>(dy, x, M, N, K, chunk, W, s_fp, c, sbl, alpha, ste_clip, part_s, part_c, flag, tiles_n)
+#define BM(F, WD) bwd_mfma_kernel<F, WD><<<grid, kThreads, 0, st>>>(dy, x, M, N, K, chunk, W, s_fp, c, sbl, alpha, ste_clip, e8m0_floor, part_s, part_c, flag, tiles_n)
     if (fmt == kFmtMX) { if (w_dt == kBF16) BM(kFmtMX, kBF16); else BM(kFmtMX, kF32); }
     else { if (w_dt == kBF16) BM(kFmtNV, kBF16); else BM(kFmtNV, kF32); }
 #undef BM

@@ -13,16 +13,17 @@ constexpr int kAbsmaxParts = 1024;    // partial maxima of the tensor-absmax pas
 constexpr size_t kWsHeader = 256;     // workspace bytes reserved for the domain flag
 
 hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64_t rows, int64_t K,
-                            const float *s_fp, const float *c, int sb, const float *alpha, void *w_hat,
-                            uint8_t *codes, uint8_t *scale_bytes, int block_major, uint32_t *flag, hipStream_t st);
+                            const float *s_fp, const float *c, int sb, const float *alpha, int e8m0_floor,
+                            void *w_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, uint32_t *flag,
+                            hipStream_t st);
 hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t rows, int64_t K,
-                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, float *alpha_out,
-                         float *partial, uint32_t *flag, hipStream_t st);
+                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, int e8m0_floor,
+                         float *alpha_out, float *partial, uint32_t *flag, hipStream_t st);
 hipError_t launch_scales_init(int fmt, int in_dt, const void *W, int64_t rows, int64_t K, float *s_fp,
-                              float *c, int sb, float *alpha_out, float *partial, hipStream_t st);
+                              float *c, int sb, int e8m0_floor, float *alpha_out, float *partial, hipStream_t st);
 hipError_t launch_fq_bwd(int fmt, int w_dt, const float *G, int64_t rows, int64_t K, const void *W,
                          const float *s_fp, const float *c, int sb, const float *alpha, int ste_clip,
-                         float *grad_s, float *grad_c, uint32_t *flag, hipStream_t st);
+                         int e8m0_floor, float *grad_s, float *grad_c, uint32_t *flag, hipStream_t st);
 
 // ---- reconstruction GEMMs ----------------------------------------------------------------------
 // Geometry of a forward launch: output tiles of tm x tn; column partial sums [mtiles][N] (double).
@@ -53,7 +54,7 @@ hipError_t launch_fwd_finish(int64_t mtiles, int64_t M, int64_t N, const double 
 hipError_t launch_recon_fwd_mx(const void *Xc, const void *Xs, const void *Wc, const void *Ws, int64_t M, int64_t N,
                                int64_t K, const void *Yref, void *dY, double *loss_out, double *col_sq_opt, void *ws,
                                hipStream_t st);
-hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int ste_clip, const void *dY,
+hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int ste_clip, int e8m0_floor, const void *dY,
                             const void *X, int64_t M, int64_t N, int64_t K, const void *W, int w_dt,
                             const float *s_fp, const float *c, const float *alpha, float *grad_s,
                             float *grad_c, float *G_out, void *ws, uint32_t *flag, hipStream_t st);

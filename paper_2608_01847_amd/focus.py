@@ -27,7 +27,7 @@ EXPORTED = ("focus_workspace_size", "focus_scales_init", "focus_fakequant_fwd", 
 
 class QConfig(ctypes.Structure):
     _fields_ = [("format", ctypes.c_int32), ("sub_block", ctypes.c_int32),
-                ("ste_clip", ctypes.c_int32), ("scale_layout", ctypes.c_int32)]
+                ("ste_clip", ctypes.c_int32), ("scale_layout", ctypes.c_int32), ("e8m0_rounding", ctypes.c_int32)]
 
 
 class AdamWConfig(ctypes.Structure):
@@ -79,10 +79,12 @@ def status_string(status: int) -> str:
 
 
 SCALES_ROW_MAJOR, SCALES_BLOCK_MAJOR = 0, 1
+E8M0_CEIL, E8M0_FLOOR = 0, 1
 
 
-def qconfig(fmt: int, sub_block: int, ste_clip: int = 1, scale_layout: int = SCALES_ROW_MAJOR) -> QConfig:
-    return QConfig(fmt, sub_block, ste_clip, scale_layout)
+def qconfig(fmt: int, sub_block: int, ste_clip: int = 1, scale_layout: int = SCALES_ROW_MAJOR,
+            e8m0_rounding: int = 0) -> QConfig:
+    return QConfig(fmt, sub_block, ste_clip, scale_layout, e8m0_rounding)
 
 
 def block_size(fmt: int) -> int:
@@ -132,10 +134,10 @@ def _ws(ws: torch.Tensor | None, call: int, q: QConfig, M: int, N: int, K: int, 
     return ws
 
 
-def scales_init(W: torch.Tensor, fmt: int, sub_block: int, ws=None, out=None):
+def scales_init(W: torch.Tensor, fmt: int, sub_block: int, ws=None, out=None, e8m0_rounding: int = 0):
     """Absmax initialisation -> (s_fp [N][K/B], c [N][K/sb] = 1, alpha [1])."""
     N, K = W.shape
-    q = qconfig(fmt, sub_block)
+    q = qconfig(fmt, sub_block, 1, SCALES_ROW_MAJOR, e8m0_rounding)
     if out is None:
         s_fp = torch.empty(N, K // block_size(fmt), dtype=torch.float32, device=W.device)
         c = torch.empty(N, K // sub_block, dtype=torch.float32, device=W.device)
@@ -151,14 +153,14 @@ def scales_init(W: torch.Tensor, fmt: int, sub_block: int, ws=None, out=None):
 def fakequant_fwd(X: torch.Tensor, fmt: int, sub_block: int = 8, s_fp=None, c=None, alpha=None,
                   out_dtype=None, want_codes: bool = False, want_scale_bytes: bool = False,
                   want_alpha: bool = False, ste_clip: int = 1, ws=None, out=None, codes_out=None,
-                  scales_out=None, scale_layout: int = SCALES_ROW_MAJOR):
+                  scales_out=None, scale_layout: int = SCALES_ROW_MAJOR, e8m0_rounding: int = 0):
     """Fake quantisation forward. Weight mode when s_fp is given, dynamic activation mode otherwise.
     codes_out / scales_out: preallocated code and scale-byte outputs (they imply want_codes /
     want_scale_bytes). scale_layout: [rows][K/B] (row-major) or [K/B][rows] (block-major).
 
     Returns (x_hat, packed_codes or None, scale_bytes or None, alpha_x or None)."""
     rows, K = X.shape
-    q = qconfig(fmt, sub_block, ste_clip, scale_layout)
+    q = qconfig(fmt, sub_block, ste_clip, scale_layout, e8m0_rounding)
     out_dtype = out_dtype or X.dtype
     x_hat = out if out is not None else torch.empty(rows, K, dtype=out_dtype, device=X.device)
     codes = codes_out
@@ -177,10 +179,10 @@ def fakequant_fwd(X: torch.Tensor, fmt: int, sub_block: int = 8, s_fp=None, c=No
 
 
 def fakequant_bwd(G: torch.Tensor, W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha=None,
-                  ste_clip: int = 1, ws=None):
+                  ste_clip: int = 1, ws=None, e8m0_rounding: int = 0):
     """Straight-through backward from G = dL/dW_hat (fp32) -> (grad_s, grad_c)."""
     N, K = W.shape
-    q = qconfig(fmt, sub_block, ste_clip)
+    q = qconfig(fmt, sub_block, ste_clip, SCALES_ROW_MAJOR, e8m0_rounding)
     grad_s = torch.empty(N, K // block_size(fmt), dtype=torch.float32, device=W.device)
     grad_c = torch.empty(N, K // sub_block, dtype=torch.float32, device=W.device)
     ws = _ws(ws, CALL_FAKEQUANT_BWD, q, 0, N, K, W.device)
@@ -229,11 +231,12 @@ def recon_gemm_fwd_mxfp4(X_codes: torch.Tensor, X_scales: torch.Tensor, W_codes:
 
 
 def recon_gemm_bwd(dY: torch.Tensor, X_hat: torch.Tensor, W: torch.Tensor, fmt: int, sub_block: int, s_fp,
-                   c=None, alpha=None, ste_clip: int = 1, want_G: bool = False, ws=None, out=None):
+                   c=None, alpha=None, ste_clip: int = 1, want_G: bool = False, ws=None, out=None,
+                   e8m0_rounding: int = 0):
     """Fused backward -> (grad_s, grad_c, G or None)."""
     M, K = X_hat.shape
     N = W.shape[0]
-    q = qconfig(fmt, sub_block, ste_clip)
+    q = qconfig(fmt, sub_block, ste_clip, SCALES_ROW_MAJOR, e8m0_rounding)
     if out is None:
         grad_s = torch.empty(N, K // block_size(fmt), dtype=torch.float32, device=W.device)
         grad_c = torch.empty(N, K // sub_block, dtype=torch.float32, device=W.device)
@@ -248,10 +251,10 @@ def recon_gemm_bwd(dY: torch.Tensor, X_hat: torch.Tensor, W: torch.Tensor, fmt: 
 
 
 def export_packed(W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha=None, ws=None, out=None,
-                  scale_layout: int = SCALES_ROW_MAJOR):
+                  scale_layout: int = SCALES_ROW_MAJOR, e8m0_rounding: int = 0):
     """Deployable export -> (packed codes [N][K/2], scale bytes [N][K/B] or, block-major, [K/B][N])."""
     N, K = W.shape
-    q = qconfig(fmt, sub_block, 1, scale_layout)
+    q = qconfig(fmt, sub_block, 1, scale_layout, e8m0_rounding)
     if out is None:
         packed = torch.empty(N, K // 2, dtype=torch.uint8, device=W.device)
         shape = (N, K // block_size(fmt)) if scale_layout == SCALES_ROW_MAJOR else (K // block_size(fmt), N)

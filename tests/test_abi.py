@@ -78,6 +78,8 @@ def test_argument_checks(L, cpu_only):
     assert fq_fwd(L, focus.qconfig(focus.NVFP4, 32)) == focus.ERR_CONFIG  # sub-block larger than the block
     assert fq_fwd(L, focus.qconfig(focus.MXFP4, 8, 2)) == focus.ERR_CONFIG
     assert fq_fwd(L, focus.QConfig(0, 8, 1, 5)) == focus.ERR_CONFIG  # no such scale layout
+    assert fq_fwd(L, focus.QConfig(0, 8, 1, 0, 2)) == focus.ERR_CONFIG  # no such E8M0 rounding
+    assert fq_fwd(L, focus.QConfig(1, 8, 1, 0, 1), K=64) == focus.ERR_CONFIG  # floor E8M0 is MXFP4 only
     assert fq_fwd(L, mx, X=None) == focus.ERR_NULL
     assert fq_fwd(L, mx, x_dt=7) == focus.ERR_DTYPE
     assert fq_fwd(L, mx, K=48) == focus.ERR_SHAPE          # not a multiple of 32
