@@ -92,7 +92,10 @@ typedef enum {
     FOCUS_CALL_RECON_GEMM_FWD = 3,
     FOCUS_CALL_RECON_GEMM_BWD = 4,
     FOCUS_CALL_EXPORT_PACKED = 5,
-    FOCUS_CALL_ADAMW = 6
+    FOCUS_CALL_ADAMW = 6,
+    FOCUS_CALL_RECON_GEMM_DX = 7,
+    FOCUS_CALL_FAKEQUANT_ACT_BWD = 8,
+    FOCUS_CALL_KL_TOP = 9
 } focus_call;
 
 /* Workspace bytes a call needs for the given sizes (M = tokens, N = rows / out features,
@@ -188,6 +191,42 @@ focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dt
                                  uint8_t *packed, uint8_t *scale_bytes,
                                  void *ws, size_t ws_bytes, focus_stream stream);
 
+/* Input gradient of a linear layer for end-to-end chaining (Sec. 3.2: the whole quantised model is
+ * trained end to end, so the gradient reaching a layer's output flows on to its input):
+ *   dX_hat [M][K] = dY [M][N] * W_hat [N][K]        (op_dtype operands, fp32 accumulation)
+ * dY is the gradient of the layer output (e.g. from focus_kl_top or from the next layer), W_hat the
+ * fake-quantised weight of the forward. The result is the gradient of the fake-quantised input;
+ * focus_fakequant_act_bwd carries it through the activation quantisation. N % 16 == 0 (N == 0
+ * writes zeros; dY and W_hat may then be NULL); all pointers 16-byte aligned; ws: focus_workspace_size(FOCUS_CALL_RECON_GEMM_DX, NULL, M, N, K)
+ * bytes (it holds the transposed W_hat). bf16 runs on the MFMA path where the shapes allow it. */
+focus_status focus_recon_gemm_dx(const void *dY, const void *W_hat, int op_dtype, int64_t M, int64_t N, int64_t K,
+                                 void *dX_hat, void *ws, size_t ws_bytes, focus_stream stream);
+
+/* Straight-through backward of the dynamic activation fake quantisation (Sec. 3.2: STE on every
+ * non-differentiable operation): dX = m * dX_hat with m = [|x / S| <= 6] (q->ste_clip = 1; m = 1 when
+ * 0), the block scale S recomputed from X exactly as focus_fakequant_fwd forms it (format and
+ * E8M0 rounding from q); a block whose scale is zero passes no gradient. The absmax scales pass no
+ * gradient (a masked element is written as +0). X [rows][K] (x_dtype), dX_hat and dX [rows][K]
+ * (g_dtype; dX may alias dX_hat). Under the
+ * default rounded-up E8M0 every MXFP4 mask is 1. ws: focus_workspace_size(
+ * FOCUS_CALL_FAKEQUANT_ACT_BWD, q, 0, rows, K) bytes (NVFP4 recomputes the tensor scale). */
+focus_status focus_fakequant_act_bwd(const focus_qconfig *q, const void *X, int x_dtype, int64_t rows, int64_t K,
+                                     const void *dX_hat, int g_dtype, void *dX, void *ws, size_t ws_bytes,
+                                     focus_stream stream);
+
+/* KL-Top objective on logits (Sec. 4.1: the end-to-end training loss, k = 1000). For each of the T
+ * token rows of the teacher logits Z_teacher [T][V] (the full-precision model) and the student
+ * logits Z_student [T][V] (the quantised model), with I the indices of the teacher's k largest
+ * logits (ties at the k-th value taken in increasing index order; every index when k >= V):
+ *   p_t = softmax(Z_teacher[row, I]),  p_s = softmax(Z_student[row, I])
+ *   loss = (1/T) sum_rows sum_{i in I} p_t[i] (log p_t[i] - log p_s[i])      -> *loss_out (device fp64)
+ *   dZ_student[row, i] = (p_s[i] - p_t[i]) / T for i in I, 0 elsewhere       (dtype, written in full)
+ * dtype FOCUS_BF16 or FOCUS_F32 for all three arrays (element-aligned). k >= 1, 1 <= V <= 2^31.
+ * The logits must be finite: a NaN or infinity raises the domain flag (results unspecified). ws:
+ * focus_workspace_size(FOCUS_CALL_KL_TOP, NULL, T, V, 0) bytes. Deterministic (fixed-order sums). */
+focus_status focus_kl_top(const void *Z_student, const void *Z_teacher, int dtype, int64_t T, int64_t V, int32_t k,
+                          void *dZ_student, double *loss_out, void *ws, size_t ws_bytes, focus_stream stream);
+
 /* AdamW hyper-parameters (Sec. 4.1: AdamW with a constant learning rate; MXFP4 uses 2e-2 for the
  * block scales and 5e-2 for the coefficients c, NVFP4 5e-3 and 1e-3).
  *   lr           : learning rate, >= 0.
@@ -223,8 +262,8 @@ focus_status focus_adamw_step(const focus_adamw_config *cfg, int64_t t, int64_t 
 
 /* Synchronises `stream`, reads and clears the workspace's sticky domain flag. Returns
  * FOCUS_ERR_DOMAIN if any call on this workspace met a NaN scale or a coefficient c that is
- * <= 0 or not finite, or a log2-domain AdamW step met a parameter that is not positive and
- * finite, since the last check (outputs of such blocks are unspecified), FOCUS_OK
+ * <= 0 or not finite, a log2-domain AdamW step met a parameter that is not positive and
+ * finite, or focus_kl_top met a logit that is not finite, since the last check (outputs of such blocks are unspecified), FOCUS_OK
  * otherwise, FOCUS_ERR_HIP on a runtime error. */
 focus_status focus_check_flags(void *ws, focus_stream stream);
 

@@ -56,6 +56,14 @@ float *partials_of(void *ws) { return reinterpret_cast<float *>(reinterpret_cast
 
 focus_status hip_status(hipError_t e) { return e == hipSuccess ? FOCUS_OK : FOCUS_ERR_HIP; }
 
+size_t round256(size_t b) { return (b + 255) / 256 * 256; }
+
+// dX_hat workspace: header, the transposed W_hat [K][N] (fp32 size, the larger), then the forward's own
+size_t dx_ws(int64_t M, int64_t N, int64_t K) {
+    return kWsHeader + round256((size_t)N * (size_t)K * sizeof(float)) +
+           std::max(plan_fwd(kF32, M, K, N).ws_bytes, plan_fwd(kBF16, M, K, N).ws_bytes);
+}
+
 size_t fwd_ws(int64_t M, int64_t N, int64_t K) {
     return std::max(plan_fwd(kF32, M, N, K).ws_bytes, plan_fwd(kBF16, M, N, K).ws_bytes);
 }
@@ -79,11 +87,20 @@ extern "C" {
 
 size_t focus_workspace_size(int call, const focus_qconfig *q, int64_t M, int64_t N, int64_t K) {
     if (call == FOCUS_CALL_ADAMW) return kWsHeader;  // the domain flag only; q may be NULL
+    if (call == FOCUS_CALL_RECON_GEMM_DX) {            // q may be NULL
+        if (M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return 0;
+        return dx_ws(M, N, K);
+    }
+    if (call == FOCUS_CALL_KL_TOP) {  // M = tokens; q may be NULL
+        if (M < 0 || M > kMaxDim) return 0;
+        return kWsHeader + round256((size_t)M * sizeof(double)) + sizeof(double);
+    }
     if (check_q(q) != FOCUS_OK) return 0;
     const int B = block_of(q->format);
     switch (call) {
         case FOCUS_CALL_SCALES_INIT:
         case FOCUS_CALL_FAKEQUANT_FWD:
+        case FOCUS_CALL_FAKEQUANT_ACT_BWD:
             return kWsHeader + (kAbsmaxParts + 64) * sizeof(float);  // partial maxima + tensor scale slot
         case FOCUS_CALL_FAKEQUANT_BWD:
         case FOCUS_CALL_EXPORT_PACKED:
@@ -223,6 +240,62 @@ focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dt
     if (N == 0 || K == 0) return FOCUS_OK;
     return hip_status(launch_fq_weight(q->format, w_dtype, w_dtype, W, N, K, s_fp, c, q->sub_block, alpha,
                                        floor_of(q), nullptr, packed, scale_bytes, q->scale_layout, flag_of(ws), (hipStream_t)stream));
+}
+
+focus_status focus_recon_gemm_dx(const void *dY, const void *W_hat, int op_dtype, int64_t M, int64_t N, int64_t K,
+                                 void *dX_hat, void *ws, size_t ws_bytes, focus_stream stream) {
+    if (!dX_hat || (N > 0 && (!dY || !W_hat))) return FOCUS_ERR_NULL;  // empty operands may be NULL
+    if (!dtype_ok(op_dtype)) return FOCUS_ERR_DTYPE;
+    if (M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return FOCUS_ERR_SHAPE;
+    if (N % 16 != 0) return FOCUS_ERR_SHAPE;  // the contraction runs over N
+    if ((M > 0 && K > kMaxElems / M) || (N > 0 && K > kMaxElems / N) || (M > 0 && N > kMaxElems / M))
+        return FOCUS_ERR_SHAPE;
+    if (!all_aligned({dY, W_hat, dX_hat})) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, dx_ws(M, N, K)));
+    if (M == 0 || K == 0) return FOCUS_OK;
+    const hipStream_t st = (hipStream_t)stream;
+    char *wt = static_cast<char *>(ws) + kWsHeader;
+    char *ws_fwd = wt + round256((size_t)N * (size_t)K * sizeof(float));
+    if (N == 0) {  // an empty sum: dX_hat = 0
+        const size_t esz = op_dtype == FOCUS_BF16 ? 2 : 4;
+        return hip_status(launch_zero_fill(dX_hat, (size_t)M * (size_t)K * esz, st));
+    }
+    hipError_t e = launch_transpose(op_dtype, W_hat, N, K, wt, st);
+    if (e != hipSuccess) return hip_status(e);
+    // dX_hat [M][K] = dY [M][N] (W_hat^T [K][N])^T: the forward GEMM's plain product with N as the
+    // contraction
+    const FwdPlan p = plan_fwd(op_dtype, M, K, N);
+    return hip_status(launch_recon_fwd(p, op_dtype, dY, wt, M, K, N, nullptr, dX_hat, nullptr, nullptr, ws_fwd, st));
+}
+
+focus_status focus_fakequant_act_bwd(const focus_qconfig *q, const void *X, int x_dtype, int64_t rows, int64_t K,
+                                     const void *dX_hat, int g_dtype, void *dX, void *ws, size_t ws_bytes,
+                                     focus_stream stream) {
+    FOCUS_TRY(check_q(q));
+    if (!X || !dX_hat || !dX) return FOCUS_ERR_NULL;
+    if (!dtype_ok(x_dtype) || !dtype_ok(g_dtype)) return FOCUS_ERR_DTYPE;
+    FOCUS_TRY(check_rows_k(rows, K, block_of(q->format)));
+    if (!all_aligned({X, dX_hat, dX})) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_FAKEQUANT_ACT_BWD, q, 0, rows, K)));
+    if (rows == 0 || K == 0) return FOCUS_OK;
+    return hip_status(launch_fq_act_bwd(q->format, x_dtype, g_dtype, X, rows, K, floor_of(q), q->ste_clip, dX_hat, dX,
+                                        partials_of(ws), (hipStream_t)stream));
+}
+
+focus_status focus_kl_top(const void *Z_student, const void *Z_teacher, int dtype, int64_t T, int64_t V, int32_t k,
+                          void *dZ_student, double *loss_out, void *ws, size_t ws_bytes, focus_stream stream) {
+    if (!Z_student || !Z_teacher || !dZ_student || !loss_out) return FOCUS_ERR_NULL;
+    if (!dtype_ok(dtype)) return FOCUS_ERR_DTYPE;
+    if (k < 1) return FOCUS_ERR_CONFIG;
+    if (T < 1 || V < 1 || T > kMaxDim || V > (int64_t(1) << 31) || V > kMaxElems / T) return FOCUS_ERR_SHAPE;
+    const size_t esz = dtype == FOCUS_BF16 ? 2 : 4;
+    if ((reinterpret_cast<uintptr_t>(Z_student) | reinterpret_cast<uintptr_t>(Z_teacher) |
+         reinterpret_cast<uintptr_t>(dZ_student)) % esz)
+        return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_KL_TOP, nullptr, T, V, 0)));
+    double *row_loss = reinterpret_cast<double *>(static_cast<char *>(ws) + kWsHeader);
+    return hip_status(launch_kl_top(dtype, Z_student, Z_teacher, T, V, k, dZ_student, row_loss, loss_out, flag_of(ws),
+                                    (hipStream_t)stream));
 }
 
 focus_status focus_adamw_step(const focus_adamw_config *cfg, int64_t t, int64_t n, float *param, const float *grad,

@@ -1,0 +1,277 @@
+// End-to-end chaining of the scale-learning step: the transposed weight operand of dX_hat = dY W_hat
+// and the KL-Top objective on logits (Sec. 4.1: the paper trains end to end with the KL-Top loss,
+// k = 1000, following the method it cites for that loss).
+#include <cmath>
+
+#include "focus_device.h"
+#include "internal.h"
+
+namespace focus {
+
+namespace {
+
+// ------------------------------------------------------------------------------------------------
+// out[c][r] = in[r][c] for an R x C matrix, 64 x 64 tiles staged through LDS (rows of 64 elements
+// read and written contiguously; the padded column breaks bank conflicts of the transposed reads).
+template <typename T>
+__global__ void __launch_bounds__(256) transpose_kernel(const T *__restrict__ in, int64_t R, int64_t C,
+                                                         T *__restrict__ out) {
+    __shared__ T tile[64][65];
+    const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int i = ty; i < 64; i += 4) {
+        const int64_t r = r0 + i, c = c0 + tx;
+        if (r < R && c < C) tile[i][tx] = in[r * C + c];
+    }
+    __syncthreads();
+    for (int i = ty; i < 64; i += 4) {
+        const int64_t c = c0 + i, r = r0 + tx;
+        if (c < C && r < R) out[c * R + r] = tile[tx][i];
+    }
+}
+
+// ------------------------------------------------------------------------------------------------
+// KL-Top. Keys order fp32 values as unsigned integers (negative values flipped, positive ones with
+// the sign bit set); -0 is taken as +0 so that equal values have equal keys.
+__device__ __forceinline__ uint32_t order_key(float f) {
+    uint32_t b = __float_as_uint(f);
+    b = b == 0x80000000u ? 0u : b;
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+template <int IN>
+__device__ __forceinline__ float load_logit(const void *p, int64_t i) {
+    if (IN == kBF16) return bf16_bits_to_f32(reinterpret_cast<const uint16_t *>(p)[i]);
+    return reinterpret_cast<const float *>(p)[i];
+}
+
+// the key of logit i; for bf16 logits only the high 16 bits carry information (the low half of a
+// flipped negative value would be all ones), so they alone are kept
+template <int IN>
+__device__ __forceinline__ uint32_t logit_key(float v) {
+    const uint32_t k = order_key(v);
+    return IN == kBF16 ? (k & 0xFFFF0000u) : k;
+}
+
+template <int IN>
+__device__ __forceinline__ void store_logit(void *p, int64_t i, float v) {
+    if (IN == kBF16) reinterpret_cast<uint16_t *>(p)[i] = (uint16_t)f32_to_bf16_bits(v);
+    else reinterpret_cast<float *>(p)[i] = v;
+}
+
+// inclusive scan of one value per thread over the workgroup (256 threads), in thread order
+__device__ __forceinline__ uint32_t block_scan(uint32_t v, uint32_t *buf) {
+    const int t = threadIdx.x;
+    buf[t] = v;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+        const uint32_t add = t >= off ? buf[t - off] : 0u;
+        __syncthreads();
+        buf[t] += add;
+        __syncthreads();
+    }
+    const uint32_t r = buf[t];
+    __syncthreads();
+    return r;
+}
+
+// One workgroup per token row. Passes over the row (L2-resident between passes):
+//   radix select of the k-th largest teacher key (8-bit digits from the top, LDS histograms);
+//   if fewer ties at that key are admitted than exist, the index of the last admitted tie (ties are
+//   taken in index order, 256 elements per trip, ballots for the in-trip ranks);
+//   online softmax statistics of both rows over the selected set (per thread, then a fixed tree);
+//   KL terms and dZ_s (zero outside the set).
+template <int IN>
+__global__ void __launch_bounds__(256)
+kl_top_kernel(const void *__restrict__ Zs, const void *__restrict__ Zt, int64_t V, int k, double inv_T,
+              void *__restrict__ dZs, double *__restrict__ row_loss, uint32_t *flag) {
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t scan_buf[256];
+    __shared__ uint32_t sel_digit, sel_above;
+    __shared__ uint32_t wave_cnt[4];
+    __shared__ float red_m[2][256];
+    __shared__ double red_s[2][256];
+    __shared__ double red_d[256];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int64_t row = blockIdx.x;
+    const char *zs = reinterpret_cast<const char *>(Zs) + row * V * (IN == kBF16 ? 2 : 4);
+    const char *zt = reinterpret_cast<const char *>(Zt) + row * V * (IN == kBF16 ? 2 : 4);
+    char *dz = reinterpret_cast<char *>(dZs) + row * V * (IN == kBF16 ? 2 : 4);
+
+    // ---- threshold key: the k-th largest teacher key ----
+    uint32_t prefix = 0u, pmask = 0u, remaining = (uint32_t)k;
+    const bool all = (int64_t)k >= V;
+    bool bad = false;
+    if (!all) {
+        constexpr int kPasses = IN == kBF16 ? 2 : 4;  // bf16 keys have zero low 16 bits
+        for (int p = 0; p < kPasses; p++) {
+            const int shift = 24 - 8 * p;
+            hist[t] = 0u;
+            __syncthreads();
+            for (int64_t i = t; i < V; i += 256) {
+                const uint32_t key = logit_key<IN>(load_logit<IN>(zt, i));
+                if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+            }
+            __syncthreads();
+            // bins in descending digit order: thread j holds digit 255 - j
+            const uint32_t h = hist[255 - t];
+            const uint32_t incl = block_scan(h, scan_buf);
+            if (incl - h < remaining && remaining <= incl) {
+                sel_digit = 255u - (uint32_t)t;
+                sel_above = incl - h;
+            }
+            __syncthreads();
+            remaining -= sel_above;
+            prefix |= sel_digit << shift;
+            pmask |= 0xFFu << shift;
+            __syncthreads();
+        }
+    }
+    const uint32_t thr = prefix;  // with `all`, every element is selected
+    // ---- ties at the threshold: admit the first `remaining` in index order ----
+    int64_t cut = V;  // selected ties are those with index < cut
+    if (!all) {
+        uint32_t seen = 0u;
+        for (int64_t base = 0; base < V; base += 256) {
+            const int64_t i = base + t;
+            const bool tie = i < V && logit_key<IN>(load_logit<IN>(zt, i)) == thr;
+            const uint64_t m = __ballot(tie);
+            if (lane == 0) wave_cnt[wave] = (uint32_t)__popcll(m);
+            __syncthreads();
+            uint32_t before = seen;
+            for (int w = 0; w < wave; w++) before += wave_cnt[w];
+            const uint32_t total = wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
+            const uint32_t rank = before + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+            __syncthreads();
+            if (seen + total >= remaining) {
+                // the remaining-th tie is in this trip: its index + 1 is the cut
+                if (tie && rank + 1u == remaining) red_d[0] = (double)(i + 1);
+                __syncthreads();
+                cut = (int64_t)red_d[0];
+                break;
+            }
+            seen += total;
+        }
+    }
+    auto selected = [&](int64_t i, uint32_t key) { return all || key > thr || (key == thr && i < cut); };
+
+    // ---- softmax statistics over the selected set (online per thread) ----
+    float mt = -INFINITY, ms = -INFINITY;
+    double st = 0.0, ss = 0.0;  // sums of exp(z - max) in double: the loss needs their logs to ~1e-12
+    for (int64_t i = t; i < V; i += 256) {
+        const float a = load_logit<IN>(zt, i), b = load_logit<IN>(zs, i);
+        bad = bad || !(__builtin_fabsf(a) < INFINITY) || !(__builtin_fabsf(b) < INFINITY);
+        if (!selected(i, logit_key<IN>(a))) continue;
+        if (a > mt) {
+            st = st * exp((double)mt - (double)a) + 1.0;
+            mt = a;
+        } else {
+            st += exp((double)a - (double)mt);
+        }
+        if (b > ms) {
+            ss = ss * exp((double)ms - (double)b) + 1.0;
+            ms = b;
+        } else {
+            ss += exp((double)b - (double)ms);
+        }
+    }
+    red_m[0][t] = mt, red_s[0][t] = st, red_m[1][t] = ms, red_s[1][t] = ss;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if (t < off) {
+            for (int q = 0; q < 2; q++) {
+                const float m1 = red_m[q][t], m2 = red_m[q][t + off];
+                const double s1 = red_s[q][t], s2 = red_s[q][t + off];
+                const float m = fmaxf(m1, m2);
+                const double s = (m1 == -INFINITY ? 0.0 : s1 * exp((double)m1 - (double)m)) +
+                                 (m2 == -INFINITY ? 0.0 : s2 * exp((double)m2 - (double)m));
+                red_m[q][t] = m;
+                red_s[q][t] = s;
+            }
+        }
+        __syncthreads();
+    }
+    // log-sum-exp of each row over the set, and their difference, in double
+    const double lt_d = (double)red_m[0][0] + log(red_s[0][0]), ls_d = (double)red_m[1][0] + log(red_s[1][0]);
+    const double dl = lt_d - ls_d;
+    __syncthreads();
+
+    // ---- KL(p_t || p_s) over the set and dZ_s = (p_s - p_t) / T ----
+    double kl = 0.0;
+    for (int64_t i = t; i < V; i += 256) {
+        const float a = load_logit<IN>(zt, i), b = load_logit<IN>(zs, i);
+        float g = 0.0f;
+        if (selected(i, logit_key<IN>(a))) {
+            // d = log p_s - log p_t; p_s - p_t = p_t expm1(d) keeps its relative accuracy where the
+            // two probabilities nearly cancel
+            const double pt = exp((double)a - lt_d);
+            const double d = ((double)b - (double)a) + dl;
+            kl -= pt * d;
+            g = (float)(pt * expm1(d) * inv_T);
+        }
+        store_logit<IN>(dz, i, g);
+    }
+    red_d[t] = kl;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if (t < off) red_d[t] += red_d[t + off];
+        __syncthreads();
+    }
+    if (t == 0) row_loss[row] = red_d[0];
+    if (bad && t == 0) raise_domain_flag(flag);
+}
+
+// loss = (sum of row losses) / T, in a fixed order
+__global__ void __launch_bounds__(256) row_mean_kernel(const double *__restrict__ row_loss, int64_t T,
+                                                        double *__restrict__ loss) {
+    __shared__ double red[256];
+    double acc = 0.0;
+    for (int64_t i = threadIdx.x; i < T; i += 256) acc += row_loss[i];
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *loss = red[0] / (double)T;
+}
+
+// zero fill of a 16-byte-aligned buffer (whole 16-byte words, then the tail bytes)
+__global__ void __launch_bounds__(256) zero_fill_kernel(char *__restrict__ p, size_t bytes) {
+    const size_t words = bytes / 16;
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < words; i += (size_t)gridDim.x * 256)
+        reinterpret_cast<uint4 *>(p)[i] = make_uint4(0u, 0u, 0u, 0u);
+    if (blockIdx.x == 0 && threadIdx.x < bytes % 16) p[words * 16 + threadIdx.x] = 0;
+}
+
+}  // namespace
+
+hipError_t launch_zero_fill(void *p, size_t bytes, hipStream_t st) {
+    const size_t words = bytes / 16;
+    const unsigned grid = (unsigned)std::max<size_t>(1, std::min<size_t>((words + 255) / 256, kStreamGridCap));
+    zero_fill_kernel<<<grid, 256, 0, st>>>(static_cast<char *>(p), bytes);
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose(int dt, const void *in, int64_t R, int64_t C, void *out, hipStream_t st) {
+    const dim3 grid((unsigned)((C + 63) / 64), (unsigned)((R + 63) / 64));
+    if (dt == kBF16)
+        transpose_kernel<uint16_t><<<grid, 256, 0, st>>>(static_cast<const uint16_t *>(in), R, C,
+                                                         static_cast<uint16_t *>(out));
+    else
+        transpose_kernel<float><<<grid, 256, 0, st>>>(static_cast<const float *>(in), R, C, static_cast<float *>(out));
+    return hipGetLastError();
+}
+
+hipError_t launch_kl_top(int dt, const void *Zs, const void *Zt, int64_t T, int64_t V, int k, void *dZs,
+                         double *row_loss, double *loss, uint32_t *flag, hipStream_t st) {
+    const double inv_T = 1.0 / (double)T;
+    if (dt == kBF16) kl_top_kernel<kBF16><<<(unsigned)T, 256, 0, st>>>(Zs, Zt, V, k, inv_T, dZs, row_loss, flag);
+    else kl_top_kernel<kF32><<<(unsigned)T, 256, 0, st>>>(Zs, Zt, V, k, inv_T, dZs, row_loss, flag);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    row_mean_kernel<<<1, 256, 0, st>>>(row_loss, T, loss);
+    return hipGetLastError();
+}
+
+}  // namespace focus

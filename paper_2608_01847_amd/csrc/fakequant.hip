@@ -219,6 +219,44 @@ fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
 }
 
 // ------------------------------------------------------------------------------------------------
+// Straight-through backward of the dynamic activation fake quantisation (Sec. 3.2: STE on every
+// non-differentiable operation): dX = m * dX_hat, m the clamp mask [|x / S| <= 6] (1 everywhere when
+// ste_clip is 0; 0 in a block whose scale is zero), with the block scale S recomputed exactly as the
+// forward forms it. The absmax scale passes no gradient. Under the paper's rounded-up E8M0, |x| <=
+// amax <= 6 S, so every MXFP4 mask is 1; the OCP floor rule and NVFP4's rounded E4M3 scale can clip.
+template <int FMT, int IN, int GD>
+__global__ void __launch_bounds__(256)
+fq_act_bwd_kernel(const void *__restrict__ X, uint32_t nchunks, int64_t row0, int64_t K,
+                  const float *__restrict__ alpha_slot, int e8m0_floor, int ste_clip,
+                  const void *__restrict__ dX_hat, void *__restrict__ dX) {
+    constexpr int B = block_of(FMT);
+    const float alpha = FMT == kFmtNV ? *alpha_slot : 1.0f;
+    const int64_t e_row0 = row0 * K;
+    for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
+        const int64_t e0 = e_row0 + (int64_t)t * 8;
+        float v[8], g[8];
+        load8(X, IN, e0, v);
+        load8(dX_hat, GD, e0, g);
+        float amax = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; i++) amax = fmaxf(amax, __builtin_fabsf(v[i]));
+        amax = group_max(amax, B / 8);
+        bool nan = false;
+        float S;
+        if (FMT == kFmtMX) {
+            const int e = e8m0_floor ? e8m0_floor_exp(amax, 2, nan) : e8m0_ceil_exp(amax / 6.0f, nan);
+            S = exp2i(e);
+        } else {
+            S = alpha * e4m3_value(e4m3_code(amax / (alpha * 6.0f), nan));
+        }
+        float out[8];
+#pragma unroll
+        for (int i = 0; i < 8; i++) out[i] = quantize_element(v[i], S, S, ste_clip != 0).m ? g[i] : 0.0f;
+        store8(dX, GD, e0, out);
+    }
+}
+
+// ------------------------------------------------------------------------------------------------
 // K8: absmax initialisation (Sec. 3.2). MXFP4: s = fl32(amax / 6) (E8M0 rounded up), or fl32(amax / 4)
 // with the OCP floor rule, whose E8M0 is then floor(log2 amax) - 2. NVFP4: Delta_fp =
 // fl32(amax / fl32(alpha * 6)) with alpha from the partial maxima; c = 1.
@@ -381,6 +419,27 @@ hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t 
         if (in_dt == kBF16) { if (out_dt == kBF16) FQN(kBF16, kBF16); else FQN(kBF16, kF32); }
         else { if (out_dt == kBF16) FQN(kF32, kBF16); else FQN(kF32, kF32); }
 #undef FQN
+    });
+}
+
+hipError_t launch_fq_act_bwd(int fmt, int in_dt, int g_dt, const void *X, int64_t rows, int64_t K, int e8m0_floor,
+                             int ste_clip, const void *dX_hat, void *dX, float *partial, hipStream_t st) {
+    const float *slot = partial + kAbsmaxParts;
+    if (fmt == kFmtNV) {
+        hipError_t e = launch_tensor_alpha(in_dt, X, rows * K, partial, nullptr, st);
+        if (e != hipSuccess) return e;
+    }
+    return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
+        (void)cpr;
+#define AB(F, I, G) fq_act_bwd_kernel<F, I, G><<<grid, 256, 0, st>>>(X, n, r0, K, slot, e8m0_floor, ste_clip, dX_hat, dX)
+        if (fmt == kFmtMX) {
+            if (in_dt == kBF16) { if (g_dt == kBF16) AB(kFmtMX, kBF16, kBF16); else AB(kFmtMX, kBF16, kF32); }
+            else { if (g_dt == kBF16) AB(kFmtMX, kF32, kBF16); else AB(kFmtMX, kF32, kF32); }
+        } else {
+            if (in_dt == kBF16) { if (g_dt == kBF16) AB(kFmtNV, kBF16, kBF16); else AB(kFmtNV, kBF16, kF32); }
+            else { if (g_dt == kBF16) AB(kFmtNV, kF32, kBF16); else AB(kFmtNV, kF32, kF32); }
+        }
+#undef AB
     });
 }
 

@@ -59,6 +59,13 @@ hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int st
                             const float *s_fp, const float *c, const float *alpha, float *grad_s,
                             float *grad_c, float *G_out, void *ws, uint32_t *flag, hipStream_t st);
 
+hipError_t launch_fq_act_bwd(int fmt, int in_dt, int g_dt, const void *X, int64_t rows, int64_t K, int e8m0_floor,
+                             int ste_clip, const void *dX_hat, void *dX, float *partial, hipStream_t st);
+hipError_t launch_zero_fill(void *p, size_t bytes, hipStream_t st);
+hipError_t launch_transpose(int dt, const void *in, int64_t R, int64_t C, void *out, hipStream_t st);
+hipError_t launch_kl_top(int dt, const void *Zs, const void *Zt, int64_t T, int64_t V, int k, void *dZs,
+                         double *row_loss, double *loss, uint32_t *flag, hipStream_t st);
+
 hipError_t launch_adamw(float lr, float beta1, float beta2, float eps, float weight_decay, int log2_domain,
                         int64_t t, int64_t n, float *param, const float *grad, float *exp_avg, float *exp_avg_sq,
                         uint32_t *flag, hipStream_t st);

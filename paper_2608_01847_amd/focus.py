@@ -17,12 +17,14 @@ MXFP4, NVFP4 = 0, 1
 F32, BF16 = 0, 1
 CALL_SCALES_INIT, CALL_FAKEQUANT_FWD, CALL_FAKEQUANT_BWD = 0, 1, 2
 CALL_RECON_GEMM_FWD, CALL_RECON_GEMM_BWD, CALL_EXPORT_PACKED, CALL_ADAMW = 3, 4, 5, 6
+CALL_RECON_GEMM_DX, CALL_FAKEQUANT_ACT_BWD, CALL_KL_TOP = 7, 8, 9
 
 OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_CONFIG, ERR_WORKSPACE, ERR_DOMAIN, ERR_HIP = range(8)
 
 EXPORTED = ("focus_workspace_size", "focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd",
             "focus_recon_gemm_fwd", "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd", "focus_export_packed",
-            "focus_adamw_step", "focus_check_flags", "focus_status_string")
+            "focus_recon_gemm_dx", "focus_fakequant_act_bwd", "focus_kl_top", "focus_adamw_step",
+            "focus_check_flags", "focus_status_string")
 
 
 class QConfig(ctypes.Structure):
@@ -62,13 +64,17 @@ def lib() -> ctypes.CDLL:
         L.focus_recon_gemm_fwd_mxfp4.argtypes = [p, p, p, p, i64, i64, i64, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_bwd.argtypes = [q, p, p, i32, i64, i64, i64, p, i32, p, p, p, p, p, p, p, sz, p]
         L.focus_export_packed.argtypes = [q, p, i32, i64, i64, p, p, p, p, p, p, sz, p]
+        L.focus_recon_gemm_dx.argtypes = [p, p, i32, i64, i64, i64, p, p, sz, p]
+        L.focus_fakequant_act_bwd.argtypes = [q, p, i32, i64, i64, p, i32, p, p, sz, p]
+        L.focus_kl_top.argtypes = [p, p, i32, i64, i64, i32, p, p, p, sz, p]
         L.focus_adamw_step.argtypes = [ctypes.POINTER(AdamWConfig), i64, i64, p, p, p, p, p, sz, p]
         L.focus_check_flags.argtypes = [p, p]
         L.focus_status_string.argtypes = [i32]
         L.focus_status_string.restype = ctypes.c_char_p
         for name in ("focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd", "focus_recon_gemm_fwd",
                      "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd", "focus_export_packed",
-                     "focus_adamw_step", "focus_check_flags"):
+                     "focus_adamw_step", "focus_check_flags", "focus_recon_gemm_dx", "focus_fakequant_act_bwd",
+                     "focus_kl_top"):
             getattr(L, name).restype = ctypes.c_int
         _LIB = L
     return _LIB
@@ -266,6 +272,46 @@ def export_packed(W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha
                                      _ptr(packed), _ptr(sbytes), _ptr(ws), ws.numel(), _stream()),
            "focus_export_packed")
     return packed, sbytes
+
+
+def recon_gemm_dx(dY: torch.Tensor, W_hat: torch.Tensor, ws=None, out=None) -> torch.Tensor:
+    """dX_hat = dY W_hat (the input gradient of a linear) -> [M][K] in dY's dtype."""
+    M, N = dY.shape
+    K = W_hat.shape[1]
+    assert W_hat.shape[0] == N and W_hat.dtype == dY.dtype
+    dX = out if out is not None else torch.empty(M, K, dtype=dY.dtype, device=dY.device)
+    need = workspace_size(CALL_RECON_GEMM_DX, qconfig(MXFP4, 8), M, N, K)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dY.device)
+    _check(lib().focus_recon_gemm_dx(_ptr(dY), _ptr(W_hat), _dt(dY), M, N, K, _ptr(dX), _ptr(ws), ws.numel(),
+                                     _stream()), "focus_recon_gemm_dx")
+    return dX
+
+
+def fakequant_act_bwd(X: torch.Tensor, dX_hat: torch.Tensor, fmt: int, ste_clip: int = 1, e8m0_rounding: int = 0,
+                      ws=None, out=None) -> torch.Tensor:
+    """Straight-through backward of the activation fake quantisation -> dX (dX_hat's dtype)."""
+    rows, K = X.shape
+    q = qconfig(fmt, 8, ste_clip, SCALES_ROW_MAJOR, e8m0_rounding)  # the sub-block plays no part here
+    dX = out if out is not None else torch.empty_like(dX_hat)
+    ws = _ws(ws, CALL_FAKEQUANT_ACT_BWD, q, 0, rows, K, X.device)
+    _check(lib().focus_fakequant_act_bwd(ctypes.byref(q), _ptr(X), _dt(X), rows, K, _ptr(dX_hat), _dt(dX_hat),
+                                         _ptr(dX), _ptr(ws), ws.numel(), _stream()), "focus_fakequant_act_bwd")
+    return dX
+
+
+def kl_top(Z_student: torch.Tensor, Z_teacher: torch.Tensor, k: int = 1000, ws=None, out=None, loss=None):
+    """KL-Top loss of student logits against teacher logits -> (dZ_student, loss [1] fp64)."""
+    T, V = Z_student.shape
+    assert Z_teacher.shape == Z_student.shape and Z_teacher.dtype == Z_student.dtype
+    dZ = out if out is not None else torch.empty_like(Z_student)
+    loss_t = loss if loss is not None else torch.empty(1, dtype=torch.float64, device=Z_student.device)
+    need = workspace_size(CALL_KL_TOP, qconfig(MXFP4, 8), T, V, 0)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, Z_student.device)
+    _check(lib().focus_kl_top(_ptr(Z_student), _ptr(Z_teacher), _dt(Z_student), T, V, k, _ptr(dZ), _ptr(loss_t),
+                              _ptr(ws), ws.numel(), _stream()), "focus_kl_top")
+    return dZ, loss_t
 
 
 def adamw_step(param: torch.Tensor, grad: torch.Tensor, exp_avg: torch.Tensor, exp_avg_sq: torch.Tensor, t: int,

@@ -1,0 +1,140 @@
+"""GPU parity of end-to-end chaining against the CPU oracle: the input gradient of a linear, the
+straight-through backward of the activation fake quantisation and the KL-Top loss (Sec. 3.2, 4.1).
+
+  * focus_recon_gemm_dx: dX_hat = dY W_hat on the bf16 MFMA path (a hidden-2560 k_proj shape and a
+    ragged one), the fp32 path (1e-5) and an empty contraction (exact zeros); bf16 within 2e-2;
+  * focus_fakequant_act_bwd: dX = m * dX_hat bit for bit (MXFP4 rounded-up E8M0: every mask 1; OCP
+    floor rule and NVFP4: clipped elements), bf16 and fp32;
+  * focus_kl_top: loss within 1e-5, dZ within 1e-5 (fp32) / 2e-2 (bf16 output), zero exactly off the
+    teacher's top-k set, for k = 1000 of ragged vocabularies, k = 1, k >= V, bf16 logits with many
+    ties (index-order tie rule), deterministic from run to run;
+  * the top layer of a stack trained on KL-Top: loss, grad_s, grad_c and dX through KL-Top, the
+    fused backward driven by dZ, dX_hat and the activation backward (fp32 1e-5; bf16 2e-2).
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_common import announce, assert_bits_equal, assert_close, device_bits, host_f32, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def F():
+    return require_gpu()
+
+
+@pytest.fixture(scope="module")
+def C():
+    from oracle import chain_oracle
+    return chain_oracle
+
+
+def dev(a, dt):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda().to(dt).contiguous()
+
+
+@pytest.mark.parametrize("M,N,K,dt,tol", [(1000, 1024, 2560, torch.bfloat16, 2e-2), (300, 272, 264, torch.bfloat16, 2e-2),
+                                          (128, 256, 256, torch.float32, 1e-5), (70, 48, 40, torch.float32, 1e-5)])
+def test_recon_gemm_dx(F, C, M, N, K, dt, tol):
+    announce(f"dx M={M} N={N} K={K} dt={dt}")
+    rng = np.random.default_rng(M + N + K)
+    dY = dev(rng.normal(size=(M, N)) * 1e-3, dt)
+    W = dev(rng.normal(size=(N, K)) * 0.02, dt)
+    dX = F.recon_gemm_dx(dY, W)
+    torch.cuda.synchronize()
+    assert_close(host_f32(dX), C.recon_dx(host_f32(dY), host_f32(W)), tol, "dX_hat")
+
+
+def test_recon_gemm_dx_empty_contraction(F):
+    announce("dx N=0")
+    dY = torch.empty(5, 0, dtype=torch.bfloat16, device="cuda")  # empty operands come as NULL pointers
+    W = torch.empty(0, 24, dtype=torch.bfloat16, device="cuda")
+    dX = F.recon_gemm_dx(dY, W, out=torch.full((5, 24), 7.0, dtype=torch.bfloat16, device="cuda"))
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(dX).item() == 0
+
+
+@pytest.mark.parametrize("fmt,floor", [(0, 0), (0, 1), (1, 0)], ids=["mx", "mx_floor", "nv"])
+@pytest.mark.parametrize("dt", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+def test_activation_backward_bitexact(F, C, fmt, floor, dt):
+    M, K = 333, 1024
+    announce(f"act bwd fmt={fmt} floor={floor} dt={dt}")
+    rng = np.random.default_rng(fmt * 2 + floor)
+    X = rng.normal(size=(M, K)) * np.exp2(rng.integers(-6, 6, (M, 1)))
+    X[:, ::41] *= 30
+    X[4] = 0.0
+    Xd = dev(X, dt)
+    g = dev(rng.normal(size=(M, K)), dt)
+    dX = F.fakequant_act_bwd(Xd, g, fmt, e8m0_rounding=floor)
+    torch.cuda.synchronize()
+    m = C.act_ste_mask(host_f32(Xd), fmt, e8m0_floor=bool(floor))
+    ref = np.where(m != 0, host_f32(g), np.float32(0.0)).astype(np.float32)  # a dropped gradient is +0
+    assert_bits_equal(device_bits(dX), device_bits(dev(ref, dt)), "dX")
+    if fmt == 0 and not floor:
+        assert np.all(m[np.abs(host_f32(Xd)) > 0] == 1.0)
+    else:
+        assert (m == 0).any()
+
+
+def logits(rng, T, V, ties=False):
+    if ties:  # multiples of 1/4 in about [-12, 12]: exact in bf16, and many equal values per row
+        return np.round(rng.normal(size=(T, V)) * 12.0) / 4.0
+    return rng.normal(size=(T, V)) * 3.0
+
+
+@pytest.mark.parametrize("T,V,k,dt,ties", [(64, 1007, 1000, torch.float32, False), (32, 32000, 1000, torch.float32, False),
+                                           (32, 32000, 1000, torch.bfloat16, False), (48, 5000, 1000, torch.bfloat16, True),
+                                           (16, 700, 1, torch.float32, False), (16, 700, 900, torch.bfloat16, False),
+                                           (8, 4099, 4099, torch.float32, False)])
+def test_kl_top(F, C, T, V, k, dt, ties):
+    announce(f"kl_top T={T} V={V} k={k} dt={dt} ties={ties}")
+    rng = np.random.default_rng(T * 7 + V + k)
+    Zt = dev(logits(rng, T, V, ties), dt)
+    Zs = dev(host_f32(Zt) + rng.normal(size=(T, V)), dt)
+    dZ, loss = F.kl_top(Zs, Zt, k)
+    dZ2, loss2 = F.kl_top(Zs, Zt, k)
+    torch.cuda.synchronize()
+    lo, dZo = C.kl_top(host_f32(Zs), host_f32(Zt), k)
+    assert abs(loss.item() - lo) <= 1e-5 * lo, (loss.item(), lo)
+    assert_close(host_f32(dZ), dZo, 1e-5 if dt == torch.float32 else 2e-2, "dZ")
+    got_set = host_f32(dZ) != 0
+    assert not np.any(got_set & (dZo == 0)), "dZ nonzero off the teacher's top-k set"
+    if ties:
+        assert (np.diff(np.sort(host_f32(Zt), axis=1), axis=1) == 0).sum() > T * 100  # ties are present
+    assert loss.item() == loss2.item() and torch.equal(dZ, dZ2)
+
+
+@pytest.mark.parametrize("fmt,dt,tol", [(0, torch.float32, 1e-5), (0, torch.bfloat16, 2e-2), (1, torch.bfloat16, 2e-2)],
+                         ids=["mx_f32", "mx_bf16", "nv_bf16"])
+def test_top_layer_of_a_kl_top_stack(F, C, fmt, dt, tol):
+    from oracle import focus_oracle as O
+    M, K, V, sb, k = 256, 512, 2048, 8, 1000
+    announce(f"kl-top stack top layer fmt={fmt} dt={dt}")
+    rng = np.random.default_rng(fmt + 40)
+    Xd = dev(rng.normal(size=(M, K)), dt)
+    Wd = dev(rng.normal(size=(V, K)) * 0.3, dt)
+    Xh, Wh = host_f32(Xd), host_f32(Wd)
+    Zt = (Xh.astype(np.float64) @ Wh.astype(np.float64).T).astype(np.float32)  # the teacher's logits
+    Ztd = dev(Zt, dt)
+    s_o, c_o, a_o = O.init_scales(Wh, fmt, sb)
+    rs = np.random.default_rng(3)
+    s_o = (s_o * np.exp2(rs.uniform(-0.5, 0.5, s_o.shape))).astype(np.float32)
+    c_o = rs.uniform(0.75, 1.25, c_o.shape).astype(np.float32)
+    s_d, c_d = dev(s_o, torch.float32), dev(c_o, torch.float32)
+    a_d = torch.tensor([a_o], dtype=torch.float32, device="cuda")
+    x_hat = F.fakequant_fwd(Xd, fmt, sb)[0]
+    w_hat = F.fakequant_fwd(Wd, fmt, sb, s_d, c_d, a_d)[0]
+    Z, _, _ = F.recon_gemm_fwd(x_hat, w_hat, None)
+    dZ, loss = F.kl_top(Z, Ztd, k)
+    gs, gc, _ = F.recon_gemm_bwd(dZ, x_hat, Wd, fmt, sb, s_d, c_d, a_d)
+    dX = F.fakequant_act_bwd(Xd, F.recon_gemm_dx(dZ, w_hat), fmt)
+    torch.cuda.synchronize()
+    ref = C.chain_layer_backward(Xh, Wh, host_f32(Ztd), fmt, sb, s_o, c_o, a_o, k, bf16=dt == torch.bfloat16)
+    assert abs(loss.item() - ref["loss"]) <= tol * ref["loss"], (loss.item(), ref["loss"])
+    assert_close(host_f32(dZ), ref["dZ"], tol, "dZ")
+    assert_close(host_f32(gs), ref["grad_s"], tol, "grad_s")
+    assert_close(host_f32(gc), ref["grad_c"], tol, "grad_c")
+    assert_close(host_f32(dX), ref["dX"], tol, "dX")
+
