@@ -279,6 +279,7 @@ def main():
                                "frac_fp4": round(f["units"] / (f["total_ms"] * 1e-3) / 1e12 / PEAK_FP4_TFLOPS, 4)},
             "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "total_ms_per_step": round(v["total_ms"] / args.steps, 4)}
                         for k, v in mx_kern.items()}}
+    result["chain"] = chain_costs(torch, F, layers, acts, x_hat, fmt, sb, M, ws_fwd, rnd)
     result["optimizer"] = optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws_fq, rnd, c_b)
     result["attainable"] = attainable(torch, ms_gemm=gemm_flops / (gemm_ms * 1e-3) / 1e12,
                                       fq_GBps=fq_bytes / (fq_ms * 1e-3) / 1e9)
@@ -335,6 +336,59 @@ def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, rnd, c_b, reps=5
             "export": {"ms_per_block": round(res["export"], 4), "weights": n_w,
                        "GBps": round(exp_bytes / (res["export"] * 1e-3) / 1e9, 1),
                        "frac_hbm": round(exp_bytes / (res["export"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}}
+
+
+def chain_costs(torch, F, layers, acts, x_hat, fmt, sb, M, ws, rnd, reps=3):
+    """Outside the step: what end-to-end chaining adds per block (the input gradient dX_hat = dY W_hat
+    of every linear, 2 M N K flops each, and the activation straight-through backward of every block
+    input), and the KL-Top loss on a vocabulary-sized logit tensor (8192 tokens x 151,936 logits,
+    k = 1000; algorithmic bytes: read both logit rows, write dZ)."""
+    dev = acts[layers[0]["lin"].source].device
+    max_n = max(L["lin"].N for L in layers)
+    dY = (torch.randn(M, max_n, device=dev) * 1e-3).to(acts[layers[0]["lin"].source].dtype)
+    ws_dx = F.workspace(max(F.workspace_size(F.CALL_RECON_GEMM_DX, F.qconfig(fmt, sb), M, L["lin"].N, L["lin"].K)
+                            for L in layers))
+    dxs = {src: torch.empty_like(x) for src, x in acts.items()}
+    W_hats = [F.fakequant_fwd(L["W"], fmt, sb, L["s"], L["cf"], L["a"], e8m0_rounding=rnd)[0] for L in layers]
+
+    def dx_all():
+        for L, Wh in zip(layers, W_hats):
+            lin = L["lin"]
+            F.recon_gemm_dx(dY.view(-1)[:M * lin.N].view(M, lin.N), Wh, ws=ws_dx, out=dxs[lin.source])
+
+    def act_all():
+        for src, x in acts.items():
+            F.fakequant_act_bwd(x, dxs[src], fmt, e8m0_rounding=rnd, ws=ws, out=dxs[src])
+
+    T, V = 8192, 151936
+    Zt = (torch.randn(T, V, device=dev) * 3).to(torch.bfloat16)
+    Zs = (Zt.float() + torch.randn(T, V, device=dev)).to(torch.bfloat16)
+    dZ = torch.empty_like(Zs)
+    ws_kl = F.workspace(F.workspace_size(F.CALL_KL_TOP, F.qconfig(fmt, sb), T, V, 0))
+    res = {}
+    for name, fn in (("dx", dx_all), ("act_bwd", act_all), ("kl_top", lambda: F.kl_top(Zs, Zt, 1000, ws=ws_kl, out=dZ))):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = e0.elapsed_time(e1) / reps
+    if F.check_flags(ws_kl) != F.OK:
+        raise RuntimeError("domain error in the KL-Top timing")
+    dx_flops = sum(2 * M * L["lin"].N * L["lin"].K for L in layers)
+    act_elems = sum(x.numel() for x in acts.values())
+    esz = acts[layers[0]["lin"].source].element_size()
+    del Zt, Zs, dZ, dY
+    return {"dx": {"ms_per_block": round(res["dx"], 4), "TFLOPs": round(dx_flops / (res["dx"] * 1e-3) / 1e12, 1),
+                   "frac_bf16": round(dx_flops / (res["dx"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
+            "act_bwd": {"ms_per_block": round(res["act_bwd"], 4),
+                        "GBps": round(act_elems * 3 * esz / (res["act_bwd"] * 1e-3) / 1e9, 1)},
+            "kl_top": {"tokens": T, "vocab": V, "k": 1000, "ms": round(res["kl_top"], 4),
+                       "us_per_token": round(res["kl_top"] * 1e3 / T, 3),
+                       "GBps": round(T * V * 6 / (res["kl_top"] * 1e-3) / 1e9, 1)}}
 
 
 def attainable(torch, ms_gemm, fq_GBps):

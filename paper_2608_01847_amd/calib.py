@@ -177,6 +177,89 @@ def ablation(w: synth.Workload, steps: int = EPOCH_STEPS, M: int | None = None, 
     return out
 
 
+class KLTopStack:
+    """A synthetic two-linear stack trained end to end on KL-Top (Sec. 4.1; f1 of the hot path's
+    extensions): X0 [M][h] -> "up" (h -> h) -> "head" (h -> V) -> logits. The teacher is the same
+    stack unquantised; the student quantises every activation and weight. One training step:
+
+        forward:  X0_hat, W_up_hat -> Y1 -> Y1_hat, W_head_hat -> Z     (plain-product GEMMs)
+        loss:     KL-Top(Z, Z_teacher), dZ
+        backward: head: grad_s, grad_c from dZ (fused straight-through epilogue);
+                  dY1 = STE_act(Y1, dZ W_head_hat); up: grad_s, grad_c from dY1
+        update:   AdamW on both layers' S_fp and c (log2 domain)
+
+    Every arithmetic step runs in libfocus."""
+
+    def __init__(self, fmt: int, variant: str, hidden: int = 2560, vocab: int = 32000, tokens: int = 4096,
+                 k: int = 1000, x_kind: str = "lowrank", hyper: Hyper | None = None, device="cuda"):
+        from .synth import Linear, Workload
+        self.w = Workload(name=f"klstack{hidden}x{vocab}", fmt=fmt, sub_block=8, M=tokens,
+                          linears=(Linear("up", hidden, hidden, "x"), Linear("head", vocab, hidden, "y")),
+                          inputs={"x": hidden, "y": hidden}, x_kind=x_kind, x_outlier_p=0.01, x_outlier_f=30.0)
+        self.variant, self.k, self.device = variant, k, device
+        self.sb, self.learn_s, self.learn_c, self.use_c = variant_setup(self.w, variant)
+        lr_s, lr_c = LEARNING_RATES[fmt]
+        self.hyper = hyper or Hyper(lr_s, lr_c)
+        q = F.qconfig(fmt, self.sb)
+        M = tokens
+        self.ws = F.workspace(max(F.workspace_size(F.CALL_FAKEQUANT_FWD, q),
+                                  max(F.workspace_size(F.CALL_RECON_GEMM_BWD, q, M, l.N, l.K) for l in self.w.linears),
+                                  max(F.workspace_size(F.CALL_RECON_GEMM_FWD, q, M, l.N, l.K) for l in self.w.linears),
+                                  F.workspace_size(F.CALL_RECON_GEMM_DX, q, M, vocab, hidden),
+                                  F.workspace_size(F.CALL_KL_TOP, q, M, vocab, 0)), device)
+        self.layers = {l.name: LayerState(synth.weight(self.w, l, device=device), fmt, self.sb, self.ws)
+                       for l in self.w.linears}
+        self.t = 0
+
+    def _c(self, L):
+        return L.c if self.use_c else None
+
+    def _update(self, L, gs, gc):
+        h = self.hyper
+        if self.learn_s:
+            F.adamw_step(L.s, gs, L.ms, L.vs, self.t, h.lr_s, h.betas, h.eps, h.weight_decay, h.log2_scales, self.ws)
+        if self.learn_c:
+            F.adamw_step(L.c, gc, L.mc, L.vc, self.t, h.lr_c, h.betas, h.eps, h.weight_decay, h.log2_coeffs, self.ws)
+
+    def run_batch(self, batch: int, learn: bool) -> float:
+        """KL-Top loss of the stack on batch `batch` (and one training step when `learn`)."""
+        fmt, sb, ws, w = self.w.fmt, self.sb, self.ws, self.w
+        up, head = self.layers["up"], self.layers["head"]
+        X0 = synth.activation_batch(w, "x", batch, w.M, device=self.device)
+        Zt = F.recon_gemm_fwd(F.recon_gemm_fwd(X0, up.W, None, ws=ws)[0], head.W, None, ws=ws)[0]
+        x0h = F.fakequant_fwd(X0, fmt, sb, ws=ws)[0]
+        w_up = F.fakequant_fwd(up.W, fmt, sb, up.s, self._c(up), up.alpha, ws=ws)[0]
+        Y1 = F.recon_gemm_fwd(x0h, w_up, None, ws=ws)[0]
+        y1h = F.fakequant_fwd(Y1, fmt, sb, ws=ws)[0]
+        w_head = F.fakequant_fwd(head.W, fmt, sb, head.s, self._c(head), head.alpha, ws=ws)[0]
+        Z = F.recon_gemm_fwd(y1h, w_head, None, ws=ws)[0]
+        dZ, loss = F.kl_top(Z, Zt, self.k, ws=ws)
+        if learn:
+            self.t += 1
+            gs2, gc2, _ = F.recon_gemm_bwd(dZ, y1h, head.W, fmt, sb, head.s, self._c(head), head.alpha, ws=ws)
+            dY1 = F.fakequant_act_bwd(Y1, F.recon_gemm_dx(dZ, w_head, ws=ws), fmt, ws=ws)
+            gs1, gc1, _ = F.recon_gemm_bwd(dY1, x0h, up.W, fmt, sb, up.s, self._c(up), up.alpha, ws=ws)
+            self._update(head, gs2, gc2)
+            self._update(up, gs1, gc1)
+        return float(loss.item())
+
+
+def kl_top_epoch(fmt: int, variant: str, steps: int = EPOCH_STEPS, **kw) -> dict:
+    """One epoch of the KL-Top stack -> held-out KL-Top before and after, and the training curve."""
+    stack = KLTopStack(fmt, variant, **kw)
+    before = stack.run_batch(EVAL_STEP, learn=False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    curve = [stack.run_batch(b, learn=True) for b in range(steps if variant != "rtn" else 0)]
+    torch.cuda.synchronize()
+    seconds = time.perf_counter() - t0
+    after = stack.run_batch(EVAL_STEP, learn=False)
+    st = F.check_flags(stack.ws)
+    if st != F.OK:
+        raise F.FocusError(st, f"KL-Top stack ({variant})")
+    return {"variant": variant, "eval_before": before, "eval_after": after, "train_curve": curve, "seconds": seconds}
+
+
 def main() -> None:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--workload", default="block2560_mxfp4", choices=sorted(synth.WORKLOADS))
@@ -186,10 +269,24 @@ def main() -> None:
     ap.add_argument("--variants", default=",".join(VARIANTS))
     ap.add_argument("--x-kind", default=None, choices=("normal", "student_t3", "lowrank"),
                     help="activation distribution (default: the workload's)")
+    ap.add_argument("--kl-top-stack", action="store_true",
+                    help="train the synthetic two-linear stack end to end on KL-Top instead")
+    ap.add_argument("--vocab", type=int, default=32000)
     a = ap.parse_args()
     if not torch.cuda.is_available():
         raise SystemExit("the calibration epoch runs on the GPU")
     w = synth.WORKLOADS[a.workload]
+    if a.kl_top_stack:
+        hidden = w.inputs[w.linears[0].source]
+        out = {"stack": f"hidden {hidden} -> {hidden} -> vocab {a.vocab}", "x_kind": a.x_kind or "lowrank",
+               "steps": a.steps, "tokens_per_step": a.tokens or 4096, "results": {}}
+        for v in a.variants.split(","):
+            r = kl_top_epoch(w.fmt, v, a.steps, hidden=hidden, vocab=a.vocab, tokens=a.tokens or 4096,
+                             x_kind=a.x_kind or "lowrank")
+            out["results"][v] = {"eval_before": r["eval_before"], "eval_after": r["eval_after"],
+                                 "seconds": round(r["seconds"], 3), "train_first_last": r["train_curve"][:1] + r["train_curve"][-1:]}
+        print(json.dumps(out))
+        return
     if a.x_kind:
         w = dataclasses.replace(w, x_kind=a.x_kind)
     res = ablation(w, a.steps, a.tokens, a.eval_tokens, tuple(a.variants.split(",")))
