@@ -34,9 +34,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=32768)
     p.add_argument("--cpu-sample-rows", type=int, default=512)
-    p.add_argument("--fwd-operands", choices=("bf16", "mxfp4"), default="bf16",
+    p.add_argument("--fwd-operands", choices=("auto", "bf16", "mxfp4"), default="auto",
                    help="forward reconstruction GEMM from bf16 X_hat / W_hat, or (MXFP4 workloads) from their "
-                        "packed FP4 codes and E8M0 scales on the block-scaled FP4 MFMA")
+                        "packed FP4 codes and E8M0 scales on the block-scaled FP4 MFMA; auto = mxfp4 where the "
+                        "workload's format and shapes allow it, else bf16")
     p.add_argument("--sub-block", type=int, default=0, help="elements per coefficient c (0 = the workload's)")
     p.add_argument("--no-coeff", action="store_true", help="the baseline mode: no coefficients (c = 1)")
     p.add_argument("--e8m0", choices=("ceil", "floor"), default="ceil",
@@ -129,12 +130,13 @@ def main():
                            W_hat=torch.empty_like(W),
                            gs=torch.empty_like(s), gc=torch.empty_like(c),
                            loss=torch.empty(1, dtype=torch.float64, device=dev)))
-    x_hat = {src: torch.empty_like(x) for src, x in acts.items()}
-    mx_primary = args.fwd_operands == "mxfp4"
-    if mx_primary and fmt != 0:
-        print("--fwd-operands mxfp4 needs an MXFP4 workload", file=sys.stderr)
+    x_hat = {src: torch.empty_like(x) for src, x in acts.items()}  # bf16 X_hat (the bf16-operand step)
+    mx_possible = (fmt == 0 and w.dtype == "bf16" and M % 4 == 0
+                   and all(l.K % 128 == 0 and l.N % 8 == 0 for l in w.linears))
+    if args.fwd_operands == "mxfp4" and not mx_possible:
+        print("--fwd-operands mxfp4 needs an MXFP4 workload whose shapes the FP4 forward takes", file=sys.stderr)
         sys.exit(2)
-    mx_possible = fmt == 0 and M % 4 == 0 and all(l.K % 128 == 0 and l.N % 8 == 0 for l in w.linears)
+    mx_primary = args.fwd_operands == "mxfp4" or (args.fwd_operands == "auto" and mx_possible)
     if mx_possible:  # packed operands of an MXFP4 forward: codes [rows][K/2] and E8M0 bytes [rows][K/32]
         # (scale bytes block-major, [K/32][rows], the layout the MXFP4 forward reads)
         x_codes = {src: torch.empty(M, x.shape[1] // 2, dtype=torch.uint8, device=dev) for src, x in acts.items()}
@@ -155,8 +157,10 @@ def main():
         for src, x in acts.items():
             rows, K = x.shape
             if mx_fwd:
-                timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src], e8m0_rounding=rnd,
-                                                                   codes_out=x_codes[src], scales_out=x_scales[src],
+                # the packed form only: both GEMMs read the codes and E8M0 bytes, no bf16 X_hat
+                timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, want_x_hat=False,
+                                                                   e8m0_rounding=rnd, codes_out=x_codes[src],
+                                                                   scales_out=x_scales[src],
                                                                    scale_layout=F.SCALES_BLOCK_MAJOR),
                           rows * K)
             else:
@@ -185,11 +189,17 @@ def main():
                 timer.run("recon_gemm_fwd",
                           lambda: F.recon_gemm_fwd(xh, L["W_hat"], L["Y"], ws=ws_fwd, out=dY, loss=L["loss"]),
                           2 * M * lin.N * lin.K)
-            timer.run("recon_gemm_bwd",
-                      lambda: F.recon_gemm_bwd(dY, xh, L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws_bwd,
-                                               e8m0_rounding=rnd,
-                                               out=(L["gs"], L["gc"])),
-                      2 * M * lin.N * lin.K)
+            if mx_fwd:
+                timer.run("recon_gemm_bwd",
+                          lambda: F.recon_gemm_bwd_mxfp4(dY, x_codes[lin.source], x_scales[lin.source], L["W"], sb,
+                                                         L["s"], L["cf"], ws=ws_bwd, e8m0_rounding=rnd,
+                                                         out=(L["gs"], L["gc"])),
+                          2 * M * lin.N * lin.K)
+            else:
+                timer.run("recon_gemm_bwd",
+                          lambda: F.recon_gemm_bwd(dY, xh, L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws_bwd,
+                                                   e8m0_rounding=rnd, out=(L["gs"], L["gc"])),
+                          2 * M * lin.N * lin.K)
 
     def run(mx_fwd):
         """Warm-up, then exactly args.steps timed steps; -> (ms per step, per-family summary)."""
@@ -217,10 +227,11 @@ def main():
 
     # ---- algorithmic work ----
     # fake quantisation bytes per element: activations read 2 + write 2 (bf16) (+2 for the NVFP4
-    # tensor-absmax pass, + 0.5 + 1/32 for the codes and scale bytes of an MXFP4 forward); weights
-    # read W 2 + S_fp 4/B + c 4/sb, write W_hat 2 (or, for an MXFP4 forward, codes 0.5 + bytes 1/32)
+    # tensor-absmax pass; the MXFP4-operand step writes codes 0.5 + scale bytes 1/32 instead of X_hat);
+    # weights read W 2 + S_fp 4/B + c 4/sb, write W_hat 2 (or, for the MXFP4-operand step, codes 0.5 +
+    # bytes 1/32)
     esz = 2 if w.dtype == "bf16" else 4
-    act_b = (2 * esz + (esz if fmt == 1 else 0)) + (0.5 + 1.0 / 32 if mx_fwd else 0.0)
+    act_b = (esz + 0.5 + 1.0 / 32) if mx_fwd else (2 * esz + (esz if fmt == 1 else 0))
     c_b = 0.0 if args.no_coeff else 4.0 / sb
     wt_b = esz + 4.0 / B + c_b + ((0.5 + 1.0 / 32) if mx_fwd else esz)
     fq_bytes = kern["fakequant_act"]["units"] * act_b + kern["fakequant_weight"]["units"] * wt_b
@@ -238,7 +249,7 @@ def main():
     achieved = per_launch_flops / (d["avg_ms"] * 1e-3) / 1e12
     src_hash = kernel_source_hash()
     kname = {"recon_gemm_fwd": "fwd_mfma_kernel_mx" if mx_fwd else "fwd_mfma_kernel",
-             "recon_gemm_bwd": "bwd_mfma_kernel"}[dominant]
+             "recon_gemm_bwd": "bwd_mfma_mx_kernel" if mx_fwd else "bwd_mfma_kernel"}[dominant]
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peaks[dominant], "unit": "TFLOP/s",
                 "frac": round(achieved / peaks[dominant], 4), "traffic": traffic_from_profile(kname, src_hash),
                 "kernel": kname, "avg_launch_ms": round(d["avg_ms"], 4), "launches": d["launches"],
@@ -248,11 +259,12 @@ def main():
         "metric": METRIC, "value": round(ms_per_step, 4), "unit": "ms per step", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
-        "dtype": ("bf16+mxfp4" if mx_fwd else "bf16") if esz == 2 else "f32",
+        "dtype": ("mxfp4+bf16" if mx_fwd else "bf16") if esz == 2 else "f32",
         "data": "synthetic (seeded; shapes and distributions of the calibration workload)",
         "config": {"workload": w.name, "tokens": M, "format": "mxfp4" if fmt == 0 else "nvfp4", "sub_block": sb,
                    "coefficients": not args.no_coeff, "e8m0": args.e8m0,
-                   "fwd_operands": args.fwd_operands, "linears": {l.name: [l.N, l.K] for l in w.linears}},
+                   "fwd_operands": "mxfp4" if mx_fwd else "bf16",
+                   "linears": {l.name: [l.N, l.K] for l in w.linears}},
         "roofline": roofline,
         "fakequant_GBps": round(fq_bytes / (fq_ms * 1e-3) / 1e9, 1),
         "fakequant_frac_hbm": round(fq_bytes / (fq_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
@@ -266,19 +278,21 @@ def main():
         "block_loss": block_loss,
         "source_hash": src_hash,
     }
-    if mx_possible and not mx_primary:
-        # the same step with the forward on the packed MXFP4 operands (block-scaled FP4 MFMA: exact
-        # products, fp32 sums, the bf16 path's result up to the accumulation order), same inputs
-        mx_ms, mx_kern = run(True)
-        mx_loss = float(sum(L["loss"].item() for L in layers))
-        f = mx_kern["recon_gemm_fwd"]
-        result["mxfp4_forward"] = {
-            "ms_per_step": round(mx_ms, 4), "block_loss": mx_loss,
-            "recon_gemm_fwd": {"TFLOPs": round(f["units"] / (f["total_ms"] * 1e-3) / 1e12, 1),
-                               "peak_fp4": PEAK_FP4_TFLOPS,
-                               "frac_fp4": round(f["units"] / (f["total_ms"] * 1e-3) / 1e12 / PEAK_FP4_TFLOPS, 4)},
+    if mx_possible:
+        # the same step with the other forward operands, same inputs: under MXFP4, X_hat and W_hat
+        # are exactly E2M1 codes times power-of-two block scales, so the bf16 and the block-scaled FP4
+        # MFMA form the same exact products and differ only in the fp32 accumulation order
+        alt = not mx_fwd
+        alt_ms, alt_kern = run(alt)
+        alt_loss = float(sum(L["loss"].item() for L in layers))
+        f = alt_kern["recon_gemm_fwd"]
+        peak = PEAK_FP4_TFLOPS if alt else PEAK_BF16_TFLOPS
+        tf = f["units"] / (f["total_ms"] * 1e-3) / 1e12
+        result["mxfp4_forward" if alt else "bf16_forward"] = {
+            "ms_per_step": round(alt_ms, 4), "block_loss": alt_loss,
+            "recon_gemm_fwd": {"TFLOPs": round(tf, 1), "peak": peak, "frac": round(tf / peak, 4)},
             "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "total_ms_per_step": round(v["total_ms"] / args.steps, 4)}
-                        for k, v in mx_kern.items()}}
+                        for k, v in alt_kern.items()}}
     result["chain"] = chain_costs(torch, F, layers, acts, x_hat, fmt, sb, M, ws_fwd, rnd)
     result["optimizer"] = optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws_fq, rnd, c_b)
     result["attainable"] = attainable(torch, ms_gemm=gemm_flops / (gemm_ms * 1e-3) / 1e12,

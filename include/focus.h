@@ -124,6 +124,8 @@ focus_status focus_scales_init(const focus_qconfig *q, const void *W, int w_dtyp
  *   fl32(alpha_x * 6)))); alpha_x is written to *alpha_out_opt when it is non-NULL.
  * Optional outputs: codes_opt [rows][K/2] packed FP4 codes (code = sign<<3 | magnitude index, the
  *   even-k code in the low nibble); scale_bytes_opt [rows][K/B] (E8M0 byte e+127, or E4M3 byte).
+ *   X_hat may be NULL when codes_opt is not (the packed form alone, e.g. for the MXFP4 GEMMs);
+ *   X_hat and codes_opt both NULL is FOCUS_ERR_NULL.
  * A zero dequantisation (or quantisation) scale quantises its block to signed zeros. */
 focus_status focus_fakequant_fwd(const focus_qconfig *q, const void *X, int x_dtype, int64_t rows, int64_t K,
                                  const float *s_fp, const float *c, const float *alpha,
@@ -182,6 +184,24 @@ focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const 
                                   const void *W, int w_dtype, const float *s_fp, const float *c,
                                   const float *alpha, float *grad_s, float *grad_c, float *G_out_opt,
                                   void *ws, size_t ws_bytes, focus_stream stream);
+
+/* Reconstruction GEMM backward with the fused straight-through epilogue, X_hat given as packed
+ * MXFP4 (MXFP4 only: FOCUS_ERR_CONFIG for NVFP4). Under MXFP4, X_hat is exactly an E2M1 code times
+ * its block's E8M0 power of two (Sec. 3.1, Eq. 1 and 3); the library rebuilds the bf16 operand from
+ * that representation without loss, so grad_s and grad_c are those of focus_recon_gemm_bwd on the
+ * bf16 X_hat up to the fp32 accumulation order.
+ *   dY [M][N] bf16; X_codes [M][K/2] (two codes per byte, even k in the low nibble) and X_scales
+ *   [K/32][M] (E8M0 bytes, block-major): the codes_opt / scale_bytes_opt outputs of
+ *   focus_fakequant_fwd in activation mode with FOCUS_SCALES_BLOCK_MAJOR. W, s_fp, c, grad_s, grad_c
+ *   as in focus_recon_gemm_bwd. Requires M % 4 == 0 and N % 8 == 0 (FOCUS_ERR_SHAPE otherwise); dY,
+ *   X_codes and W 16-byte aligned, X_scales 4-byte aligned. The workspace is that of
+ *   FOCUS_CALL_RECON_GEMM_BWD. A scale byte 255 (NaN, never written by the library) makes its
+ *   block's values NaN. */
+focus_status focus_recon_gemm_bwd_mxfp4(const focus_qconfig *q, const void *dY, const uint8_t *X_codes,
+                                        const uint8_t *X_scales, int64_t M, int64_t N, int64_t K,
+                                        const void *W, int w_dtype, const float *s_fp, const float *c,
+                                        float *grad_s, float *grad_c, void *ws, size_t ws_bytes,
+                                        focus_stream stream);
 
 /* Export of the deployable tensor (Fig. 3(d): only FP4 codes and dequantisation scales are kept;
  * the coefficients and S_q are discarded): packed [N][K/2] codes as in focus_fakequant_fwd and

@@ -136,7 +136,7 @@ focus_status focus_fakequant_fwd(const focus_qconfig *q, const void *X, int x_dt
                                  int xhat_dtype, uint8_t *codes_opt, uint8_t *scale_bytes_opt,
                                  float *alpha_out_opt, void *ws, size_t ws_bytes, focus_stream stream) {
     FOCUS_TRY(check_q(q));
-    if (!X || !X_hat) return FOCUS_ERR_NULL;
+    if (!X || (!X_hat && !codes_opt)) return FOCUS_ERR_NULL;  // X_hat may be left out when codes are asked for
     const bool weight_mode = s_fp != nullptr;
     if (weight_mode && q->format == FOCUS_NVFP4 && !alpha) return FOCUS_ERR_NULL;
     if (!weight_mode && (c || alpha)) return FOCUS_ERR_CONFIG;
@@ -225,6 +225,28 @@ focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const 
     return hip_status(launch_recon_bwd(p, op_dtype, q->format, q->sub_block, q->ste_clip, floor_of(q), dY, X_hat, M, N, K, W,
                                        w_dtype, s_fp, c, alpha, grad_s, grad_c, G_out_opt, ws, flag_of(ws),
                                        (hipStream_t)stream));
+}
+
+focus_status focus_recon_gemm_bwd_mxfp4(const focus_qconfig *q, const void *dY, const uint8_t *X_codes,
+                                        const uint8_t *X_scales, int64_t M, int64_t N, int64_t K, const void *W,
+                                        int w_dtype, const float *s_fp, const float *c, float *grad_s,
+                                        float *grad_c, void *ws, size_t ws_bytes, focus_stream stream) {
+    FOCUS_TRY(check_q(q));
+    if (q->format != FOCUS_MXFP4) return FOCUS_ERR_CONFIG;
+    if (!dY || !X_codes || !X_scales || !W || !s_fp || !grad_s || !grad_c) return FOCUS_ERR_NULL;
+    if (!dtype_ok(w_dtype)) return FOCUS_ERR_DTYPE;
+    FOCUS_TRY(check_rows_k(N, K, 32));
+    if (M < 0 || M > kMaxDim || (M > 0 && K > kMaxElems / M) || (M > 0 && N > kMaxElems / M))
+        return FOCUS_ERR_SHAPE;
+    if (M % 4 != 0 || N % 8 != 0) return FOCUS_ERR_SHAPE;
+    if (!all_aligned({dY, X_codes, W})) return FOCUS_ERR_SHAPE;
+    if (reinterpret_cast<uintptr_t>(X_scales) & 3u) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_ws(ws, ws_bytes, bwd_ws(q->format, q->sub_block, M, N, K)));
+    if (N == 0 || K == 0) return FOCUS_OK;
+    if (!mfma_bwd_mx_supported(M, N, K)) return FOCUS_ERR_SHAPE;
+    const BwdPlan p = plan_bwd(FOCUS_BF16, q->format, q->sub_block, M, N, K, false);
+    return hip_status(launch_recon_bwd_mx(p, q->sub_block, q->ste_clip, floor_of(q), dY, X_codes, X_scales, M, N, K,
+                                          W, w_dtype, s_fp, c, grad_s, grad_c, ws, flag_of(ws), (hipStream_t)stream));
 }
 
 focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dtype, int64_t N, int64_t K,

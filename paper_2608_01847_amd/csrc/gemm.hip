@@ -342,4 +342,20 @@ hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int st
     return hipGetLastError();
 }
 
+hipError_t launch_recon_bwd_mx(const BwdPlan &p, int sb, int ste_clip, int e8m0_floor, const void *dY, const void *Xc,
+                               const void *Xs, int64_t M, int64_t N, int64_t K, const void *W, int w_dt,
+                               const float *s_fp, const float *c, float *grad_s, float *grad_c, void *ws,
+                               uint32_t *flag, hipStream_t st) {
+    const int64_t nb = K / 32, ns = K / sb;
+    float *part_s = reinterpret_cast<float *>(reinterpret_cast<char *>(ws) + kWsHeader);
+    float *part_c = part_s + p.splits * N * nb;
+    hipError_t e = launch_bwd_mfma_mx(w_dt, dY, Xc, Xs, M, N, K, p.chunk, p.splits, W, s_fp, c, sb, ste_clip,
+                                      e8m0_floor, part_s, part_c, flag, st);
+    if (e != hipSuccess) return e;
+    const int64_t total = N * (nb + ns);
+    const unsigned g = (unsigned)std::min<int64_t>(std::max<int64_t>(cdiv(total, 256), 1), kStreamGridCap);
+    bwd_finish_kernel<<<g, 256, 0, st>>>(part_s, part_c, p.splits, N * nb, N * ns, c, nullptr, kFmtMX, grad_s, grad_c);
+    return hipGetLastError();
+}
+
 }  // namespace focus

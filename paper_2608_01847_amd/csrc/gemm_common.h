@@ -46,4 +46,11 @@ hipError_t launch_bwd_mfma(int fmt, int w_dt, const void *dY, const void *X, int
                            int sb, const float *alpha, int ste_clip, int e8m0_floor, float *part_s,
                            float *part_c, uint32_t *flag, hipStream_t st);
 
+// the backward from X_hat as packed MXFP4 (codes [M][K/2], E8M0 bytes block-major [K/32][M])
+bool mfma_bwd_mx_supported(int64_t M, int64_t N, int64_t K);
+hipError_t launch_bwd_mfma_mx(int w_dt, const void *dY, const void *Xc, const void *Xs, int64_t M, int64_t N,
+                              int64_t K, int64_t chunk, int64_t splits, const void *W, const float *s_fp,
+                              const float *c, int sb, int ste_clip, int e8m0_floor, float *part_s, float *part_c,
+                              uint32_t *flag, hipStream_t st);
+
 }  // namespace focus

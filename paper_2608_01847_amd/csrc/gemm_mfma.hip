@@ -516,95 +516,18 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     if (n0 + t < N) colpart[(int64_t)tm * N + n0 + t] = red[t] + red[kTile + t];
 }
 
-// ------------------------------------------------------------------------------------------------
+// Fused straight-through epilogue of the backward kernels on G^T = acc (a 256 k x 256 n tile):
+// per-split partial sums of G m w per sub-block and of G (q - m u) per block.
+// acc[i][j][r] is G[n][k] for n = n0 + 128 wn + 32 j + (lane % 32) and
+// k = k0 + 128 wm + 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4: lane l holds, for each group g of
+// 8 k, the 4 consecutive k 4 (l / 32) .. + 3, and lanes l, l ^ 32 together hold the whole group.
 template <int FMT, int WDT>
-__global__ void __launch_bounds__(kThreads, 1)
-bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X, int64_t M, int64_t N, int64_t K,
-                int64_t chunk, const void *__restrict__ W, const float *__restrict__ s_fp,
-                const float *__restrict__ c, int sb_log2, const float *__restrict__ alpha_ptr, int ste_clip,
-                int e8m0_floor, float *__restrict__ part_s, float *__restrict__ part_c, uint32_t *flag, int tiles_n) {
-    __shared__ __attribute__((aligned(16))) char smem[kBwdStages * kBwdStageBytes];
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
-    // linear id -> (split, tile): splits outermost, tiles of one split in grouped order, so that an
-    // XCD's concurrent workgroups share the operand panels of one token range
-    const uint32_t id = xcd_tile(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
-    uint32_t tk, tn;
-    grouped_tile(id % gridDim.x, gridDim.x / tiles_n, tiles_n, tk, tn);
-    const int64_t k0 = (int64_t)tk * kTile, n0 = (int64_t)tn * kTile;
-    const int64_t split = id / gridDim.x;
-    const int64_t t_begin = split * chunk, t_end = std::min<int64_t>(M, t_begin + chunk);
-
-    f32x16_t acc[4][4];
-    const f32x16_t zero = {};
-#pragma unroll
-    for (int i = 0; i < 4; i++)
-#pragma unroll
-        for (int j = 0; j < 4; j++) acc[i][j] = zero;
-
-    // A = X_hat^T (rows = in features k), B = dY (columns = out features n), both staged as
-    // token-major tiles. Four stages of 32 tokens, pipelined as in the forward kernel: slot j
-    // (8 loads per thread) fills stage j % 4 with step j; slots past the token range are empty
-    // resources whose loads only write zeros, which keeps every slot at 8 loads for the waits.
-    lds_char *const lsm = (lds_char *)smem;
-    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-    BwdDma pa, pb;
-    pa.init(K, k0, wave_u, lane);
-    pb.init(N, n0, wave_u, lane);
-    const int64_t nk = t_end > t_begin ? (t_end - t_begin + kBwdStep - 1) / kBwdStep : 0;
-#pragma unroll
-    for (int s0 = 0; s0 < kBwdStages - 1; s0++) {
-        const int64_t t0 = t_begin + s0 * kBwdStep;
-        const __amdgpu_buffer_rsrc_t ra = BwdDma::step_rsrc(X, K, t0, t_end), rb = BwdDma::step_rsrc(dY, N, t0, t_end);
-        lds_char *st = lsm + s0 * kBwdStageBytes;
-#pragma unroll
-        for (int i = 0; i < 4; i++) pa.issue_one(ra, st, wave_u, i);
-#pragma unroll
-        for (int i = 0; i < 4; i++) pb.issue_one(rb, st + kBwdOpBytes, wave_u, i);
-    }
-    uint32_t a_off[4], b_off[4];
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-        a_off[i] = tr_lane_off(wm * 128 + i * 32, lane);
-        b_off[i] = tr_lane_off(wn * 128 + i * 32, lane);
-    }
-    const uint32_t lds0 = lds_addr(smem);
-    FOCUS_WAIT_VMCNT(8);
-    asm volatile("s_barrier" ::: "memory");
-    Frags f, g;
-    load_frags_tr<0>(f, lds0, a_off, b_off);
-    for (int64_t kt = 0; kt < nk; kt++) {
-        FOCUS_WAIT_VMCNT(8);
-        asm volatile("s_barrier" ::: "memory");
-        const uint32_t cur = lds0 + (uint32_t)(kt & 3) * kBwdStageBytes;
-        const uint32_t nxt = lds0 + (uint32_t)((kt + 1) & 3) * kBwdStageBytes;
-        const int64_t t0 = t_begin + (kt + 3) * kBwdStep;
-        const __amdgpu_buffer_rsrc_t ra = BwdDma::step_rsrc(X, K, t0, t_end), rb = BwdDma::step_rsrc(dY, N, t0, t_end);
-        lds_char *st = lsm + (int)((kt + 3) & 3) * kBwdStageBytes;
-        tr_wait(f);  // f (read during the previous step's second half) has landed
-        load_frags_tr<1>(g, cur, a_off, b_off);
-        // the 8 loads of slot kt + 3 go out one after every second MFMA (see the forward kernel)
-        static_for<16>([&](auto idx) {
-            constexpr int i = idx / 4, jj = idx % 4;
-            acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[jj], acc[i][jj], 0, 0, 0);
-            if constexpr (idx % 2 == 1) {
-                __builtin_amdgcn_sched_barrier(0);
-                if constexpr (idx / 2 < 4) pa.issue_one(ra, st, wave_u, idx / 2);
-                else pb.issue_one(rb, st + kBwdOpBytes, wave_u, idx / 2 - 4);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        });
-        tr_wait(g);  // read before the first half's MFMAs, long landed
-        load_frags_tr<0>(f, nxt, a_off, b_off);
-        mma_frags(g, acc);
-    }
-    tr_wait(f);  // no read may still be in flight when the workgroup ends
-    // the empty slots' zero writes must land before the workgroup's LDS is handed on
-    FOCUS_WAIT_VMCNT(0);
-
-    // ---- fused straight-through epilogue on G^T = acc ----
-    // acc[i][j][r] is G[n][k] for n = n0 + 128 wn + 32 j + (lane % 32) and
-    // k = k0 + 128 wm + 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4: lane l holds, for each group g of
-    // 8 k, the 4 consecutive k 4 (l / 32) .. + 3, and lanes l, l ^ 32 together hold the whole group.
+__device__ __forceinline__ void ste_epilogue(const f32x16_t (&acc)[4][4], int64_t k0, int64_t n0, int64_t split,
+                                             int64_t N, int64_t K, const void *__restrict__ W,
+                                             const float *__restrict__ s_fp, const float *__restrict__ c, int sb_log2,
+                                             const float *__restrict__ alpha_ptr, int ste_clip, int e8m0_floor,
+                                             float *__restrict__ part_s, float *__restrict__ part_c, uint32_t *flag,
+                                             int wm, int wn, int lane) {
     constexpr int B = block_of(FMT);
     constexpr int NBI = 32 / B;                   // blocks per 32 k (1 MXFP4, 2 NVFP4)
     constexpr int WB = WDT == kBF16 ? 2 : 4;      // bytes per weight element
@@ -750,6 +673,355 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
     if (bad) raise_domain_flag(flag);
 }
 
+// ------------------------------------------------------------------------------------------------
+template <int FMT, int WDT>
+__global__ void __launch_bounds__(kThreads, 1)
+bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X, int64_t M, int64_t N, int64_t K,
+                int64_t chunk, const void *__restrict__ W, const float *__restrict__ s_fp,
+                const float *__restrict__ c, int sb_log2, const float *__restrict__ alpha_ptr, int ste_clip,
+                int e8m0_floor, float *__restrict__ part_s, float *__restrict__ part_c, uint32_t *flag, int tiles_n) {
+    __shared__ __attribute__((aligned(16))) char smem[kBwdStages * kBwdStageBytes];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
+    // linear id -> (split, tile): splits outermost, tiles of one split in grouped order, so that an
+    // XCD's concurrent workgroups share the operand panels of one token range
+    const uint32_t id = xcd_tile(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
+    uint32_t tk, tn;
+    grouped_tile(id % gridDim.x, gridDim.x / tiles_n, tiles_n, tk, tn);
+    const int64_t k0 = (int64_t)tk * kTile, n0 = (int64_t)tn * kTile;
+    const int64_t split = id / gridDim.x;
+    const int64_t t_begin = split * chunk, t_end = std::min<int64_t>(M, t_begin + chunk);
+
+    f32x16_t acc[4][4];
+    const f32x16_t zero = {};
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) acc[i][j] = zero;
+
+    // A = X_hat^T (rows = in features k), B = dY (columns = out features n), both staged as
+    // token-major tiles. Four stages of 32 tokens, pipelined as in the forward kernel: slot j
+    // (8 loads per thread) fills stage j % 4 with step j; slots past the token range are empty
+    // resources whose loads only write zeros, which keeps every slot at 8 loads for the waits.
+    lds_char *const lsm = (lds_char *)smem;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    BwdDma pa, pb;
+    pa.init(K, k0, wave_u, lane);
+    pb.init(N, n0, wave_u, lane);
+    const int64_t nk = t_end > t_begin ? (t_end - t_begin + kBwdStep - 1) / kBwdStep : 0;
+#pragma unroll
+    for (int s0 = 0; s0 < kBwdStages - 1; s0++) {
+        const int64_t t0 = t_begin + s0 * kBwdStep;
+        const __amdgpu_buffer_rsrc_t ra = BwdDma::step_rsrc(X, K, t0, t_end), rb = BwdDma::step_rsrc(dY, N, t0, t_end);
+        lds_char *st = lsm + s0 * kBwdStageBytes;
+#pragma unroll
+        for (int i = 0; i < 4; i++) pa.issue_one(ra, st, wave_u, i);
+#pragma unroll
+        for (int i = 0; i < 4; i++) pb.issue_one(rb, st + kBwdOpBytes, wave_u, i);
+    }
+    uint32_t a_off[4], b_off[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        a_off[i] = tr_lane_off(wm * 128 + i * 32, lane);
+        b_off[i] = tr_lane_off(wn * 128 + i * 32, lane);
+    }
+    const uint32_t lds0 = lds_addr(smem);
+    FOCUS_WAIT_VMCNT(8);
+    asm volatile("s_barrier" ::: "memory");
+    Frags f, g;
+    load_frags_tr<0>(f, lds0, a_off, b_off);
+    for (int64_t kt = 0; kt < nk; kt++) {
+        FOCUS_WAIT_VMCNT(8);
+        asm volatile("s_barrier" ::: "memory");
+        const uint32_t cur = lds0 + (uint32_t)(kt & 3) * kBwdStageBytes;
+        const uint32_t nxt = lds0 + (uint32_t)((kt + 1) & 3) * kBwdStageBytes;
+        const int64_t t0 = t_begin + (kt + 3) * kBwdStep;
+        const __amdgpu_buffer_rsrc_t ra = BwdDma::step_rsrc(X, K, t0, t_end), rb = BwdDma::step_rsrc(dY, N, t0, t_end);
+        lds_char *st = lsm + (int)((kt + 3) & 3) * kBwdStageBytes;
+        tr_wait(f);  // f (read during the previous step's second half) has landed
+        load_frags_tr<1>(g, cur, a_off, b_off);
+        // the 8 loads of slot kt + 3 go out one after every second MFMA (see the forward kernel)
+        static_for<16>([&](auto idx) {
+            constexpr int i = idx / 4, jj = idx % 4;
+            acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[jj], acc[i][jj], 0, 0, 0);
+            if constexpr (idx % 2 == 1) {
+                __builtin_amdgcn_sched_barrier(0);
+                if constexpr (idx / 2 < 4) pa.issue_one(ra, st, wave_u, idx / 2);
+                else pb.issue_one(rb, st + kBwdOpBytes, wave_u, idx / 2 - 4);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        });
+        tr_wait(g);  // read before the first half's MFMAs, long landed
+        load_frags_tr<0>(f, nxt, a_off, b_off);
+        mma_frags(g, acc);
+    }
+    tr_wait(f);  // no read may still be in flight when the workgroup ends
+    // the empty slots' zero writes must land before the workgroup's LDS is handed on
+    FOCUS_WAIT_VMCNT(0);
+    ste_epilogue<FMT, WDT>(acc, k0, n0, split, N, K, W, s_fp, c, sb_log2, alpha_ptr, ste_clip, e8m0_floor, part_s,
+                           part_c, flag, wm, wn, lane);
+}
+
+// ------------------------------------------------------------------------------------------------
+// Backward reconstruction GEMM with X_hat given as packed MXFP4 (codes [M][K / 2], even k in the low
+// nibble, and E8M0 bytes block-major [K / 32][M], the arrays focus_fakequant_fwd writes). Under
+// MXFP4 X_hat is exactly an E2M1 code times its block's power of two (Eq. 1, 3), so the bf16 operand
+// is rebuilt in LDS without loss, reading a quarter of the bytes of the bf16 X_hat. Same tile, MFMA
+// and fused epilogue as bwd_mfma_kernel.
+//
+// Per 32-token step a DMA slot brings the dY tile (16 KB, the bf16 kernel's token-major layout), the
+// step's codes ([32 tokens][128 bytes]) and its scale bytes ([8 blocks][32 tokens], one copy per
+// wave so that every thread issues the same number of loads). Three steps after a slot's loads are
+// issued, each thread converts one token's 32 codes of one block (16 bytes, one scale) into 32 bf16
+// with the scaled FP4 conversion and writes them into one of three bf16 A stages, in the layout the
+// transposing fragment reads expect. Step kt issues slot kt + 4, converts slot kt + 2 and multiplies
+// step kt: 5 DMA stages + 3 A stages = 153 KB of LDS.
+constexpr int kMxDmaStages = 5;
+constexpr int kMxCodeOff = kBwdOpBytes;            // codes after the dY tile
+constexpr int kMxScaleOff = kMxCodeOff + 32 * 128; // then 4 per-wave copies of the scale bytes
+constexpr int kMxDmaStageBytes = kMxScaleOff + 4 * 256;
+constexpr int kMxAStages = 3;
+constexpr int kMxAOff = kMxDmaStages * kMxDmaStageBytes;
+constexpr int kMxLdsBytes = kMxAOff + kMxAStages * kBwdOpBytes;
+constexpr int kMxLoads = 6;  // loads per slot per thread: dY 4, codes 1, scales 1
+static_assert(kMxLdsBytes <= kLdsBytes, "MXFP4 backward stages fit the LDS");
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+template <int OFF>
+__device__ __forceinline__ u32x4_t ds_read_b128(uint32_t addr) {
+    u32x4_t r;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+
+template <int OFF>
+__device__ __forceinline__ uint32_t ds_read_u8(uint32_t addr) {
+    uint32_t r;
+    asm volatile("ds_read_u8 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+
+__device__ __forceinline__ void ds_write_b128(uint32_t addr, u32x4_t v) {
+    asm volatile("ds_write_b128 %0, %1" : : "v"(addr), "v"(v) : "memory");
+}
+
+// Waits until at most N LDS operations of this wave are in flight; the values read by the earlier
+// ones are passed through so that no consumer is scheduled above the wait.
+template <int N>
+__device__ __forceinline__ void lds_wait(u32x4_t &a, uint32_t &b) {
+    static_assert(N >= 0 && N < 16, "lgkmcnt is a 4-bit field");
+    asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "i"(N));
+}
+
+// Byte offset of (token row r, column c) in an A stage of the MXFP4 backward: the bf16 kernel's
+// token-major layout with one more xor on the 16-byte chunk index, by its 32-column block b:
+// (b ^ b / 4) % 4. Within a block that is a fixed permutation of its 4 chunks, so the transposing
+// fragment reads stay conflict-free; the conversion's 16-byte writes (8 lanes of one row, blocks
+// 0-7, the same chunk of each block) then fall on 8 distinct 16-byte bank groups instead of 2.
+__device__ __forceinline__ uint32_t mx_a_off(uint32_t r, uint32_t c) {
+    const uint32_t ch = c >> 3, b = ch >> 2;
+    return r * (uint32_t)kBwdRowBytes + ((ch ^ ((r & 3u) << 2) ^ ((b ^ (b >> 2)) & 3u)) << 4) + (c & 7u) * 2u;
+}
+
+// tr_lane_off for the A stages of the MXFP4 backward
+__device__ __forceinline__ uint32_t mx_tr_lane_off(uint32_t c, int lane) {
+    const uint32_t j = lane & 15;
+    const uint32_t cc = c + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+    const uint32_t r = 8 * (lane >> 5) + (j >> 2);
+    return mx_a_off(r, cc);
+}
+
+// a buffer resource of `bytes` (< 2^31) bytes
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc_u32(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kRsrcWord3);
+}
+
+// buffer resources of one DMA slot of the MXFP4 backward
+struct MxSlot {
+    __amdgpu_buffer_rsrc_t rd, rc, rs;  // dY rows, code rows, scale bytes
+    uint32_t t0;                        // the slot's first token
+};
+
+template <int WDT>
+__global__ void __launch_bounds__(kThreads, 1)
+bwd_mfma_mx_kernel(const uint16_t *__restrict__ dY, const uint8_t *__restrict__ Xc, const uint8_t *__restrict__ Xs,
+                   int64_t M, int64_t N, int64_t K, int64_t chunk, const void *__restrict__ W,
+                   const float *__restrict__ s_fp, const float *__restrict__ c, int sb_log2, int ste_clip,
+                   int e8m0_floor, float *__restrict__ part_s, float *__restrict__ part_c, uint32_t *flag,
+                   int tiles_n) {
+    __shared__ __attribute__((aligned(16))) char smem[kMxLdsBytes];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
+    const uint32_t id = xcd_tile(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
+    uint32_t tk, tn;
+    grouped_tile(id % gridDim.x, gridDim.x / tiles_n, tiles_n, tk, tn);
+    const int64_t k0 = (int64_t)tk * kTile, n0 = (int64_t)tn * kTile;
+    const int64_t split = id / gridDim.x;
+    const int64_t t_begin = split * chunk, t_end = std::min<int64_t>(M, t_begin + chunk);
+
+    f32x16_t acc[4][4];
+    const f32x16_t zero = {};
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) acc[i][j] = zero;
+
+    lds_char *const lsm = (lds_char *)smem;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    BwdDma pb;
+    pb.init(N, n0, wave_u, lane);
+    const int64_t kc = K / 2;  // code bytes per token row
+    // this lane's code chunk: token row 8 wave + lane / 8 of the step, 16 bytes = block lane % 8 of the tile
+    const uint32_t c_row = 8u * wave_u + ((uint32_t)lane >> 3), c_blk = (uint32_t)lane & 7u;
+    const uint32_t c_col = (uint32_t)(k0 / 2) + 16u * c_blk;
+    const uint32_t c_off = (c_row * (uint32_t)kc + c_col) | ((uint32_t)((int32_t)kc - 1 - (int32_t)c_col) >> 31 << 31);
+    // this lane's 4 scale bytes: block lane / 8 of the tile, tokens 4 (lane % 8) .. + 3 of the step
+    const uint32_t s_blk = (uint32_t)(k0 / 32) + ((uint32_t)lane >> 3);
+    const uint32_t s_bad = (uint32_t)((int32_t)(K / 32) - 1 - (int32_t)s_blk) >> 31 << 31;
+    const uint32_t s_off = s_blk * (uint32_t)M + 4u * ((uint32_t)lane & 7u);
+    const __amdgpu_buffer_rsrc_t rs_all = make_rsrc(Xs, (K / 32) * M), rs_none = make_rsrc(Xs, 0);
+    const int64_t nk = t_end > t_begin ? (t_end - t_begin + kBwdStep - 1) / kBwdStep : 0;
+
+    // The resources of the slot whose first token is t: the dY rows and code rows of its 32 tokens
+    // (rows past the token range read as zeros; a slot past the range has empty resources, whose
+    // loads write zeros) and the scale bytes (all blocks; offsets carry the slot's first token).
+    auto slot_at = [&](int64_t t) {
+        MxSlot sl;
+        const int64_t rem = t_end - t;
+        const uint32_t rows = rem <= 0 ? 0u : (rem < kBwdStep ? (uint32_t)rem : (uint32_t)kBwdStep);
+        sl.rd = make_rsrc_u32(dY + t * N, rows * (uint32_t)N * 2u);
+        sl.rc = make_rsrc_u32(Xc + t * kc, rows * (uint32_t)kc);
+        sl.rs = rows ? rs_all : rs_none;
+        sl.t0 = (uint32_t)t;
+        return sl;
+    };
+    // load i (0..5) of a slot into the DMA stage at st: 0-3 the dY tile, 4 the codes, 5 the scale bytes
+    auto issue = [&](lds_char *st, const MxSlot &sl, int i) {
+        if (i < 4) {
+            pb.issue_one(sl.rd, st, wave_u, i);
+        } else if (i == 4) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(sl.rc, st + kMxCodeOff + wave_u * 1024, 16, (int)c_off, 0, 0, 0);
+        } else {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(sl.rs, st + kMxScaleOff + wave_u * 256, 4,
+                                                     (int)((s_off + sl.t0) | s_bad), 0, 0, 0);
+        }
+    };
+    const uint32_t lds0 = lds_addr(smem);
+    // conversion: this thread's 16 code bytes and scale byte of a DMA stage, 32 bf16 into an A stage
+    const uint32_t cv_code = (uint32_t)kMxCodeOff + (uint32_t)wave_u * 1024u + 16u * (uint32_t)lane;
+    const uint32_t cv_scale = (uint32_t)kMxScaleOff + (uint32_t)wave_u * 256u + 32u * c_blk + c_row;
+    // write j: chunk j (k 8 j .. 8 j + 7) of this thread's block
+    uint32_t cv_dst[4];
+#pragma unroll
+    for (int j = 0; j < 4; j++) cv_dst[j] = mx_a_off(c_row, 8u * (4u * c_blk + j));
+    auto cvt_chunk = [&](uint32_t word, float sc, uint32_t dst) {
+        u32x4_t v;
+        v.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, sc, 0));
+        v.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, sc, 1));
+        v.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, sc, 2));
+        v.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, sc, 3));
+        ds_write_b128(dst, v);
+    };
+    auto scale_of = [](uint32_t byte) { return exp2i((int)(byte & 0xFFu) - 127); };
+    auto d_addr = [&](int i) { return lds0 + (uint32_t)(i * kMxDmaStageBytes); };
+    auto a_addr = [&](int i) { return lds0 + (uint32_t)(kMxAOff + i * kBwdOpBytes); };
+
+    // prologue: slots 0-3 in flight, slots 0 and 1 converted into A stages 0 and 1
+#pragma unroll
+    for (int s0 = 0; s0 < 4; s0++) {
+        const MxSlot sl = slot_at(t_begin + s0 * kBwdStep);
+#pragma unroll
+        for (int i = 0; i < kMxLoads; i++) issue(lsm + s0 * kMxDmaStageBytes, sl, i);
+    }
+    FOCUS_WAIT_VMCNT(2 * kMxLoads);
+    asm volatile("s_barrier" ::: "memory");
+#pragma unroll
+    for (int s0 = 0; s0 < 2; s0++) {
+        u32x4_t w = ds_read_b128<0>(d_addr(s0) + cv_code);
+        uint32_t sb = ds_read_u8<0>(d_addr(s0) + cv_scale);
+        lds_wait<0>(w, sb);
+        const float sc = scale_of(sb);
+        cvt_chunk(w.x, sc, a_addr(s0) + cv_dst[0]);
+        cvt_chunk(w.y, sc, a_addr(s0) + cv_dst[1]);
+        cvt_chunk(w.z, sc, a_addr(s0) + cv_dst[2]);
+        cvt_chunk(w.w, sc, a_addr(s0) + cv_dst[3]);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+    uint32_t a_off[4], b_off[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        a_off[i] = mx_tr_lane_off(wm * 128 + i * 32, lane);
+        b_off[i] = tr_lane_off(wn * 128 + i * 32, lane);  // the dY tile opens its DMA stage
+    }
+    // A fragments live in an A stage, B fragments in a DMA stage: one base per operand
+    auto frags = [&](auto ks, Frags &fr, uint32_t abase, uint32_t bbase) {
+        constexpr int kRow = decltype(ks)::value * 16 * kBwdRowBytes;
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            const i16x4_t a_lo = ds_read_tr<kRow>(abase + a_off[i]);
+            const i16x4_t a_hi = ds_read_tr<kRow + 4 * kBwdRowBytes>(abase + a_off[i]);
+            const i16x4_t b_lo = ds_read_tr<kRow>(bbase + b_off[i]);
+            const i16x4_t b_hi = ds_read_tr<kRow + 4 * kBwdRowBytes>(bbase + b_off[i]);
+            const i16x4_t va[2] = {a_lo, a_hi}, vb[2] = {b_lo, b_hi};
+            fr.a[i] = __builtin_bit_cast(bf16x8_t, va);
+            fr.b[i] = __builtin_bit_cast(bf16x8_t, vb);
+        }
+    };
+    // LDS offsets of the stages, rotated each step (no divisions in the loop): DMA stages of slots kt,
+    // kt + 2 and kt + 4, A stages of steps kt and kt + 2
+    uint32_t o_cur = 0, o_cv = 2 * kMxDmaStageBytes, o_is = 4 * kMxDmaStageBytes;
+    uint32_t a_cur = kMxAOff, a_cv = kMxAOff + 2 * kBwdOpBytes;
+    auto next_d = [](uint32_t o) { return o == (kMxDmaStages - 1) * kMxDmaStageBytes ? 0u : o + kMxDmaStageBytes; };
+    auto next_a = [](uint32_t o) {
+        return o == kMxAOff + (kMxAStages - 1) * kBwdOpBytes ? (uint32_t)kMxAOff : o + kBwdOpBytes;
+    };
+    int64_t t_is = t_begin + 4 * kBwdStep;  // first token of slot kt + 4
+    Frags f, g;
+    frags(std::integral_constant<int, 0>{}, f, a_addr(0), d_addr(0));
+    for (int64_t kt = 0; kt < nk; kt++, t_is += kBwdStep) {
+        const MxSlot sl = slot_at(t_is);
+        lds_char *st = lsm + o_is;
+        const uint32_t cds = lds0 + o_cv, cas = lds0 + a_cv;
+        // this thread's loads of slot kt + 2 have landed (slot kt + 3 may be in flight); after the
+        // barrier everyone's have, and every wave is done with step kt - 1's stages
+        FOCUS_WAIT_VMCNT(kMxLoads);
+        asm volatile("s_barrier" ::: "memory");
+        tr_wait(f);
+        // the conversion's two reads go first, then the 16 fragment reads of the second half: LDS
+        // operations complete in order, so lgkmcnt(15) means the first two have
+        u32x4_t w = ds_read_b128<0>(cds + cv_code);
+        uint32_t sb = ds_read_u8<0>(cds + cv_scale);
+        frags(std::integral_constant<int, 1>{}, g, lds0 + a_cur, lds0 + o_cur);
+        float sc = 0.0f;
+        static_for<16>([&](auto idx) {
+            constexpr int i = idx / 4, jj = idx % 4;
+            acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[jj], acc[i][jj], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            // slot kt + 4: one load after every second MFMA; the conversion of slot kt + 2 after
+            // MFMAs 4, 6, 8, 10 (one 16-byte chunk each), starting with the wait for its reads
+            if constexpr (idx % 2 == 1 && idx / 2 < kMxLoads) issue(st, sl, idx / 2);
+            if constexpr (idx == 4) {
+                lds_wait<15>(w, sb);
+                sc = scale_of(sb);
+            }
+            if constexpr (idx >= 4 && idx <= 10 && idx % 2 == 0) {
+                constexpr int ch = (idx - 4) / 2;
+                cvt_chunk(w[ch], sc, cas + cv_dst[ch]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        });
+        o_cur = next_d(o_cur), o_cv = next_d(o_cv), o_is = next_d(o_is);
+        a_cur = next_a(a_cur), a_cv = next_a(a_cv);
+        tr_wait(g);  // also covers the conversion's writes, before the barrier that publishes them
+        frags(std::integral_constant<int, 0>{}, f, lds0 + a_cur, lds0 + o_cur);  // step kt + 1's stages
+        mma_frags(g, acc);
+    }
+    tr_wait(f);  // no read may still be in flight when the workgroup ends
+    FOCUS_WAIT_VMCNT(0);
+    ste_epilogue<kFmtMX, WDT>(acc, k0, n0, split, N, K, W, s_fp, c, sb_log2, nullptr, ste_clip, e8m0_floor, part_s,
+                              part_c, flag, wm, wn, lane);
+}
+
 // ================================================================================================
 
 // Buffer offsets are 32-bit: a tile's rows must span less than 2^31 bytes.
@@ -791,6 +1063,31 @@ hipError_t launch_fwd_mfma_mx(const void *Xc, const void *Xs, const void *Wc, co
     uint16_t *d = static_cast<uint16_t *>(dY);
     if (Yref) fwd_mfma_kernel<true, true><<<grid, kThreads, 0, st>>>(Xc, Wc, xs, ws, M, N, K, y, d, dscale, colpart, tiles_n);
     else fwd_mfma_kernel<false, true><<<grid, kThreads, 0, st>>>(Xc, Wc, xs, ws, M, N, K, y, d, dscale, colpart, tiles_n);
+    return hipGetLastError();
+}
+
+bool mfma_bwd_mx_supported(int64_t M, int64_t N, int64_t K) {
+    return N > 0 && K > 0 && M >= 0 && N % 8 == 0 && K % 32 == 0 && M % 4 == 0 &&
+           int64_t(kBwdStep) * N * 2 < (int64_t(1) << 31) && (K / 32) * M < (int64_t(1) << 31) - 64 &&
+           int64_t(kTile) * K * 4 < (int64_t(1) << 31);
+}
+
+hipError_t launch_bwd_mfma_mx(int w_dt, const void *dY, const void *Xc, const void *Xs, int64_t M, int64_t N,
+                              int64_t K, int64_t chunk, int64_t splits, const void *W, const float *s_fp,
+                              const float *c, int sb, int ste_clip, int e8m0_floor, float *part_s, float *part_c,
+                              uint32_t *flag, hipStream_t st) {
+    const int tiles_k = (int)((K + kTile - 1) / kTile), tiles_n = (int)((N + kTile - 1) / kTile);
+    int sbl = 0;
+    while ((1 << sbl) < sb) sbl++;
+    const dim3 grid((unsigned)tiles_k * tiles_n, (unsigned)splits);
+    const uint16_t *dy = static_cast<const uint16_t *>(dY);
+    const uint8_t *xc = static_cast<const uint8_t *>(Xc), *xs = static_cast<const uint8_t *>(Xs);
+    if (w_dt == kBF16)
+        bwd_mfma_mx_kernel<kBF16><<<grid, kThreads, 0, st>>>(dy, xc, xs, M, N, K, chunk, W, s_fp, c, sbl, ste_clip,
+                                                             e8m0_floor, part_s, part_c, flag, tiles_n);
+    else
+        bwd_mfma_mx_kernel<kF32><<<grid, kThreads, 0, st>>>(dy, xc, xs, M, N, K, chunk, W, s_fp, c, sbl, ste_clip,
+                                                            e8m0_floor, part_s, part_c, flag, tiles_n);
     return hipGetLastError();
 }
 

@@ -59,6 +59,12 @@ hipError_t launch_recon_bwd(const BwdPlan &p, int op_dt, int fmt, int sb, int st
                             const float *s_fp, const float *c, const float *alpha, float *grad_s,
                             float *grad_c, float *G_out, void *ws, uint32_t *flag, hipStream_t st);
 
+// the backward from X_hat as packed MXFP4 (MFMA path only; the plan is that of the bf16 operands)
+hipError_t launch_recon_bwd_mx(const BwdPlan &p, int sb, int ste_clip, int e8m0_floor, const void *dY, const void *Xc,
+                               const void *Xs, int64_t M, int64_t N, int64_t K, const void *W, int w_dt,
+                               const float *s_fp, const float *c, float *grad_s, float *grad_c, void *ws,
+                               uint32_t *flag, hipStream_t st);
+
 hipError_t launch_fq_act_bwd(int fmt, int in_dt, int g_dt, const void *X, int64_t rows, int64_t K, int e8m0_floor,
                              int ste_clip, const void *dX_hat, void *dX, float *partial, hipStream_t st);
 hipError_t launch_zero_fill(void *p, size_t bytes, hipStream_t st);

@@ -22,9 +22,9 @@ CALL_RECON_GEMM_DX, CALL_FAKEQUANT_ACT_BWD, CALL_KL_TOP = 7, 8, 9
 OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_CONFIG, ERR_WORKSPACE, ERR_DOMAIN, ERR_HIP = range(8)
 
 EXPORTED = ("focus_workspace_size", "focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd",
-            "focus_recon_gemm_fwd", "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd", "focus_export_packed",
-            "focus_recon_gemm_dx", "focus_fakequant_act_bwd", "focus_kl_top", "focus_adamw_step",
-            "focus_check_flags", "focus_status_string")
+            "focus_recon_gemm_fwd", "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd",
+            "focus_recon_gemm_bwd_mxfp4", "focus_export_packed", "focus_recon_gemm_dx", "focus_fakequant_act_bwd",
+            "focus_kl_top", "focus_adamw_step", "focus_check_flags", "focus_status_string")
 
 
 class QConfig(ctypes.Structure):
@@ -63,6 +63,7 @@ def lib() -> ctypes.CDLL:
         L.focus_recon_gemm_fwd.argtypes = [p, p, i32, i64, i64, i64, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_fwd_mxfp4.argtypes = [p, p, p, p, i64, i64, i64, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_bwd.argtypes = [q, p, p, i32, i64, i64, i64, p, i32, p, p, p, p, p, p, p, sz, p]
+        L.focus_recon_gemm_bwd_mxfp4.argtypes = [q, p, p, p, i64, i64, i64, p, i32, p, p, p, p, p, sz, p]
         L.focus_export_packed.argtypes = [q, p, i32, i64, i64, p, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_dx.argtypes = [p, p, i32, i64, i64, i64, p, p, sz, p]
         L.focus_fakequant_act_bwd.argtypes = [q, p, i32, i64, i64, p, i32, p, p, sz, p]
@@ -72,8 +73,8 @@ def lib() -> ctypes.CDLL:
         L.focus_status_string.argtypes = [i32]
         L.focus_status_string.restype = ctypes.c_char_p
         for name in ("focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd", "focus_recon_gemm_fwd",
-                     "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd", "focus_export_packed",
-                     "focus_adamw_step", "focus_check_flags", "focus_recon_gemm_dx", "focus_fakequant_act_bwd",
+                     "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd", "focus_recon_gemm_bwd_mxfp4",
+                     "focus_export_packed", "focus_adamw_step", "focus_check_flags", "focus_recon_gemm_dx", "focus_fakequant_act_bwd",
                      "focus_kl_top"):
             getattr(L, name).restype = ctypes.c_int
         _LIB = L
@@ -159,16 +160,19 @@ def scales_init(W: torch.Tensor, fmt: int, sub_block: int, ws=None, out=None, e8
 def fakequant_fwd(X: torch.Tensor, fmt: int, sub_block: int = 8, s_fp=None, c=None, alpha=None,
                   out_dtype=None, want_codes: bool = False, want_scale_bytes: bool = False,
                   want_alpha: bool = False, ste_clip: int = 1, ws=None, out=None, codes_out=None,
-                  scales_out=None, scale_layout: int = SCALES_ROW_MAJOR, e8m0_rounding: int = 0):
+                  scales_out=None, scale_layout: int = SCALES_ROW_MAJOR, e8m0_rounding: int = 0,
+                  want_x_hat: bool = True):
     """Fake quantisation forward. Weight mode when s_fp is given, dynamic activation mode otherwise.
     codes_out / scales_out: preallocated code and scale-byte outputs (they imply want_codes /
     want_scale_bytes). scale_layout: [rows][K/B] (row-major) or [K/B][rows] (block-major).
+    want_x_hat=False (with codes) writes the packed form only.
 
-    Returns (x_hat, packed_codes or None, scale_bytes or None, alpha_x or None)."""
+    Returns (x_hat or None, packed_codes or None, scale_bytes or None, alpha_x or None)."""
     rows, K = X.shape
     q = qconfig(fmt, sub_block, ste_clip, scale_layout, e8m0_rounding)
     out_dtype = out_dtype or X.dtype
-    x_hat = out if out is not None else torch.empty(rows, K, dtype=out_dtype, device=X.device)
+    x_hat = out if out is not None else (torch.empty(rows, K, dtype=out_dtype, device=X.device) if want_x_hat
+                                         else None)
     codes = codes_out
     if codes is None and want_codes:
         codes = torch.empty(rows, K // 2, dtype=torch.uint8, device=X.device)
@@ -179,7 +183,8 @@ def fakequant_fwd(X: torch.Tensor, fmt: int, sub_block: int = 8, s_fp=None, c=No
     alpha_out = torch.empty(1, dtype=torch.float32, device=X.device) if want_alpha else None
     ws = _ws(ws, CALL_FAKEQUANT_FWD, q, 0, rows, K, X.device)
     _check(lib().focus_fakequant_fwd(ctypes.byref(q), _ptr(X), _dt(X), rows, K, _ptr(s_fp), _ptr(c), _ptr(alpha),
-                                     _ptr(x_hat), _dt(x_hat), _ptr(codes), _ptr(sbytes), _ptr(alpha_out),
+                                     _ptr(x_hat), _dt(x_hat) if x_hat is not None else _dt(X), _ptr(codes),
+                                     _ptr(sbytes), _ptr(alpha_out),
                                      _ptr(ws), ws.numel(), _stream()), "focus_fakequant_fwd")
     return x_hat, codes, sbytes, alpha_out
 
@@ -254,6 +259,25 @@ def recon_gemm_bwd(dY: torch.Tensor, X_hat: torch.Tensor, W: torch.Tensor, fmt: 
                                       _dt(W), _ptr(s_fp), _ptr(c), _ptr(alpha), _ptr(grad_s), _ptr(grad_c),
                                       _ptr(G), _ptr(ws), ws.numel(), _stream()), "focus_recon_gemm_bwd")
     return grad_s, grad_c, G
+
+
+def recon_gemm_bwd_mxfp4(dY: torch.Tensor, X_codes: torch.Tensor, X_scales: torch.Tensor, W: torch.Tensor,
+                         sub_block: int, s_fp, c=None, ste_clip: int = 1, ws=None, out=None, e8m0_rounding: int = 0):
+    """Fused backward with X_hat as packed MXFP4 (codes [M][K/2], block-major E8M0 bytes [K/32][M])
+    -> (grad_s, grad_c)."""
+    M, K = X_codes.shape[0], X_codes.shape[1] * 2
+    N = W.shape[0]
+    q = qconfig(MXFP4, sub_block, ste_clip, SCALES_ROW_MAJOR, e8m0_rounding)
+    if out is None:
+        grad_s = torch.empty(N, K // 32, dtype=torch.float32, device=W.device)
+        grad_c = torch.empty(N, K // sub_block, dtype=torch.float32, device=W.device)
+    else:
+        grad_s, grad_c = out
+    ws = _ws(ws, CALL_RECON_GEMM_BWD, q, M, N, K, W.device)
+    _check(lib().focus_recon_gemm_bwd_mxfp4(ctypes.byref(q), _ptr(dY), _ptr(X_codes), _ptr(X_scales), M, N, K,
+                                            _ptr(W), _dt(W), _ptr(s_fp), _ptr(c), _ptr(grad_s), _ptr(grad_c),
+                                            _ptr(ws), ws.numel(), _stream()), "focus_recon_gemm_bwd_mxfp4")
+    return grad_s, grad_c
 
 
 def export_packed(W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha=None, ws=None, out=None,

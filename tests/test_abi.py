@@ -81,6 +81,9 @@ def test_argument_checks(L, cpu_only):
     assert fq_fwd(L, focus.QConfig(0, 8, 1, 0, 2)) == focus.ERR_CONFIG  # no such E8M0 rounding
     assert fq_fwd(L, focus.QConfig(1, 8, 1, 0, 1), K=64) == focus.ERR_CONFIG  # floor E8M0 is MXFP4 only
     assert fq_fwd(L, mx, X=None) == focus.ERR_NULL
+    # X_hat may be left out only when the codes are asked for
+    assert L.focus_fakequant_fwd(ctypes.byref(mx), BOGUS, 1, 4, 64, None, None, None, None, 1, None, BOGUS, None,
+                                 BOGUS, 1 << 20, None) == focus.ERR_NULL
     assert fq_fwd(L, mx, x_dt=7) == focus.ERR_DTYPE
     assert fq_fwd(L, mx, K=48) == focus.ERR_SHAPE          # not a multiple of 32
     assert fq_fwd(L, mx, rows=-1) == focus.ERR_SHAPE
@@ -121,6 +124,19 @@ def test_argument_checks(L, cpu_only):
                1 << 30, None) == focus.ERR_SHAPE  # scale bytes not 4-byte aligned
     assert mxf(BOGUS, BOGUS, BOGUS, BOGUS, 8, 8, 128, None, BOGUS, None, None, BOGUS, 16,
                None) == focus.ERR_WORKSPACE
+    # fused backward from packed MXFP4 activations
+    mxb = L.focus_recon_gemm_bwd_mxfp4
+    def bwd_mx(q, M=8, N=8, K=64, scales=BOGUS, ws_bytes=1 << 30, w_dt=1):
+        return mxb(ctypes.byref(q), BOGUS, BOGUS, scales, M, N, K, BOGUS, w_dt, BOGUS, None, BOGUS, BOGUS, BOGUS,
+                   ws_bytes, None)
+    assert bwd_mx(nv) == focus.ERR_CONFIG                   # MXFP4 only
+    assert bwd_mx(mx, K=48) == focus.ERR_SHAPE               # K not a multiple of 32
+    assert bwd_mx(mx, N=12) == focus.ERR_SHAPE               # N not a multiple of 8
+    assert bwd_mx(mx, M=6) == focus.ERR_SHAPE                # M not a multiple of 4
+    assert bwd_mx(mx, scales=None) == focus.ERR_NULL
+    assert bwd_mx(mx, scales=ctypes.c_void_p((1 << 20) + 2)) == focus.ERR_SHAPE  # scale bytes not 4-byte aligned
+    assert bwd_mx(mx, w_dt=5) == focus.ERR_DTYPE
+    assert bwd_mx(mx, ws_bytes=16) == focus.ERR_WORKSPACE
     # export and init
     assert L.focus_export_packed(ctypes.byref(mx), BOGUS, 1, 4, 64, BOGUS, None, None, None, BOGUS, BOGUS,
                                  1 << 20, None) == focus.ERR_NULL
