@@ -26,6 +26,12 @@ PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 
 def parse():
     p = argparse.ArgumentParser()
+    p.add_argument("--summarize-trace", metavar="DIR",
+                   help="write profiles/ summaries from a rocprofv3 --kernel-trace --stats output directory and exit")
+    p.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="write profiles/traffic.json and the HBM traffic summary from the two rocprofv3 --pmc "
+                        "output directories (FETCH_SIZE, WRITE_SIZE) of a --steps 1 --warmup 0 "
+                        "--copy-calibration run and exit")
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
@@ -95,6 +101,12 @@ def traffic_from_profile(kernel: str, src_hash: str):
 
 def main():
     args = parse()
+    if args.summarize_trace or args.summarize_counters:
+        if args.summarize_trace:
+            summarize_trace(args.summarize_trace, args.workload)
+        if args.summarize_counters:
+            summarize_counters(*args.summarize_counters, args.workload)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the data-parallel path across GPUs is not built "
               f"(asked for --gpus {args.gpus})", file=sys.stderr)
@@ -473,6 +485,95 @@ def cpu_baseline(w, sample_tokens, sample_rows):
     return {"value": round(full_ms, 1), "unit": "ms per step", "cores": threads, "kind": "oracle",
             "sample": f"{Ms} of {w.M} tokens per input; {sample_rows} weight rows per linear "
                       f"({sample_s:.1f} s measured), extrapolated linearly to the full step"}
+
+
+# ---- rocprofv3 summaries (host only) ------------------------------------------------------------
+# Library kernels by the name bench.py reports them under, and the rocprofv3 name prefix of each.
+PROFILED = {"bwd_mfma_mx_kernel": "void focus::bwd_mfma_mx_kernel<",
+            "fwd_mfma_kernel_mx": "void focus::fwd_mfma_kernel<true, true>",
+            "fwd_mfma_kernel": "void focus::fwd_mfma_kernel<true, false>",
+            "bwd_mfma_kernel": "void focus::bwd_mfma_kernel<"}
+TRACE_CMD = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof_trace -o run --output-format csv -- "
+             "python3 -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration")
+PMC_CMD = ("rocprofv3 --pmc {c} -d gpurun_out/prof_{d} -o run --output-format csv -- "
+           "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --copy-calibration")
+
+
+def algorithmic_bytes(kernel, M, N, K, sb):
+    """Bytes each input is read and each output written once, per launch (one linear)."""
+    grads = N * K // 32 * 4 + N * K // sb * 4
+    wparams = 2 * N * K + N * K // 32 * 4 + N * K // sb * 4
+    return {"fwd_mfma_kernel": 2 * M * K + 2 * N * K + 4 * M * N,
+            "fwd_mfma_kernel_mx": (M + N) * (K // 2 + K // 32) + 4 * M * N,
+            "bwd_mfma_kernel": 2 * M * N + 2 * M * K + wparams + grads,
+            "bwd_mfma_mx_kernel": 2 * M * N + M * (K // 2 + K // 32) + wparams + grads}[kernel]
+
+
+def summarize_trace(trace_dir, workload):
+    import csv
+    rows = [r for r in csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv")))
+            if "focus::" in r["Name"]]
+    out = os.path.join(REPO, "profiles", f"step_{workload.replace('_mxfp4', '')}_{workload.split('_')[-1]}_kernel_stats.md")
+    with open(out, "w") as f:
+        f.write(f"# Kernel-trace summary: scale-learning steps of the {workload} workload\n\n")
+        f.write("Command (from the repository root on one MI355X):\n\n    " + TRACE_CMD + "\n\n")
+        f.write("The run times the default step (2 warm-up + 5 timed) and then the same step with the other forward and "
+                "backward operands, and the calls outside the step (chaining, AdamW, export); library kernels only, "
+                f"source hash `{kernel_source_hash()}`:\n\n")
+        f.write("| Kernel | Calls | Avg us | Min us | Max us | Share of GPU time |\n|---|---|---|---|---|---|\n")
+        for r in rows:
+            name = r["Name"].replace("(anonymous namespace)::", "").split("(")[0].replace("void ", "")
+            f.write(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | {float(r['MinNs']) / 1e3:.1f} | "
+                    f"{float(r['MaxNs']) / 1e3:.1f} | {float(r['Percentage']):.2f}% |\n")
+    print(out)
+
+
+def summarize_counters(fetch_dir, write_dir, workload):
+    import csv
+
+    from paper_2608_01847_amd import synth
+    w = synth.WORKLOADS[workload]
+    runs = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = [r for r in csv.DictReader(open(os.path.join(d, "run_counter_collection.csv")))
+                if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        # the untimed 1 GiB device copy of --copy-calibration is the run's first copy kernel
+        copy = next(r for r in rows if "copyBuffer" in r["Kernel_Name"])
+        scale = (1 << 30) / (float(copy["Counter_Value"]) * 1024)
+        per = {k: [float(r["Counter_Value"]) * 1024 * scale for r in rows if r["Kernel_Name"].startswith(pre)][:len(w.linears)]
+               for k, pre in PROFILED.items()}
+        runs[counter] = (scale, per, float(copy["Counter_Value"]))
+    fscale, fetch, fraw = runs["FETCH_SIZE"]
+    wscale, write, wraw = runs["WRITE_SIZE"]
+    src = kernel_source_hash()
+    data = {"_calibration": {"copy_bytes": 1 << 30, "fetch_scale": fscale, "write_scale": wscale,
+                             "note": "scales = known bytes of a 1 GiB device copy / what FETCH_SIZE and WRITE_SIZE "
+                                     "read for it"}}
+    md = [f"# HBM-side traffic of the reconstruction GEMMs ({workload}, {w.M:,} tokens)\n",
+          "Commands (one counter per run, from the repository root on one MI355X):\n",
+          "    " + PMC_CMD.format(c="FETCH_SIZE", d="fetch"), "    " + PMC_CMD.format(c="WRITE_SIZE", d="write") + "\n",
+          f"Calibration with the untimed 1 GiB device copy in the same runs: FETCH_SIZE reads {fraw:.0f} KiB (scale "
+          f"{fscale:.3f}), WRITE_SIZE reads {wraw:.0f} KiB (scale {wscale:.3f}). The counters count L2 misses (traffic "
+          f"to the Infinity Cache / HBM), per dispatch. Algorithmic bytes: every input read and every output written "
+          f"once. Source hash of the kernels: `{src}`.\n",
+          "| Kernel | Layer (N x K) | fetched MB | written MB | algorithmic MB | ratio |", "|---|---|---|---|---|---|"]
+    for k in PROFILED:
+        if not fetch[k]:
+            continue
+        n = min(len(fetch[k]), len(write[k]))
+        tot = [fetch[k][i] + write[k][i] for i in range(n)]
+        data[k] = {"bytes_per_launch": sum(tot) / n, "source_hash": src, "launches": n}
+        for i, lin in enumerate(w.linears[:n]):
+            alg = algorithmic_bytes(k, w.M, lin.N, lin.K, w.sub_block)
+            md.append(f"| `{k}` | {lin.N}x{lin.K} | {fetch[k][i] / 1e6:.0f} | {write[k][i] / 1e6:.0f} | {alg / 1e6:.0f} | "
+                      f"{tot[i] / alg:.2f} |")
+    with open(os.path.join(REPO, "profiles", "traffic.json"), "w") as f:
+        json.dump(data, f, indent=1)
+    out = os.path.join(REPO, "profiles", f"hbm_traffic_{workload}.md")
+    with open(out, "w") as f:
+        f.write("\n".join(md) + "\n")
+    print(out)
 
 
 if __name__ == "__main__":

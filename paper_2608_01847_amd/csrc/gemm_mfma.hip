@@ -241,14 +241,15 @@ __device__ __forceinline__ uint32_t xcd_tile(uint32_t id, uint32_t count) {
     return id < per * 8u ? (id % 8u) * per + id / 8u : id;
 }
 
-// Position t of a rows x cols tile grid in grouped order: groups of kGroupRows row-tiles are
-// walked column by column, so the ~32 workgroups an XCD runs at once cover about 4 x 8 tiles and
+// Position t of a rows x cols tile grid in grouped order: groups of `group` row-tiles (default 4)
+// are walked column by column, so the ~32 workgroups an XCD runs at once cover about 4 x 8 tiles and
 // share 4 row panels and 8 column panels instead of 1 and 32.
 constexpr uint32_t kGroupRows = 4;
-__device__ __forceinline__ void grouped_tile(uint32_t t, uint32_t rows, uint32_t cols, uint32_t &r, uint32_t &c) {
-    const uint32_t per_group = kGroupRows * cols;
-    const uint32_t first = (t / per_group) * kGroupRows;
-    const uint32_t in_group = rows - first < kGroupRows ? rows - first : kGroupRows;
+__device__ __forceinline__ void grouped_tile(uint32_t t, uint32_t rows, uint32_t cols, uint32_t &r, uint32_t &c,
+                                             uint32_t group = kGroupRows) {
+    const uint32_t per_group = group * cols;
+    const uint32_t first = (t / per_group) * group;
+    const uint32_t in_group = rows - first < group ? rows - first : group;
     const uint32_t u = t % per_group;
     r = first + u % in_group;
     c = u / in_group;
@@ -851,9 +852,12 @@ bwd_mfma_mx_kernel(const uint16_t *__restrict__ dY, const uint8_t *__restrict__ 
                    int tiles_n) {
     __shared__ __attribute__((aligned(16))) char smem[kMxLdsBytes];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
+    // groups of 8 k-tiles: the ~32 workgroups an XCD runs at once cover about 8 k-tiles x 4 out-
+    // feature tiles, so each dY panel (four times the bytes of a packed X_hat panel) is shared by 8
+    // of them and each X_hat panel by 4
     const uint32_t id = xcd_tile(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
     uint32_t tk, tn;
-    grouped_tile(id % gridDim.x, gridDim.x / tiles_n, tiles_n, tk, tn);
+    grouped_tile(id % gridDim.x, gridDim.x / tiles_n, tiles_n, tk, tn, 8);
     const int64_t k0 = (int64_t)tk * kTile, n0 = (int64_t)tn * kTile;
     const int64_t split = id / gridDim.x;
     const int64_t t_begin = split * chunk, t_end = std::min<int64_t>(M, t_begin + chunk);
@@ -894,15 +898,17 @@ bwd_mfma_mx_kernel(const uint16_t *__restrict__ dY, const uint8_t *__restrict__ 
         sl.t0 = (uint32_t)t;
         return sl;
     };
-    // load i (0..5) of a slot into the DMA stage at st: 0-3 the dY tile, 4 the codes, 5 the scale bytes
+    // load i (0..5) of a slot into the DMA stage at st: 0 the codes, 1 the scale bytes, 2-5 the dY
+    // tile. The codes go first: loads complete in issue order, so waiting for a slot's codes leaves
+    // its dY loads in flight (they are needed two steps later than the codes).
     auto issue = [&](lds_char *st, const MxSlot &sl, int i) {
-        if (i < 4) {
-            pb.issue_one(sl.rd, st, wave_u, i);
-        } else if (i == 4) {
+        if (i == 0) {
             __builtin_amdgcn_raw_ptr_buffer_load_lds(sl.rc, st + kMxCodeOff + wave_u * 1024, 16, (int)c_off, 0, 0, 0);
-        } else {
+        } else if (i == 1) {
             __builtin_amdgcn_raw_ptr_buffer_load_lds(sl.rs, st + kMxScaleOff + wave_u * 256, 4,
                                                      (int)((s_off + sl.t0) | s_bad), 0, 0, 0);
+        } else {
+            pb.issue_one(sl.rd, st, wave_u, i - 2);
         }
     };
     const uint32_t lds0 = lds_addr(smem);
@@ -982,9 +988,10 @@ bwd_mfma_mx_kernel(const uint16_t *__restrict__ dY, const uint8_t *__restrict__ 
         const MxSlot sl = slot_at(t_is);
         lds_char *st = lsm + o_is;
         const uint32_t cds = lds0 + o_cv, cas = lds0 + a_cv;
-        // this thread's loads of slot kt + 2 have landed (slot kt + 3 may be in flight); after the
-        // barrier everyone's have, and every wave is done with step kt - 1's stages
-        FOCUS_WAIT_VMCNT(kMxLoads);
+        // this thread's codes and scale bytes of slot kt + 2 and all of slot kt + 1 have landed (slot
+        // kt + 3 and the dY loads of slot kt + 2 may be in flight); after the barrier everyone's
+        // have, and every wave is done with step kt - 1's stages
+        FOCUS_WAIT_VMCNT(kMxLoads + 4);
         asm volatile("s_barrier" ::: "memory");
         tr_wait(f);
         // the conversion's two reads go first, then the 16 fragment reads of the second half: LDS
