@@ -323,10 +323,12 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     const int64_t nk = (K + kKStep - 1) / kKStep;
     // Quarter q of the output tile holds tile rows q*32 + 0..31 and 128 + q*32 + 0..31 (local rows
     // 0..63), i.e. accumulator block i == q of every wave. In LDS a quarter is 64 rows of 512 bytes;
-    // the two 64-byte halves of each 128-byte span are swapped on rows with bit 2 set, so the lanes
-    // reading rows r and r + 4 of one column group use different banks.
+    // the 16-byte chunk index of row r is xor-ed with 2 (r % 4) ^ 4 ((r / 4) % 2): the transposing
+    // reads of the epilogue (4 consecutive rows x 32 bytes per 16 lanes) then touch 8 distinct
+    // chunk slots, and the 2-byte writes of rows r and r + 4 (the two lane halves) different banks.
     auto q_row = [](uint32_t rl, uint32_t q) { return (rl >> 5) * 128u + q * 32u + (rl & 31u); };
-    auto q_off = [](uint32_t rl, uint32_t chunk) { return rl * 512u + ((chunk ^ (((rl >> 2) & 1u) << 2)) << 4); };
+    auto q_key = [](uint32_t rl) { return ((rl & 3u) << 1) ^ (((rl >> 2) & 1u) << 2); };
+    auto q_off = [&](uint32_t rl, uint32_t chunk) { return rl * 512u + ((chunk ^ q_key(rl)) << 4); };
     auto stage = [&](int sidx) { return lsm + sidx * kStage; };
     // Load i of slot j into stage st: loads 0-3 bring X rows, 4-7 W rows of an operand step, and in
     // MX mode 8 / 9 the scale bytes of block 4 j + wave of the tile's 256 X / W rows (a [4][256]
@@ -353,7 +355,7 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
         }
         const uint32_t q = (uint32_t)((j - nk) & 3);
         const uint32_t blk = wave_u * 8 + i, rl = 2 * blk + (lane >> 5);
-        const uint32_t chunk = (uint32_t)(lane & 31) ^ (((rl >> 2) & 1u) << 2);
+        const uint32_t chunk = (uint32_t)(lane & 31) ^ q_key(rl);
         const uint32_t col = (uint32_t)n0 + chunk * 8;
         const uint32_t bad = ((uint32_t)((int32_t)N32 - 1 - (int32_t)col) >> 31) << 31;  // col >= N
         const uint32_t off = ((q_row(rl, q) * N32 + col) * 2u) | bad;
@@ -453,19 +455,25 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     }
 
     // ---- epilogue, one quarter at a time: D = Y_hat - Y_ref, dY = D * dscale, column sums of D^2
-    // Each lane reads its 16 Y values of an accumulator tile from LDS, then writes the 16 dY values
-    // over them (batched: the compiler cannot move LDS reads across the writes); the quarter then
-    // leaves with coalesced 16-byte stores, which drain while the next quarter is processed. Rows
-    // past M and columns past N hold zero accumulators and read Y_ref as zero, so they add nothing
-    // to the column sums; their stores fall outside the resource and are dropped. D^2 is summed per
-    // accumulator tile in fp32 (16 terms), then into the column's fp64 total.
+    // Each lane reads its 16 Y values of an accumulator tile from LDS with four transposing reads
+    // (4 consecutive rows of its column each), then writes the 16 dY values over them; the quarter
+    // then leaves with coalesced 16-byte stores, which drain while the next quarter is processed.
+    // Rows past M and columns past N hold zero accumulators and read Y_ref as zero, so they add
+    // nothing to the column sums; their stores fall outside the resource and are dropped. D^2 is
+    // summed per accumulator tile in fp32 (16 terms), then into the column's fp64 total. dY is
+    // rounded to bf16 by the hardware conversion (round to nearest even).
     double csum[4] = {0.0, 0.0, 0.0, 0.0};
+    // transposing-read lane geometry: the 16-lane group g16 covers rows 4 (g16 / 2) .. + 3 of an
+    // 8-row group and columns 16 (g16 % 2) .. + 15 of the 32 of an accumulator tile; lane j16 of it
+    // points at row j16 / 4 and columns 4 (j16 % 4) .. + 3 (see the backward's fragment reads)
+    const uint32_t g16 = (uint32_t)lane >> 4, j16 = (uint32_t)lane & 15u;
     static_for<4>([&](auto q) {
         if (q == 0) {
             FOCUS_WAIT_VMCNT(3 * kLoads);  // this thread's loads of quarter 0 have landed
             asm volatile("s_barrier" ::: "memory");
         }
         lds_char *qb = stage((int)((nk + q) % S));
+        const uint32_t qa = (uint32_t)(uintptr_t)qb;  // the quarter's LDS byte address
         static_for<4>([&](auto j) {
             const uint32_t n = wn * 128 + j * 32 + lr;  // column in the tile
             typedef __attribute__((address_space(3))) uint16_t lds_u16;
@@ -474,17 +482,30 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
             static_for<16>([&](auto r) {
                 const uint32_t rl = wm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);  // local row of the quarter
                 p[r] = reinterpret_cast<lds_u16 *>(qb + q_off(rl, n >> 3)) + (n & 7);
-                y[r] = MSE ? __uint_as_float((uint32_t)*p[r] << 16) : 0.0f;
             });
+            if constexpr (MSE) {
+                i16x4_t yv[4];
+                const uint32_t col = wn * 128 + j * 32 + 16 * (g16 & 1u) + 4 * (j16 & 3u);
+                static_for<4>([&](auto g) {
+                    const uint32_t row = wm * 32 + 8 * g + 4 * (g16 >> 1) + (j16 >> 2);
+                    yv[g] = ds_read_tr<0>(qa + q_off(row, col >> 3) + (col & 7u) * 2u);
+                });
+                asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(yv[0]), "+v"(yv[1]), "+v"(yv[2]), "+v"(yv[3]));
+                static_for<16>([&](auto r) {
+                    y[r] = __uint_as_float((uint32_t)(uint16_t)yv[r >> 2][r & 3] << 16);
+                });
+            }
             float sq = 0.0f;
+            // one scalar conversion per value: the two-element vector form of this conversion is
+            // miscompiled for gfx950 by the toolchain in use (it converts the first element only)
             static_for<16>([&](auto r) {
                 const float v = acc[q][j][(int)r];
                 if (MSE) {
                     const float d = v - y[r];
-                    *p[r] = (uint16_t)f32_to_bf16_bits(d * dscale);
+                    *p[r] = __builtin_bit_cast(uint16_t, (__bf16)(d * dscale));
                     sq = __builtin_fmaf(d, d, sq);
                 } else {
-                    *p[r] = (uint16_t)f32_to_bf16_bits(v);
+                    *p[r] = __builtin_bit_cast(uint16_t, (__bf16)v);
                 }
             });
             csum[j] += (double)sq;
