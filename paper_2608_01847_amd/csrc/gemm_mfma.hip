@@ -603,9 +603,12 @@ __device__ __forceinline__ void ste_epilogue(const f32x16_t (&acc)[4][4], int64_
                 // coefficients of elements 0-1 and 2-3 (the same sub-block unless sb == 2); without
                 // c the resource is empty and the select makes them 1
                 const uint32_t c0 = ((nl * ns32 + (k >> sb_log2)) * 4u) | past(k);
-                const uint32_t c1 = ((nl * ns32 + ((k + 2) >> sb_log2)) * 4u) | past(k);
                 const float l0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rc, (int)c0, 0, 0));
-                const float l1 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rc, (int)c1, 0, 0));
+                float l1 = l0;  // a sub-block of 4 or more holds all four k (sb_log2 is uniform)
+                if (sb_log2 == 1) {
+                    const uint32_t c1 = ((nl * ns32 + ((k + 2) >> sb_log2)) * 4u) | past(k);
+                    l1 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rc, (int)c1, 0, 0));
+                }
                 cv[i][g][0] = has_c ? l0 : 1.0f;
                 cv[i][g][1] = has_c ? l1 : 1.0f;
             });
@@ -873,12 +876,13 @@ bwd_mfma_mx_kernel(const uint16_t *__restrict__ dY, const uint8_t *__restrict__ 
                    int tiles_n) {
     __shared__ __attribute__((aligned(16))) char smem[kMxLdsBytes];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, wm = wave >> 1, wn = wave & 1;
-    // groups of 8 k-tiles: the ~32 workgroups an XCD runs at once cover about 8 k-tiles x 4 out-
-    // feature tiles, so each dY panel (four times the bytes of a packed X_hat panel) is shared by 8
-    // of them and each X_hat panel by 4
+    // groups of up to 10 k-tiles of equal size: the ~32 workgroups an XCD runs at once cover about
+    // 8-10 k-tiles x 3-4 out-feature tiles, so each dY panel (four times the bytes of a packed X_hat
+    // panel) is shared by 8-10 of them and each X_hat panel by 3-4
     const uint32_t id = xcd_tile(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
+    const uint32_t tiles_k = gridDim.x / tiles_n, ngroups = (tiles_k + 9) / 10;
     uint32_t tk, tn;
-    grouped_tile(id % gridDim.x, gridDim.x / tiles_n, tiles_n, tk, tn, 8);
+    grouped_tile(id % gridDim.x, tiles_k, tiles_n, tk, tn, (tiles_k + ngroups - 1) / ngroups);
     const int64_t k0 = (int64_t)tk * kTile, n0 = (int64_t)tn * kTile;
     const int64_t split = id / gridDim.x;
     const int64_t t_begin = split * chunk, t_end = std::min<int64_t>(M, t_begin + chunk);
