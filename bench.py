@@ -22,6 +22,7 @@ METRIC = "ms per fwd+bwd scale-learning step per decoder block; fake-quant GB/s"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_FP4_TFLOPS = 10100.0   # MI355X dense MXFP4 MFMA
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector (the fp32 operand path runs on VALU FMAs)
 
 
 def parse():
@@ -251,7 +252,10 @@ def main():
     gemm_flops = kern["recon_gemm_fwd"]["units"] + kern["recon_gemm_bwd"]["units"]
     gemm_ms = kern["recon_gemm_fwd"]["total_ms"] + kern["recon_gemm_bwd"]["total_ms"]
 
-    peaks = {"recon_gemm_fwd": PEAK_FP4_TFLOPS if mx_fwd else PEAK_BF16_TFLOPS, "recon_gemm_bwd": PEAK_BF16_TFLOPS}
+    if esz == 4:  # fp32 operands: the VALU kernels
+        peaks = {"recon_gemm_fwd": PEAK_FP32_TFLOPS, "recon_gemm_bwd": PEAK_FP32_TFLOPS}
+    else:
+        peaks = {"recon_gemm_fwd": PEAK_FP4_TFLOPS if mx_fwd else PEAK_BF16_TFLOPS, "recon_gemm_bwd": PEAK_BF16_TFLOPS}
     gemm = {k: {"TFLOPs": round(kern[k]["units"] / (kern[k]["total_ms"] * 1e-3) / 1e12, 1), "peak": peaks[k],
                 "frac": round(kern[k]["units"] / (kern[k]["total_ms"] * 1e-3) / 1e12 / peaks[k], 4)}
             for k in ("recon_gemm_fwd", "recon_gemm_bwd")}
@@ -260,9 +264,13 @@ def main():
     per_launch_flops = d["units"] / d["launches"]
     achieved = per_launch_flops / (d["avg_ms"] * 1e-3) / 1e12
     src_hash = kernel_source_hash()
-    kname = {"recon_gemm_fwd": "fwd_mfma_kernel_mx" if mx_fwd else "fwd_mfma_kernel",
-             "recon_gemm_bwd": "bwd_mfma_mx_kernel" if mx_fwd else "bwd_mfma_kernel"}[dominant]
-    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peaks[dominant], "unit": "TFLOP/s",
+    if esz == 4:
+        kname = {"recon_gemm_fwd": "fwd_valu_kernel", "recon_gemm_bwd": "bwd_valu_kernel"}[dominant]
+    else:
+        kname = {"recon_gemm_fwd": "fwd_mfma_kernel_mx" if mx_fwd else "fwd_mfma_kernel",
+                 "recon_gemm_bwd": "bwd_mfma_mx_kernel" if mx_fwd else "bwd_mfma_kernel"}[dominant]
+    roofline = {"bound": "alu" if esz == 4 else "mfma", "achieved": round(achieved, 2), "peak": peaks[dominant],
+                "unit": "TFLOP/s",
                 "frac": round(achieved / peaks[dominant], 4), "traffic": traffic_from_profile(kname, src_hash),
                 "kernel": kname, "avg_launch_ms": round(d["avg_ms"], 4), "launches": d["launches"],
                 "flops_per_launch": per_launch_flops}
