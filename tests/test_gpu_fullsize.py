@@ -7,7 +7,11 @@ on the GPU with the seeded inputs at their real shapes:
     perturbed state), and for the hidden-8192 block the exported packed codes and scale bytes;
   * loss and straight-through gradients on sampled output rows (first, last, 30 seeded rows and
     rows holding injected weight outliers), against the oracle computed row by row (loss and
-    gradients of an output row depend only on that row), within 2e-2 relative.
+    gradients of an output row depend only on that row), within 2e-2 relative;
+  * for the MXFP4 blocks also the packed-operand step the benchmark times there: activation codes
+    and block-major E8M0 bytes without X_hat and the weights' export, bit-exact against the
+    oracle's codes and scale bytes; the FP4-MFMA forward and the backward from the packed
+    activations, loss and gradients on the sampled rows against the same oracle results.
 """
 import numpy as np
 import pytest
@@ -118,3 +122,26 @@ def test_fullsize_layer(F, O, name, layer):
     assert_close(host_f32(gs)[rows], res.grad_s, TOL, "grad_s")
     assert_close(host_f32(gc)[rows], res.grad_c, TOL, "grad_c")
 
+    if not mx:
+        return
+    # the packed-operand step (the benchmark's default for MXFP4): codes and block-major bytes only
+    announce(f"fullsize packed-operand step {name} {layer}")
+    bm = F.SCALES_BLOCK_MAJOR
+    _, xc, xs, _ = F.fakequant_fwd(X, fmt, sb, want_codes=True, want_scale_bytes=True, want_x_hat=False,
+                                   scale_layout=bm)
+    wc, ws = F.export_packed(W, fmt, sb, s_d, c_d, a_d, scale_layout=bm)
+    _, xcodes_o, xbytes_o, _ = O.fq_act(host_f32(X), fmt)
+    assert_bits_equal(xc.cpu().numpy(), O.pack_codes(xcodes_o), "activation codes")
+    assert_bits_equal(xs.cpu().numpy(), np.ascontiguousarray(xbytes_o.T), "activation scale bytes (block-major)")
+    del xcodes_o, xbytes_o
+    assert_bits_equal(wc.cpu().numpy(), O.pack_codes(fq.codes), "weight codes")
+    assert_bits_equal(ws.cpu().numpy(), np.ascontiguousarray(fq.scale_bytes.T), "weight scale bytes (block-major)")
+    dYm, lossm, colm = F.recon_gemm_fwd_mxfp4(xc, xs, wc, ws, Y, want_col_sq=True)
+    gsm, gcm = F.recon_gemm_bwd_mxfp4(dYm, xc, xs, W, sb, s_d, c_d)
+    torch.cuda.synchronize()
+    colm = colm.cpu().numpy()
+    assert_close(colm[rows], res.col_sq, TOL, "col_sq (packed)")
+    assert abs(lossm.item() - colm.sum() / (w.M * lin.N)) <= 1e-9 * lossm.item()
+    assert abs(lossm.item() - loss.item()) <= 1e-4 * loss.item(), (lossm.item(), loss.item())
+    assert_close(host_f32(gsm)[rows], res.grad_s, TOL, "grad_s (packed)")
+    assert_close(host_f32(gcm)[rows], res.grad_c, TOL, "grad_c (packed)")
