@@ -125,7 +125,8 @@ focus_status focus_scales_init(const focus_qconfig *q, const void *W, int w_dtyp
  * Optional outputs: codes_opt [rows][K/2] packed FP4 codes (code = sign<<3 | magnitude index, the
  *   even-k code in the low nibble); scale_bytes_opt [rows][K/B] (E8M0 byte e+127, or E4M3 byte).
  *   X_hat may be NULL when codes_opt is not (the packed form alone, e.g. for the MXFP4 GEMMs);
- *   X_hat and codes_opt both NULL is FOCUS_ERR_NULL.
+ *   X_hat and codes_opt both NULL is FOCUS_ERR_NULL. With rows == 0 nothing is read or written and
+ *   X, X_hat and codes_opt may be NULL.
  * A zero dequantisation (or quantisation) scale quantises its block to signed zeros. */
 focus_status focus_fakequant_fwd(const focus_qconfig *q, const void *X, int x_dtype, int64_t rows, int64_t K,
                                  const float *s_fp, const float *c, const float *alpha,
@@ -178,7 +179,7 @@ focus_status focus_recon_gemm_fwd_mxfp4(const uint8_t *X_codes, const uint8_t *X
  *   in focus_fakequant_bwd, from W [N][K] (w_dtype), s_fp, c (NULL = ones) and alpha (NVFP4).
  *   dY [M][N] and X_hat [M][K] are in op_dtype. If G_out_opt != NULL the fp32 G is also written.
  *   Long token ranges are split across workgroups; the per-split partial gradients are summed in a
- *   fixed order. */
+ *   fixed order. With M == 0 the gradients are zero (an empty sum) and dY, X_hat may be NULL. */
 focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const void *X_hat, int op_dtype,
                                   int64_t M, int64_t N, int64_t K,
                                   const void *W, int w_dtype, const float *s_fp, const float *c,
@@ -196,7 +197,7 @@ focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const 
  *   as in focus_recon_gemm_bwd. Requires M % 4 == 0 and N % 8 == 0 (FOCUS_ERR_SHAPE otherwise); dY,
  *   X_codes and W 16-byte aligned, X_scales 4-byte aligned. The workspace is that of
  *   FOCUS_CALL_RECON_GEMM_BWD. A scale byte 255 (NaN, never written by the library) makes its
- *   block's values NaN. */
+ *   block's values NaN. With M == 0 the gradients are zero and dY, X_codes, X_scales may be NULL. */
 focus_status focus_recon_gemm_bwd_mxfp4(const focus_qconfig *q, const void *dY, const uint8_t *X_codes,
                                         const uint8_t *X_scales, int64_t M, int64_t N, int64_t K,
                                         const void *W, int w_dtype, const float *s_fp, const float *c,

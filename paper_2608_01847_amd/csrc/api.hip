@@ -136,7 +136,8 @@ focus_status focus_fakequant_fwd(const focus_qconfig *q, const void *X, int x_dt
                                  int xhat_dtype, uint8_t *codes_opt, uint8_t *scale_bytes_opt,
                                  float *alpha_out_opt, void *ws, size_t ws_bytes, focus_stream stream) {
     FOCUS_TRY(check_q(q));
-    if (!X || (!X_hat && !codes_opt)) return FOCUS_ERR_NULL;  // X_hat may be left out when codes are asked for
+    // X_hat may be left out when codes are asked for; an empty tensor (rows == 0) may come as NULL
+    if (rows != 0 && (!X || (!X_hat && !codes_opt))) return FOCUS_ERR_NULL;
     const bool weight_mode = s_fp != nullptr;
     if (weight_mode && q->format == FOCUS_NVFP4 && !alpha) return FOCUS_ERR_NULL;
     if (!weight_mode && (c || alpha)) return FOCUS_ERR_CONFIG;
@@ -212,7 +213,8 @@ focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const 
                                   float *grad_c, float *G_out_opt, void *ws, size_t ws_bytes,
                                   focus_stream stream) {
     FOCUS_TRY(check_q(q));
-    if (!dY || !X_hat || !W || !s_fp || !grad_s || !grad_c) return FOCUS_ERR_NULL;
+    // with no tokens (M == 0) the token operands are never read and may be NULL; the gradients are zero
+    if ((M != 0 && (!dY || !X_hat)) || !W || !s_fp || !grad_s || !grad_c) return FOCUS_ERR_NULL;
     if (q->format == FOCUS_NVFP4 && !alpha) return FOCUS_ERR_NULL;
     if (!dtype_ok(op_dtype) || !dtype_ok(w_dtype)) return FOCUS_ERR_DTYPE;
     FOCUS_TRY(check_rows_k(N, K, block_of(q->format)));
@@ -233,7 +235,8 @@ focus_status focus_recon_gemm_bwd_mxfp4(const focus_qconfig *q, const void *dY, 
                                         float *grad_c, void *ws, size_t ws_bytes, focus_stream stream) {
     FOCUS_TRY(check_q(q));
     if (q->format != FOCUS_MXFP4) return FOCUS_ERR_CONFIG;
-    if (!dY || !X_codes || !X_scales || !W || !s_fp || !grad_s || !grad_c) return FOCUS_ERR_NULL;
+    // with no tokens (M == 0) the token operands are never read and may be NULL; the gradients are zero
+    if ((M != 0 && (!dY || !X_codes || !X_scales)) || !W || !s_fp || !grad_s || !grad_c) return FOCUS_ERR_NULL;
     if (!dtype_ok(w_dtype)) return FOCUS_ERR_DTYPE;
     FOCUS_TRY(check_rows_k(N, K, 32));
     if (M < 0 || M > kMaxDim || (M > 0 && K > kMaxElems / M) || (M > 0 && N > kMaxElems / M))

@@ -81,6 +81,9 @@ def test_argument_checks(L, cpu_only):
     assert fq_fwd(L, focus.QConfig(0, 8, 1, 0, 2)) == focus.ERR_CONFIG  # no such E8M0 rounding
     assert fq_fwd(L, focus.QConfig(1, 8, 1, 0, 1), K=64) == focus.ERR_CONFIG  # floor E8M0 is MXFP4 only
     assert fq_fwd(L, mx, X=None) == focus.ERR_NULL
+    # an empty tensor may come as NULL pointers (nothing is launched)
+    assert L.focus_fakequant_fwd(ctypes.byref(mx), None, 1, 0, 64, None, None, None, None, 1, None, None, None,
+                                 BOGUS, 1 << 20, None) == focus.OK
     # X_hat may be left out only when the codes are asked for
     assert L.focus_fakequant_fwd(ctypes.byref(mx), BOGUS, 1, 4, 64, None, None, None, None, 1, None, BOGUS, None,
                                  BOGUS, 1 << 20, None) == focus.ERR_NULL
@@ -134,6 +137,8 @@ def test_argument_checks(L, cpu_only):
     assert bwd_mx(mx, N=12) == focus.ERR_SHAPE               # N not a multiple of 8
     assert bwd_mx(mx, M=6) == focus.ERR_SHAPE                # M not a multiple of 4
     assert bwd_mx(mx, scales=None) == focus.ERR_NULL
+    assert mxb(ctypes.byref(mx), BOGUS, BOGUS, BOGUS, 8, 8, 64, None, 1, BOGUS, None, BOGUS, BOGUS, BOGUS,
+               1 << 30, None) == focus.ERR_NULL  # W is needed even for no tokens
     assert bwd_mx(mx, scales=ctypes.c_void_p((1 << 20) + 2)) == focus.ERR_SHAPE  # scale bytes not 4-byte aligned
     assert bwd_mx(mx, w_dt=5) == focus.ERR_DTYPE
     assert bwd_mx(mx, ws_bytes=16) == focus.ERR_WORKSPACE

@@ -149,3 +149,57 @@ def test_codes_only_activation_quant(F):
                                           scale_layout=F.SCALES_BLOCK_MAJOR, e8m0_rounding=rnd)
         assert none is None and x_hat is not None
         assert torch.equal(c0, c1) and torch.equal(s0, s1), f"rounding {rnd}"
+
+
+def test_packed_step_is_deterministic(F):
+    """The packed-operand step (fixed-order reductions, no atomics) repeats bit for bit."""
+    from paper_2608_01847_amd import synth
+    w = synth.scaled(synth.WORKLOADS["block2560_mxfp4"], M=3000, hidden_div=4)
+    lin = w.linears[4]  # gate_proj 2432 x 640
+    announce(f"packed determinism {lin.name} M={w.M} N={lin.N} K={lin.K}")
+    X = synth.activation(w, lin.source, device="cuda")
+    W = synth.weight(w, lin, device="cuda")
+    Y = synth.reference_output(X, W)
+    bm = F.SCALES_BLOCK_MAJOR
+    outs = []
+    for _ in range(2):
+        _, xc, xs, _ = F.fakequant_fwd(X, MX, 8, want_codes=True, want_scale_bytes=True, want_x_hat=False,
+                                       scale_layout=bm)
+        s, c, a = F.scales_init(W, MX, 8)
+        wc, ws = F.export_packed(W, MX, 8, s, c, a, scale_layout=bm)
+        dY, loss, col = F.recon_gemm_fwd_mxfp4(xc, xs, wc, ws, Y, want_col_sq=True)
+        gs, gc = F.recon_gemm_bwd_mxfp4(dY, xc, xs, W, 8, s, c)
+        outs.append([t.cpu().clone() for t in (dY, loss, col, gs, gc)])
+    for a_, b_ in zip(*outs):
+        assert torch.equal(a_.view(torch.uint8), b_.view(torch.uint8))
+
+
+@pytest.mark.parametrize("M", [0, 4, 36])
+def test_backward_short_token_ranges(F, O, M):
+    """No tokens gives zero gradients; a few tokens (less than one 32-token step, or one step and a
+    ragged tail) give the oracle's, from both backward entry points."""
+    announce(f"short token range M={M}")
+    g = torch.Generator().manual_seed(41 + M)
+    K, N = 256, 72
+    X = (torch.randn(max(M, 1), K, generator=g) * 2)[:M].to(torch.bfloat16).cuda()
+    W = (torch.randn(N, K, generator=g) * 0.02).to(torch.bfloat16).cuda()
+    dY = (torch.randn(max(M, 1), N, generator=g) * 1e-3)[:M].to(torch.bfloat16).cuda()
+    s, c, a = F.scales_init(W, MX, 8)
+    x_hat, xc, xs, _ = F.fakequant_fwd(X, MX, 8, want_codes=True, want_scale_bytes=True,
+                                       scale_layout=F.SCALES_BLOCK_MAJOR)
+    gs, gc = F.recon_gemm_bwd_mxfp4(dY, xc, xs, W, 8, s, c)
+    gsb, gcb, _ = F.recon_gemm_bwd(dY, x_hat, W, MX, 8, s, c, a)
+    torch.cuda.synchronize()
+    same_bits(gs, gsb, f"grad_s M={M}")
+    same_bits(gc, gcb, f"grad_c M={M}")
+    if M == 0:
+        assert not gs.any() and not gc.any()
+        return
+    Wh = host_f32(W)
+    so, co, ao = O.init_scales(Wh, MX, 8)
+    fq = O.fq_weight(Wh, MX, 8, so, co, ao)
+    xo, _, _, _ = O.fq_act(host_f32(X), MX)
+    G = host_f32(dY).astype(np.float64).T @ xo.astype(np.float64)
+    gs_o, gc_o = O.ste_gradients_from_G(G, fq, MX, 8, ao)
+    assert_close(host_f32(gs), gs_o, TOL, f"grad_s M={M}")
+    assert_close(host_f32(gc), gc_o, TOL, f"grad_c M={M}")
