@@ -80,10 +80,16 @@ class Timer:
 
 
 def kernel_source_hash():
+    """Hash of the library sources with comments and whitespace removed: a change of code changes
+    it, a change of comments does not."""
+    import re
     h = hashlib.sha256()
     for f in sorted(os.listdir(os.path.join(REPO, "paper_2608_01847_amd", "csrc"))):
-        with open(os.path.join(REPO, "paper_2608_01847_amd", "csrc", f), "rb") as fh:
-            h.update(f.encode() + fh.read())
+        with open(os.path.join(REPO, "paper_2608_01847_amd", "csrc", f), encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(f.encode() + " ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -795,7 +795,7 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
 //
 // Per 32-token step a DMA slot brings the dY tile (16 KB, the bf16 kernel's token-major layout), the
 // step's codes ([32 tokens][128 bytes]) and its scale bytes ([8 blocks][32 tokens], one copy per
-// wave so that every thread issues the same number of loads). Three steps after a slot's loads are
+// wave so that every thread issues the same number of loads). Two steps after a slot's loads are
 // issued, each thread converts one token's 32 codes of one block (16 bytes, one scale) into 32 bf16
 // with the scaled FP4 conversion and writes them into one of three bf16 A stages, in the layout the
 // transposing fragment reads expect. Step kt issues slot kt + 4, converts slot kt + 2 and multiplies
