@@ -303,6 +303,7 @@ def main():
                     "max": round(per_step[-1], 4)},
         "block_loss": block_loss,
         "source_hash": src_hash,
+        "device": device_info(torch),
     }
     if mx_possible:
         # the same step with the other forward operands, same inputs: under MXFP4, X_hat and W_hat
@@ -431,6 +432,24 @@ def chain_costs(torch, F, layers, acts, x_hat, fmt, sb, M, ws, rnd, reps=3):
                        "GBps": round(T * V * 6 / (res["kl_top"] * 1e-3) / 1e9, 1)}}
 
 
+def device_info(torch):
+    """What ran the measurement: the GPU, its architecture and CU count, the HIP runtime of torch."""
+    prop = torch.cuda.get_device_properties(0)
+    return {"name": prop.name, "arch": getattr(prop, "gcnArchName", ""), "compute_units": prop.multi_processor_count,
+            "memory_GiB": round(prop.total_memory / 2 ** 30, 1), "hip": torch.version.hip}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def attainable(torch, ms_gemm, fq_GBps):
     """Measured attainable rates on this GPU as secondary denominators (not the product's code): a
     1 GiB device copy and a large bf16 library GEMM (torch.mm, 8192^3, random data)."""
@@ -497,6 +516,7 @@ def cpu_baseline(w, sample_tokens, sample_rows):
         sample_s += t2 - t0
         full_ms += (t1 - t0) * 1e3 * (lin.N / R) + (t2 - t1) * 1e3 * (lin.N / R) * (w.M / Ms)
     return {"value": round(full_ms, 1), "unit": "ms per step", "cores": threads, "kind": "oracle",
+            "cpu": cpu_model(), "host_cpus": os.cpu_count(),
             "sample": f"{Ms} of {w.M} tokens per input; {sample_rows} weight rows per linear "
                       f"({sample_s:.1f} s measured), extrapolated linearly to the full step"}
 
