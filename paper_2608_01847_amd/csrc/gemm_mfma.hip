@@ -202,6 +202,15 @@ __device__ __forceinline__ i16x4_t ds_read_tr(uint32_t addr) {
     return r;
 }
 
+// Two fp32 values rounded to bf16 (to nearest, ties to even) in one instruction: lo in bits 0-15,
+// hi in bits 16-31. Written out because the toolchain in use miscompiles the two-element vector
+// conversion for gfx950 (it converts the first element only).
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+    uint32_t r;
+    asm("v_cvt_pk_bf16_f32 %0, %1, %2" : "=v"(r) : "v"(lo), "v"(hi));
+    return r;
+}
+
 // Per-lane byte offset, inside a tile, of the lower read of the fragment at columns c (step 0).
 __device__ __forceinline__ uint32_t tr_lane_off(uint32_t c, int lane) {
     const uint32_t j = lane & 15;
@@ -409,10 +418,18 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     uint32_t sa[4], sb[4], na[4], nb[4];
     load_frags_fwd(f, smem, smem + kFwdOpBytes, 0, wm, wn, lane);
     if constexpr (MX) load_scales(smem, na, nb);
-    // One step (sc = kt % S). The loads of slot kt + S - 1 go out between the MFMAs of the first
-    // half (8 after every second one, MX's scale loads after the first and the ninth): issued back
-    // to back they would fill the texture unit's queue, and a wave stalled on a full queue issues
-    // no MFMA. The scheduling barriers keep the compiler from regrouping them.
+    // One step (sc = kt % S). The loads of slot kt + S - 1 go out spread over the step's 32 MFMAs:
+    // one after every fourth (operand loads 0-3 in the first half, 4-7 in the second; MX's scale
+    // loads after the fourth MFMA of each half). Issued closer together they fill the texture
+    // unit's queue, and a wave stalled on a full queue issues no MFMA (loads after every second
+    // MFMA of the first half only: 4-7% slower). The scheduling barriers keep the compiler from
+    // regrouping them. Stage (kt - 1) % S, which they fill, was last read in step kt - 1.
+    auto issue_at = [&](lds_char *st, int64_t kt, int li, auto y_slot) {
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (decltype(y_slot)::value) issue_y(st, kt + S - 1, li);
+        else issue_op(st, kt + S - 1, li);
+        __builtin_amdgcn_sched_barrier(0);
+    };
     auto step = [&](int64_t kt, int sc, auto y_slot) {
         FOCUS_WAIT_VMCNT(kLoads * (S - 3));
         asm volatile("s_barrier" ::: "memory");
@@ -428,19 +445,16 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
         static_for<16>([&](auto idx) {
             constexpr int i = idx / 4, jj = idx % 4;
             mfma(std::integral_constant<int, i>{}, std::integral_constant<int, jj>{}, f, sa, sb, std::integral_constant<int, 0>{});
-            if constexpr (idx % 2 == 1 || (MX && (idx == 0 || idx == 8))) {
-                constexpr int li = idx % 2 == 1 ? idx / 2 : 8 + idx / 8;
-                __builtin_amdgcn_sched_barrier(0);
-                if constexpr (decltype(y_slot)::value) issue_y(st, kt + S - 1, li);
-                else issue_op(st, kt + S - 1, li);
-                __builtin_amdgcn_sched_barrier(0);
-            }
+            if constexpr (idx % 4 == 1) issue_at(st, kt, idx / 4, y_slot);
+            if constexpr (MX && idx == 3) issue_at(st, kt, 8, y_slot);
         });
         load_frags_fwd(f, An, Bn, 0, wm, wn, lane);
         if constexpr (MX) load_scales(An, na, nb);
         static_for<16>([&](auto idx) {
             constexpr int i = idx / 4, jj = idx % 4;
             mfma(std::integral_constant<int, i>{}, std::integral_constant<int, jj>{}, g, sa, sb, std::integral_constant<int, 1>{});
+            if constexpr (idx % 4 == 1) issue_at(st, kt, 4 + idx / 4, y_slot);
+            if constexpr (MX && idx == 3) issue_at(st, kt, 9, y_slot);
         });
     };
     const int64_t n_op = nk > S - 1 ? nk - (S - 1) : 0;  // steps whose slot kt + S - 1 is an operand step
@@ -463,50 +477,74 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     // summed per accumulator tile in fp32 (16 terms), then into the column's fp64 total. dY is
     // rounded to bf16 by the hardware conversion (round to nearest even).
     double csum[4] = {0.0, 0.0, 0.0, 0.0};
-    // transposing-read lane geometry: the 16-lane group g16 covers rows 4 (g16 / 2) .. + 3 of an
-    // 8-row group and columns 16 (g16 % 2) .. + 15 of the 32 of an accumulator tile; lane j16 of it
-    // points at row j16 / 4 and columns 4 (j16 % 4) .. + 3 (see the backward's fragment reads)
+    // The epilogue is bound by vector instructions, so every LDS address is a per-lane offset
+    // computed once here plus the quarter's base and a constant: q_key(rl) depends on rl % 8 only,
+    // so 8 more rows are 4096 bytes further, and two accumulator tiles further right (64 columns,
+    // 8 chunks, which the key's 3 bits leave alone) are 128 bytes further.
+    //  * dY writes of accumulator tile j, register r: row wm 32 + 8 (r / 4) + 4 lh + r % 4, column
+    //    wn 128 + 32 j + lr: w_off[j % 2][r % 4] + 4096 (r / 4) + 128 (j / 2).
+    //  * transposing Y_ref reads of tile j, row group g: the 16-lane group g16 covers rows
+    //    4 (g16 / 2) .. + 3 of an 8-row group and columns 16 (g16 % 2) .. + 15 of the tile's 32;
+    //    lane j16 of it points at row j16 / 4, columns 4 (j16 % 4) .. + 3 (see the backward's
+    //    fragment reads): y_off[j % 2] + 4096 g + 128 (j / 2).
+    //  * the quarter's coalesced stores: thread t moves chunk t % 32 of local rows t / 32 + 8 i
+    //    (i = 0..7): LDS st_lds + 4096 i; memory st_mem + (q_row(8 i, q) - q_row(0, 0)) 2 N, the
+    //    column bound folded into st_mem's bit 31 (rows past M fall outside the resource).
     const uint32_t g16 = (uint32_t)lane >> 4, j16 = (uint32_t)lane & 15u;
+    uint32_t w_off[2][4], y_off[2];
+#pragma unroll
+    for (int jb = 0; jb < 2; jb++) {
+        const uint32_t n = wn * 128 + jb * 32 + lr;
+#pragma unroll
+        for (int rr = 0; rr < 4; rr++) w_off[jb][rr] = q_off(wm * 32 + 4 * lh + rr, n >> 3) + (n & 7u) * 2u;
+        const uint32_t col = wn * 128 + jb * 32 + 16 * (g16 & 1u) + 4 * (j16 & 3u);
+        y_off[jb] = q_off(wm * 32 + 4 * (g16 >> 1) + (j16 >> 2), col >> 3) + (col & 7u) * 2u;
+    }
+    const uint32_t st_lds = q_off((uint32_t)t >> 5, (uint32_t)t & 31u);
+    const uint32_t st_col = (uint32_t)n0 + ((uint32_t)t & 31u) * 8u;
+    const uint32_t st_mem = (((uint32_t)t >> 5) * N32 + st_col) * 2u |
+                            ((uint32_t)((int32_t)N32 - 1 - (int32_t)st_col) >> 31) << 31;  // col >= N
+    typedef __attribute__((address_space(3))) uint16_t lds_u16;
+    auto lds16 = [](uint32_t addr) { return reinterpret_cast<lds_u16 *>((uintptr_t)addr); };
     static_for<4>([&](auto q) {
         if (q == 0) {
             FOCUS_WAIT_VMCNT(3 * kLoads);  // this thread's loads of quarter 0 have landed
             asm volatile("s_barrier" ::: "memory");
         }
-        lds_char *qb = stage((int)((nk + q) % S));
-        const uint32_t qa = (uint32_t)(uintptr_t)qb;  // the quarter's LDS byte address
+        const uint32_t qa = (uint32_t)(uintptr_t)stage((int)((nk + q) % S));  // the quarter's LDS address
+        uint32_t wa[2][4];
+#pragma unroll
+        for (int jb = 0; jb < 2; jb++)
+#pragma unroll
+            for (int rr = 0; rr < 4; rr++) wa[jb][rr] = qa + w_off[jb][rr];
         static_for<4>([&](auto j) {
-            const uint32_t n = wn * 128 + j * 32 + lr;  // column in the tile
-            typedef __attribute__((address_space(3))) uint16_t lds_u16;
-            lds_u16 *p[16];
+            constexpr uint32_t jo = 128u * (j / 2);
             float y[16];
-            static_for<16>([&](auto r) {
-                const uint32_t rl = wm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);  // local row of the quarter
-                p[r] = reinterpret_cast<lds_u16 *>(qb + q_off(rl, n >> 3)) + (n & 7);
-            });
             if constexpr (MSE) {
+                const uint32_t ya = qa + y_off[j % 2];
                 i16x4_t yv[4];
-                const uint32_t col = wn * 128 + j * 32 + 16 * (g16 & 1u) + 4 * (j16 & 3u);
-                static_for<4>([&](auto g) {
-                    const uint32_t row = wm * 32 + 8 * g + 4 * (g16 >> 1) + (j16 >> 2);
-                    yv[g] = ds_read_tr<0>(qa + q_off(row, col >> 3) + (col & 7u) * 2u);
-                });
+                static_for<4>([&](auto g) { yv[g] = ds_read_tr<4096 * g + jo>(ya); });
                 asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(yv[0]), "+v"(yv[1]), "+v"(yv[2]), "+v"(yv[3]));
                 static_for<16>([&](auto r) {
                     y[r] = __uint_as_float((uint32_t)(uint16_t)yv[r >> 2][r & 3] << 16);
                 });
             }
             float sq = 0.0f;
-            // one scalar conversion per value: the two-element vector form of this conversion is
-            // miscompiled for gfx950 by the toolchain in use (it converts the first element only)
-            static_for<16>([&](auto r) {
-                const float v = acc[q][j][(int)r];
-                if (MSE) {
-                    const float d = v - y[r];
-                    *p[r] = __builtin_bit_cast(uint16_t, (__bf16)(d * dscale));
-                    sq = __builtin_fmaf(d, d, sq);
-                } else {
-                    *p[r] = __builtin_bit_cast(uint16_t, (__bf16)v);
+            // two rows per conversion (round to nearest even, the low half from the first operand),
+            // the halves stored by separate 2-byte writes
+            static_for<8>([&](auto h) {
+                constexpr int r0 = 2 * h, r1 = 2 * h + 1;
+                float o0 = acc[q][j][r0], o1 = acc[q][j][r1];
+                if constexpr (MSE) {
+                    const float d0 = o0 - y[r0], d1 = o1 - y[r1];
+                    sq = __builtin_fmaf(d0, d0, sq);
+                    sq = __builtin_fmaf(d1, d1, sq);
+                    o0 = d0 * dscale;
+                    o1 = d1 * dscale;
                 }
+                const uint32_t pk = cvt_pk_bf16(o0, o1);
+                *(lds16(wa[j % 2][r0 & 3]) + (4096u * (r0 >> 2) + jo) / 2) = (uint16_t)pk;
+                *(lds16(wa[j % 2][r1 & 3]) + (4096u * (r1 >> 2) + jo) / 2) = (uint16_t)(pk >> 16);
             });
             csum[j] += (double)sq;
         });
@@ -516,13 +554,11 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
         __syncthreads();
 #pragma unroll
         for (int i = 0; i < 8; i++) {
-            const uint32_t cidx = t + 256 * i, rl = cidx >> 5, chunk = cidx & 31;
-            const uint32_t col = (uint32_t)n0 + chunk * 8;
-            const uint32_t bad = ((uint32_t)((int32_t)N32 - 1 - (int32_t)col) >> 31) << 31;  // col >= N
-            const uint32_t off = ((q_row(rl, q) * N32 + col) * 2u) | bad;
             typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-            const u32x4 w = *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(qb + q_off(rl, chunk));
-            __builtin_amdgcn_raw_buffer_store_b128(w, rs_d, (int)off, 0, 0);
+            const u32x4 w = *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(
+                (uintptr_t)(qa + st_lds + 4096u * i));
+            const uint32_t rows = (uint32_t)(i / 4) * 128u + (uint32_t)(i % 4) * 8u + (uint32_t)q * 32u;
+            __builtin_amdgcn_raw_buffer_store_b128(w, rs_d, (int)(st_mem + rows * N32 * 2u), 0, 0);
         }
     });
     if (!MSE) return;
