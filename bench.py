@@ -33,6 +33,9 @@ def parse():
                    help="write profiles/traffic.json and the HBM traffic summary from the two rocprofv3 --pmc "
                         "output directories (FETCH_SIZE, WRITE_SIZE) of a --steps 1 --warmup 0 "
                         "--copy-calibration run and exit")
+    p.add_argument("--summarize-mfma", metavar="DIR",
+                   help="write the MFMA-utilisation summary from the rocprofv3 --pmc output directory of a "
+                        "--steps 1 --warmup 0 --copy-calibration run with the counters of PMC_MFMA and exit")
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
@@ -108,11 +111,13 @@ def traffic_from_profile(kernel: str, src_hash: str):
 
 def main():
     args = parse()
-    if args.summarize_trace or args.summarize_counters:
+    if args.summarize_trace or args.summarize_counters or args.summarize_mfma:
         if args.summarize_trace:
             summarize_trace(args.summarize_trace, args.workload)
         if args.summarize_counters:
             summarize_counters(*args.summarize_counters, args.workload)
+        if args.summarize_mfma:
+            summarize_mfma(args.summarize_mfma, args.workload)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the data-parallel path across GPUs is not built "
@@ -533,6 +538,12 @@ PMC_CMD = ("rocprofv3 --pmc {c} -d gpurun_out/prof_{d} -o run --output-format cs
            "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --copy-calibration")
 
 
+# one counter pass (6 SQ and 1 GRBM counters, within what one rocprofv3 pass can collect on gfx950);
+# MfmaUtil is rocprofv3's own metric: MFMA-busy cycles summed over SIMDs / (GPU-busy cycles x SIMDs)
+PMC_MFMA = ("MfmaUtil SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU_MFMA_MOPS_F8 "
+            "SQ_BUSY_CYCLES SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE")  # pass as one --pmc argument list
+
+
 def algorithmic_bytes(kernel, M, N, K, sb):
     """Bytes each input is read and each output written once, per launch (one linear)."""
     grads = N * K // 32 * 4 + N * K // sb * 4
@@ -605,6 +616,56 @@ def summarize_counters(fetch_dir, write_dir, workload):
     with open(os.path.join(REPO, "profiles", "traffic.json"), "w") as f:
         json.dump(data, f, indent=1)
     out = os.path.join(REPO, "profiles", f"hbm_traffic_{workload}.md")
+    with open(out, "w") as f:
+        f.write("\n".join(md) + "\n")
+    print(out)
+
+
+def summarize_mfma(pmc_dir, workload):
+    import csv
+
+    from paper_2608_01847_amd import synth
+    w = synth.WORKLOADS[workload]
+    vals = {}  # (dispatch, kernel name) -> {counter: value, "ns": duration}
+    for r in csv.DictReader(open(os.path.join(pmc_dir, "run_counter_collection.csv"))):
+        d = vals.setdefault((int(r["Dispatch_Id"]), r["Kernel_Name"]), {})
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+        d["ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    simds = 256 * 4
+    md = [f"# MFMA utilisation of the reconstruction GEMMs ({workload}, {w.M:,} tokens)\n",
+          "Command (from the repository root on one MI355X):\n",
+          "    " + PMC_CMD.format(c=PMC_MFMA, d="mfma") + "\n",
+          "Per launch (one linear layer), the first launches of each kernel in the run (the default step's). "
+          "`MFMA busy` is rocprofv3's MfmaUtil: cycles in which a SIMD's matrix unit is busy, summed over the "
+          "1,024 SIMDs, over GPU-busy cycles x 1,024. `clock` is the GPU-busy cycle count (the counter's maximum over "
+          "instances, recovered from MfmaUtil and the MFMA-busy sum) over the launch's duration in the counter run. "
+          "`executed / algorithmic` compares the MFMA work the counters saw with 2 M N K: bf16 MOPS x 512, and for "
+          "the FP4 kernel, whose block-scaled MFMA no MOPS counter records, its busy cycles / 32 (a 32x32x64 FP4 "
+          "MFMA occupies its SIMD's matrix unit for 32 cycles, as a 32x32x16 bf16 one does) x 131,072 flops. `frac of peak` = algorithmic flops / duration / the dense "
+          "peak (bf16 2.5 PFLOP/s, FP4 10.1, both at 2.4 GHz); `frac at the clock` = frac of peak x 2.4 GHz / clock, "
+          "the fraction of what the matrix units deliver at the clock they ran at. The clock is as good as the "
+          "counter window: where the derived figure exceeds the chip's 2.4 GHz the window was longer than the "
+          "kernel's timestamps, and that row's busy share and clock are approximate. LDS conflicts: bank-"
+          f"conflict cycles / LDS-active cycles. Source hash of the kernels: `{kernel_source_hash()}`.\n",
+          "| Kernel | Layer (N x K) | us | MFMA busy | clock GHz | executed / algorithmic | TFLOP/s | frac of peak | "
+          "frac at the clock | LDS conflicts |", "|---|---|---|---|---|---|---|---|---|---|"]
+    for k, pre in PROFILED.items():
+        runs = [(disp, v) for (disp, name), v in sorted(vals.items()) if name.startswith(pre)][:len(w.linears)]
+        fp4 = k == "fwd_mfma_kernel_mx"
+        peak = PEAK_FP4_TFLOPS if fp4 else PEAK_BF16_TFLOPS
+        for (disp, v), lin in zip(runs, w.linears):
+            alg = 2.0 * w.M * lin.N * lin.K
+            util = v.get("MfmaUtil", 0.0)
+            busy = v.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+            gui = busy * 100.0 / (util * simds) if util > 0 else 0.0
+            ghz = gui / v["ns"] if v["ns"] > 0 else 0.0
+            mops = busy / 32 * 131072 if fp4 else v.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512
+            tf = alg / v["ns"] / 1e3
+            frac = tf / peak
+            lds = v.get("SQ_LDS_BANK_CONFLICT", 0.0) / max(v.get("SQ_LDS_IDX_ACTIVE", 0.0), 1.0)
+            md.append(f"| `{k}` | {lin.N}x{lin.K} | {v['ns'] / 1e3:.0f} | {util:.1f}% | {ghz:.2f} | "
+                      f"{mops / alg:.3f} | {tf:.0f} | {frac:.3f} | {frac * 2.4 / ghz if ghz else 0:.3f} | {100 * lds:.1f}% |")
+    out = os.path.join(REPO, "profiles", f"mfma_util_{workload}.md")
     with open(out, "w") as f:
         f.write("\n".join(md) + "\n")
     print(out)
