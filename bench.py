@@ -528,13 +528,14 @@ def cpu_baseline(w, sample_tokens, sample_rows):
 
 # ---- rocprofv3 summaries (host only) ------------------------------------------------------------
 # Library kernels by the name bench.py reports them under, and the rocprofv3 name prefix of each.
+# The commands below write into OUT, any output directory; the summaries are made from it.
 PROFILED = {"bwd_mfma_mx_kernel": "void focus::bwd_mfma_mx_kernel<",
             "fwd_mfma_kernel_mx": "void focus::fwd_mfma_kernel<true, true>",
             "fwd_mfma_kernel": "void focus::fwd_mfma_kernel<true, false>",
             "bwd_mfma_kernel": "void focus::bwd_mfma_kernel<"}
-TRACE_CMD = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof_trace -o run --output-format csv -- "
+TRACE_CMD = ("rocprofv3 --kernel-trace --stats -d OUT/prof_trace -o run --output-format csv -- "
              "python3 -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration")
-PMC_CMD = ("rocprofv3 --pmc {c} -d gpurun_out/prof_{d} -o run --output-format csv -- "
+PMC_CMD = ("rocprofv3 --pmc {c} -d OUT/prof_{d} -o run --output-format csv -- "
            "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --copy-calibration")
 
 
@@ -561,7 +562,7 @@ def summarize_trace(trace_dir, workload):
     out = os.path.join(REPO, "profiles", f"step_{workload.replace('_mxfp4', '')}_{workload.split('_')[-1]}_kernel_stats.md")
     with open(out, "w") as f:
         f.write(f"# Kernel-trace summary: scale-learning steps of the {workload} workload\n\n")
-        f.write("Command (from the repository root on one MI355X):\n\n    " + TRACE_CMD + "\n\n")
+        f.write("Command (from the repository root on one MI355X; OUT is any output directory):\n\n    " + TRACE_CMD + "\n\n")
         f.write("The run times the default step (2 warm-up + 5 timed) and then the same step with the other forward and "
                 "backward operands, and the calls outside the step (chaining, AdamW, export); library kernels only, "
                 f"source hash `{kernel_source_hash()}`:\n\n")
@@ -596,7 +597,7 @@ def summarize_counters(fetch_dir, write_dir, workload):
                              "note": "scales = known bytes of a 1 GiB device copy / what FETCH_SIZE and WRITE_SIZE "
                                      "read for it"}}
     md = [f"# HBM-side traffic of the reconstruction GEMMs ({workload}, {w.M:,} tokens)\n",
-          "Commands (one counter per run, from the repository root on one MI355X):\n",
+          "Commands (one counter per run, from the repository root on one MI355X; OUT is any output directory):\n",
           "    " + PMC_CMD.format(c="FETCH_SIZE", d="fetch"), "    " + PMC_CMD.format(c="WRITE_SIZE", d="write") + "\n",
           f"Calibration with the untimed 1 GiB device copy in the same runs: FETCH_SIZE reads {fraw:.0f} KiB (scale "
           f"{fscale:.3f}), WRITE_SIZE reads {wraw:.0f} KiB (scale {wscale:.3f}). The counters count L2 misses (traffic "
@@ -633,7 +634,7 @@ def summarize_mfma(pmc_dir, workload):
         d["ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
     simds = 256 * 4
     md = [f"# MFMA utilisation of the reconstruction GEMMs ({workload}, {w.M:,} tokens)\n",
-          "Command (from the repository root on one MI355X):\n",
+          "Command (from the repository root on one MI355X; OUT is any output directory):\n",
           "    " + PMC_CMD.format(c=PMC_MFMA, d="mfma") + "\n",
           "Per launch (one linear layer), the first launches of each kernel in the run (the default step's). "
           "`MFMA busy` is rocprofv3's MfmaUtil: cycles in which a SIMD's matrix unit is busy, summed over the "
