@@ -82,13 +82,14 @@ class Timer:
         return res
 
 
-def kernel_source_hash():
+def kernel_source_hash(csrc_dir=None):
     """Hash of the library sources with comments and whitespace removed: a change of code changes
     it, a change of comments does not."""
     import re
+    csrc_dir = csrc_dir or os.path.join(REPO, "paper_2608_01847_amd", "csrc")
     h = hashlib.sha256()
-    for f in sorted(os.listdir(os.path.join(REPO, "paper_2608_01847_amd", "csrc"))):
-        with open(os.path.join(REPO, "paper_2608_01847_amd", "csrc", f), encoding="utf-8") as fh:
+    for f in sorted(os.listdir(csrc_dir)):
+        with open(os.path.join(csrc_dir, f), encoding="utf-8") as fh:
             text = fh.read()
         text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
         text = re.sub(r"//[^\n]*", " ", text)
@@ -96,9 +97,9 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(kernel: str, src_hash: str):
+def traffic_from_profile(kernel: str, src_hash: str, path=None):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it is current."""
-    path = os.path.join(REPO, "profiles", "traffic.json")
+    path = path or os.path.join(REPO, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -555,11 +556,12 @@ def algorithmic_bytes(kernel, M, N, K, sb):
             "bwd_mfma_mx_kernel": 2 * M * N + M * (K // 2 + K // 32) + wparams + grads}[kernel]
 
 
-def summarize_trace(trace_dir, workload):
+def summarize_trace(trace_dir, workload, out_dir=None):
     import csv
     rows = [r for r in csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv")))
             if "focus::" in r["Name"]]
-    out = os.path.join(REPO, "profiles", f"step_{workload.replace('_mxfp4', '')}_{workload.split('_')[-1]}_kernel_stats.md")
+    out = os.path.join(out_dir or os.path.join(REPO, "profiles"),
+                       f"step_{workload.replace('_mxfp4', '')}_{workload.split('_')[-1]}_kernel_stats.md")
     with open(out, "w") as f:
         f.write(f"# Kernel-trace summary: scale-learning steps of the {workload} workload\n\n")
         f.write("Command (from the repository root on one MI355X; OUT is any output directory):\n\n    " + TRACE_CMD + "\n\n")
@@ -574,7 +576,7 @@ def summarize_trace(trace_dir, workload):
     print(out)
 
 
-def summarize_counters(fetch_dir, write_dir, workload):
+def summarize_counters(fetch_dir, write_dir, workload, out_dir=None):
     import csv
 
     from paper_2608_01847_amd import synth
@@ -614,15 +616,16 @@ def summarize_counters(fetch_dir, write_dir, workload):
             alg = algorithmic_bytes(k, w.M, lin.N, lin.K, w.sub_block)
             md.append(f"| `{k}` | {lin.N}x{lin.K} | {fetch[k][i] / 1e6:.0f} | {write[k][i] / 1e6:.0f} | {alg / 1e6:.0f} | "
                       f"{tot[i] / alg:.2f} |")
-    with open(os.path.join(REPO, "profiles", "traffic.json"), "w") as f:
+    out_dir = out_dir or os.path.join(REPO, "profiles")
+    with open(os.path.join(out_dir, "traffic.json"), "w") as f:
         json.dump(data, f, indent=1)
-    out = os.path.join(REPO, "profiles", f"hbm_traffic_{workload}.md")
+    out = os.path.join(out_dir, f"hbm_traffic_{workload}.md")
     with open(out, "w") as f:
         f.write("\n".join(md) + "\n")
     print(out)
 
 
-def summarize_mfma(pmc_dir, workload):
+def summarize_mfma(pmc_dir, workload, out_dir=None):
     import csv
 
     from paper_2608_01847_amd import synth
@@ -666,7 +669,7 @@ def summarize_mfma(pmc_dir, workload):
             lds = v.get("SQ_LDS_BANK_CONFLICT", 0.0) / max(v.get("SQ_LDS_IDX_ACTIVE", 0.0), 1.0)
             md.append(f"| `{k}` | {lin.N}x{lin.K} | {v['ns'] / 1e3:.0f} | {util:.1f}% | {ghz:.2f} | "
                       f"{mops / alg:.3f} | {tf:.0f} | {frac:.3f} | {frac * 2.4 / ghz if ghz else 0:.3f} | {100 * lds:.1f}% |")
-    out = os.path.join(REPO, "profiles", f"mfma_util_{workload}.md")
+    out = os.path.join(out_dir or os.path.join(REPO, "profiles"), f"mfma_util_{workload}.md")
     with open(out, "w") as f:
         f.write("\n".join(md) + "\n")
     print(out)

@@ -1,0 +1,123 @@
+"""Host logic of bench.py (no GPU): algorithmic work, the source hash that gates the traffic figure,
+the rocprofv3 summaries, and the one-GPU guard."""
+import csv
+import json
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+REPO = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, REPO)
+import bench  # noqa: E402
+
+
+def test_algorithmic_bytes_per_tensor():
+    M, N, K, sb = 256, 128, 64, 8
+    x_bf16, w_bf16, y_ref, dy = 2 * M * K, 2 * N * K, 2 * M * N, 2 * M * N
+    x_packed, w_packed = M * (K // 2 + K // 32), N * (K // 2 + K // 32)  # codes + one E8M0 byte per 32
+    s_fp, coeff = 4 * N * K // 32, 4 * N * K // sb                          # fp32 parameters
+    grad_s, grad_c = s_fp, coeff
+    assert bench.algorithmic_bytes("fwd_mfma_kernel", M, N, K, sb) == x_bf16 + w_bf16 + y_ref + dy
+    assert bench.algorithmic_bytes("fwd_mfma_kernel_mx", M, N, K, sb) == x_packed + w_packed + y_ref + dy
+    # the backward reads dY, X_hat and W with its scales and coefficients, and writes both gradients
+    assert bench.algorithmic_bytes("bwd_mfma_kernel", M, N, K, sb) == dy + x_bf16 + w_bf16 + s_fp + coeff + grad_s + grad_c
+    assert bench.algorithmic_bytes("bwd_mfma_mx_kernel", M, N, K, sb) == dy + x_packed + w_bf16 + s_fp + coeff + grad_s + grad_c
+
+
+def test_source_hash_ignores_comments_not_code(tmp_path):
+    src = os.path.join(REPO, "paper_2608_01847_amd", "csrc")
+    d = tmp_path / "csrc"
+    shutil.copytree(src, d)
+    h0 = bench.kernel_source_hash(str(d))
+    assert h0 == bench.kernel_source_hash()
+    f = d / "optim.hip"
+    text = f.read_text()
+    f.write_text("// a new comment line\n/* and a block\n comment */\n" + text.replace("\n", "\n\n", 3))
+    assert bench.kernel_source_hash(str(d)) == h0
+    f.write_text(text + "\nstatic int focus_unused_symbol = 1;\n")
+    assert bench.kernel_source_hash(str(d)) != h0
+
+
+def test_traffic_reported_only_for_the_recorded_hash(tmp_path):
+    p = tmp_path / "traffic.json"
+    p.write_text(json.dumps({"bwd_mfma_mx_kernel": {"bytes_per_launch": 123.0, "source_hash": "abc", "launches": 7}}))
+    assert bench.traffic_from_profile("bwd_mfma_mx_kernel", "abc", str(p)) == 123.0
+    assert bench.traffic_from_profile("bwd_mfma_mx_kernel", "abd", str(p)) is None
+    assert bench.traffic_from_profile("fwd_mfma_kernel", "abc", str(p)) is None
+    assert bench.traffic_from_profile("bwd_mfma_mx_kernel", "abc", str(tmp_path / "missing.json")) is None
+
+
+COLS = ["Correlation_Id", "Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp",
+        "End_Timestamp"]
+
+
+def write_counter_csv(d, rows):
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, "run_counter_collection.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=COLS)
+        w.writeheader()
+        for i, (disp, name, counter, value, ns) in enumerate(rows):
+            w.writerow({"Correlation_Id": i, "Dispatch_Id": disp, "Kernel_Name": name, "Counter_Name": counter,
+                        "Counter_Value": value, "Start_Timestamp": 1000, "End_Timestamp": 1000 + ns})
+
+
+BWD_MX = "void focus::bwd_mfma_mx_kernel<1>(unsigned short const*)"
+COPY = "__amd_rocclr_copyBuffer"
+
+
+def test_counter_summary_scales_by_the_copy(tmp_path):
+    # the 1 GiB copy reads 524288 KiB on FETCH_SIZE (scale 2) and 1048576 KiB on WRITE_SIZE (scale 1)
+    fetch = [(1, COPY, "FETCH_SIZE", 524288.0, 10)] + [(10 + i, BWD_MX, "FETCH_SIZE", 1000.0 * (i + 1), 10)
+                                                       for i in range(7)]
+    write = [(1, COPY, "WRITE_SIZE", 1048576.0, 10)] + [(10 + i, BWD_MX, "WRITE_SIZE", 10.0, 10) for i in range(7)]
+    write_counter_csv(tmp_path / "f", fetch)
+    write_counter_csv(tmp_path / "w", write)
+    out = tmp_path / "out"
+    out.mkdir()
+    bench.summarize_counters(str(tmp_path / "f"), str(tmp_path / "w"), "block2560_mxfp4", out_dir=str(out))
+    data = json.loads((out / "traffic.json").read_text())
+    assert data["_calibration"]["fetch_scale"] == pytest.approx(2.0)
+    assert data["_calibration"]["write_scale"] == pytest.approx(1.0)
+    want = sum(1000.0 * (i + 1) * 1024 * 2 + 10.0 * 1024 for i in range(7)) / 7
+    assert data["bwd_mfma_mx_kernel"]["bytes_per_launch"] == pytest.approx(want)
+    assert data["bwd_mfma_mx_kernel"]["source_hash"] == bench.kernel_source_hash()
+    assert "fwd_mfma_kernel" not in data  # no rows, no entry
+    assert (out / "hbm_traffic_block2560_mxfp4.md").exists()
+
+
+def test_mfma_summary_row(tmp_path):
+    from paper_2608_01847_amd import synth
+    w = synth.WORKLOADS["block2560_mxfp4"]
+    lin = w.linears[0]
+    alg = 2.0 * w.M * lin.N * lin.K
+    ns = 1.0e6
+    busy = alg / 32768 * 32          # 32 busy cycles per 32x32x16 bf16 MFMA, summed over SIMDs
+    util = 55.0                      # percent of GPU-busy cycles x 1024 SIMDs
+    rows = [(20, BWD_MX, "MfmaUtil", util, ns), (20, BWD_MX, "SQ_VALU_MFMA_BUSY_CYCLES", busy, ns),
+            (20, BWD_MX, "SQ_INSTS_VALU_MFMA_MOPS_BF16", alg / 512, ns),
+            (20, BWD_MX, "SQ_LDS_BANK_CONFLICT", 10.0, ns), (20, BWD_MX, "SQ_LDS_IDX_ACTIVE", 1000.0, ns)]
+    write_counter_csv(tmp_path / "m", rows)
+    bench.summarize_mfma(str(tmp_path / "m"), "block2560_mxfp4", out_dir=str(tmp_path))
+    text = (tmp_path / "mfma_util_block2560_mxfp4.md").read_text()
+    row = next(l for l in text.splitlines() if l.startswith("| `bwd_mfma_mx_kernel`"))
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    ghz = busy * 100 / (util * 1024) / ns
+    frac = alg / ns / 1e3 / bench.PEAK_BF16_TFLOPS
+    assert cells[1] == f"{lin.N}x{lin.K}"
+    assert cells[3] == "55.0%"
+    assert float(cells[4]) == pytest.approx(ghz, abs=0.006)
+    assert cells[5] == "1.000"
+    assert float(cells[7]) == pytest.approx(frac, abs=0.0006)
+    assert float(cells[8]) == pytest.approx(frac * 2.4 / ghz, abs=0.0006)
+    assert cells[9] == "1.0%"
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(REPO, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120, cwd=REPO)
+    assert r.returncode == 2
+    assert "one GPU only" in r.stderr
+    assert r.stdout == ""
