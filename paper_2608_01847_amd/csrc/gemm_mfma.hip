@@ -1,24 +1,24 @@
 // bf16 MFMA reconstruction GEMMs for gfx950 (v_mfma_f32_32x32x16_bf16, fp32 accumulation).
 //
-// Both kernels compute a 256 x 256 output tile per workgroup of 256 threads (four waves, 2 x 2,
-// each owning 128 x 128 = 4 x 4 MFMA tiles of 32 x 32), with one barrier per reduction step:
-//   forward : operand tiles go straight from memory into four LDS stages of 32 of K
-//             (buffer_load ... lds), three steps ahead of the MFMAs;
-//   backward: operand tiles are token-major and must be transposed, so each thread fetches the
-//             next 64-token step into registers while the current one runs, transposes 8 x 8
-//             blocks in registers and stores them into the other of two LDS stages.
+// Every kernel computes a 256 x 256 output tile per workgroup of 256 threads (four waves, 2 x 2,
+// each owning 128 x 128 = 4 x 4 MFMA tiles of 32 x 32; one workgroup per CU), with one barrier per
+// reduction step. Operand tiles go from memory straight into a ring of LDS stages with
+// direct-to-LDS buffer loads (buffer_load ... lds), several steps ahead of the MFMAs:
+//   forward : 32 of K per step (128 for packed MXFP4 operands) in 5 (4) stages;
+//   backward: 32 tokens per step in 4 stages; with packed MXFP4 X_hat, 5 stages of dY, codes and
+//             scale bytes, whose codes are converted to bf16 into 3 further stages.
 //
 // MFMA operand layout (32x32x16): lane l holds 8 consecutive reduction values of row l % 32 of A
 // (resp. column l % 32 of B), starting at reduction index 8 (l / 32). Accumulator register r of
 // lane l holds C[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].
 //
 // Forward:  C = X_hat W_hat^T (rows = tokens, columns = out features). X_hat [M][K] and
-//           W_hat [N][K] are K-contiguous, so tiles are copied straight into LDS. The epilogue
+//           W_hat [N][K] are K-contiguous, so fragments are plain 16-byte LDS reads. The epilogue
 //           forms D = C - Y_ref, dY = D * 2/(M N) and per-column sums of D^2: a lane owns one
 //           column, so the column sums are in-lane plus one cross-lane add.
 // Backward: C = X_hat^T dY (rows = in features k, columns = out features n), i.e. G^T with the
-//           reduction over tokens. Both operands are token-major in memory, so each thread loads
-//           an 8 x 8 block and transposes it in registers before the LDS store. In the epilogue a
+//           reduction over tokens. Both operands are token-major in memory and are staged as they
+//           lie; transposing LDS reads (ds_read_b64_tr_b16) form the fragments. In the epilogue a
 //           lane holds 4 consecutive k of one n per register group, so a sub-block of 8 is an
 //           in-lane sum of 4 plus one exchange with lane l ^ 32, and a block of 32 is 16 in-lane
 //           values plus the same exchange.
@@ -54,7 +54,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, in
 // ---- forward operand staging: direct-to-LDS buffer loads ---------------------------------------
 // The forward operands are K-contiguous, so their tiles go from HBM / L2 straight into LDS with
 // buffer_load_dwordx4 ... lds (no VGPR round trip, no LDS store instructions). A step covers 32
-// of K; four 32 KB stages keep the loads of three steps in flight while one step is computed.
+// of K; five 32 KB stages (the default) keep up to three steps' loads in flight while one step is
+// computed and the next step's fragments are read.
 constexpr int kFwdStep = 32;
 constexpr int kFwdOpBytes = kTile * 64;   // 256 rows x 32 bf16 = 16 KB
 constexpr int kFwdStageBytes = 2 * kFwdOpBytes;
