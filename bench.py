@@ -36,6 +36,9 @@ def parse():
     p.add_argument("--summarize-mfma", metavar="DIR",
                    help="write the MFMA-utilisation summary from the rocprofv3 --pmc output directory of a "
                         "--steps 1 --warmup 0 --copy-calibration run with the counters of PMC_MFMA and exit")
+    p.add_argument("--summarize-stalls", metavar="DIR",
+                   help="write the wave-cycle breakdown of the GEMMs from the rocprofv3 --pmc output directory of a "
+                        "--steps 1 --warmup 0 run with the counters of PMC_STALL and exit")
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
@@ -112,13 +115,15 @@ def traffic_from_profile(kernel: str, src_hash: str, path=None):
 
 def main():
     args = parse()
-    if args.summarize_trace or args.summarize_counters or args.summarize_mfma:
+    if args.summarize_trace or args.summarize_counters or args.summarize_mfma or args.summarize_stalls:
         if args.summarize_trace:
             summarize_trace(args.summarize_trace, args.workload)
         if args.summarize_counters:
             summarize_counters(*args.summarize_counters, args.workload)
         if args.summarize_mfma:
             summarize_mfma(args.summarize_mfma, args.workload)
+        if args.summarize_stalls:
+            summarize_stalls(args.summarize_stalls, args.workload)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the data-parallel path across GPUs is not built "
@@ -546,6 +551,13 @@ PMC_MFMA = ("MfmaUtil SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_INSTS_VALU_MFM
             "SQ_BUSY_CYCLES SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE")  # pass as one --pmc argument list
 
 
+# where the GEMM waves' cycles go (8 SQ counters, one pass)
+PMC_STALL = ("SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_WAIT_INST_LDS SQ_ACTIVE_INST_LDS SQ_ACTIVE_INST_VMEM "
+             "SQ_LDS_DATA_FIFO_FULL SQ_LDS_CMD_FIFO_FULL")
+STALL_CMD = ("rocprofv3 --pmc {c} -d OUT/prof_stall -o run --output-format csv -- "
+             "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline")
+
+
 def algorithmic_bytes(kernel, M, N, K, sb):
     """Bytes each input is read and each output written once, per launch (one linear)."""
     grads = N * K // 32 * 4 + N * K // sb * 4
@@ -670,6 +682,42 @@ def summarize_mfma(pmc_dir, workload, out_dir=None):
             md.append(f"| `{k}` | {lin.N}x{lin.K} | {v['ns'] / 1e3:.0f} | {util:.1f}% | {ghz:.2f} | "
                       f"{mops / alg:.3f} | {tf:.0f} | {frac:.3f} | {frac * 2.4 / ghz if ghz else 0:.3f} | {100 * lds:.1f}% |")
     out = os.path.join(out_dir or os.path.join(REPO, "profiles"), f"mfma_util_{workload}.md")
+    with open(out, "w") as f:
+        f.write("\n".join(md) + "\n")
+    print(out)
+
+
+def summarize_stalls(pmc_dir, workload, out_dir=None):
+    import csv
+
+    from paper_2608_01847_amd import synth
+    w = synth.WORKLOADS[workload]
+    vals = {}
+    for r in csv.DictReader(open(os.path.join(pmc_dir, "run_counter_collection.csv"))):
+        d = vals.setdefault((int(r["Dispatch_Id"]), r["Kernel_Name"]), {})
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+        d["ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    cols = [("SQ_WAIT_ANY", "waiting (waitcnt, barrier)"), ("SQ_WAIT_INST_ANY", "waiting to issue"),
+            ("SQ_WAIT_INST_LDS", "waiting to issue LDS"), ("SQ_ACTIVE_INST_LDS", "issuing LDS"),
+            ("SQ_ACTIVE_INST_VMEM", "issuing VMEM"), ("SQ_LDS_CMD_FIFO_FULL", "LDS command FIFO full"),
+            ("SQ_LDS_DATA_FIFO_FULL", "LDS data FIFO full")]
+    md = [f"# Where the GEMM waves' cycles go ({workload}, {w.M:,} tokens)\n",
+          "Command (from the repository root on one MI355X; OUT is any output directory):\n",
+          "    " + STALL_CMD.format(c=PMC_STALL) + "\n",
+          "Per launch (one linear layer; the first launches of each kernel, the default step's): each counter as a "
+          "fraction of SQ_WAVE_CYCLES (cycles the kernel's waves are resident). With one wave per SIMD, a wave "
+          "waiting to issue is mostly its next MFMA waiting for the matrix unit; waiting on counters or the barrier "
+          "is time in which, unless MFMAs are still in flight, the unit idles. The columns overlap (an LDS or "
+          f"memory instruction issues while an MFMA runs). Source hash of the kernels: `{kernel_source_hash()}`.\n",
+          "| Kernel | Layer (N x K) | us | " + " | ".join(c for _, c in cols) + " |",
+          "|---|---|---|" + "---|" * len(cols)]
+    for k, pre in PROFILED.items():
+        runs = [v for (disp, name), v in sorted(vals.items()) if name.startswith(pre)][:len(w.linears)]
+        for v, lin in zip(runs, w.linears):
+            wc = max(v.get("SQ_WAVE_CYCLES", 0.0), 1.0)
+            md.append(f"| `{k}` | {lin.N}x{lin.K} | {v['ns'] / 1e3:.0f} | " +
+                      " | ".join(f"{100 * v.get(c, 0.0) / wc:.1f}%" for c, _ in cols) + " |")
+    out = os.path.join(out_dir or os.path.join(REPO, "profiles"), f"gemm_stalls_{workload}.md")
     with open(out, "w") as f:
         f.write("\n".join(md) + "\n")
     print(out)

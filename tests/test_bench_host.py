@@ -121,3 +121,15 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2
     assert "one GPU only" in r.stderr
     assert r.stdout == ""
+
+
+def test_stall_summary_row(tmp_path):
+    rows = [(30, BWD_MX, "SQ_WAVE_CYCLES", 1000.0, 5.0e5), (30, BWD_MX, "SQ_WAIT_ANY", 170.0, 5.0e5),
+            (30, BWD_MX, "SQ_WAIT_INST_ANY", 343.0, 5.0e5), (30, BWD_MX, "SQ_ACTIVE_INST_LDS", 125.0, 5.0e5)]
+    write_counter_csv(tmp_path / "s", rows)
+    bench.summarize_stalls(str(tmp_path / "s"), "block2560_mxfp4", out_dir=str(tmp_path))
+    text = (tmp_path / "gemm_stalls_block2560_mxfp4.md").read_text()
+    row = next(l for l in text.splitlines() if l.startswith("| `bwd_mfma_mx_kernel`"))
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    assert cells[2] == "500"
+    assert cells[3:7] == ["17.0%", "34.3%", "0.0%", "12.5%"]
