@@ -305,6 +305,11 @@ def main():
         "roofline": roofline,
         "fakequant_GBps": round(fq_bytes / (fq_ms * 1e-3) / 1e9, 1),
         "fakequant_frac_hbm": round(fq_bytes / (fq_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        # each family on its own: algorithmic bytes per element and GB/s against the HBM peak
+        "fakequant": {k: {"bytes_per_element": round(b, 4),
+                          "GBps": round(kern[k]["units"] * b / (kern[k]["total_ms"] * 1e-3) / 1e9, 1),
+                          "frac_hbm": round(kern[k]["units"] * b / (kern[k]["total_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}
+                      for k, b in (("fakequant_act", act_b), ("fakequant_weight", wt_b))},
         "gemm_TFLOPs": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
         "gemm_frac_bf16": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "gemm": gemm,
