@@ -287,7 +287,12 @@ def main():
     ms_per_step, kern = run(mx_fwd)
     per_step = sorted(run.per_step)
     block_loss = float(sum(L["loss"].item() for L in layers))
-    graph_ms, graph_loss = graph_run(mx_fwd)
+    try:
+        graph_ms, graph_loss = graph_run(mx_fwd)
+        graph_res = {"ms_per_step": round(graph_ms, 4), "replays": args.steps, "same_loss": graph_loss == block_loss}
+    except RuntimeError as e:  # the eager line stands on its own; report why the replay is missing
+        torch.cuda.synchronize()
+        graph_res = {"error": str(e).splitlines()[0][:200]}
 
     # ---- algorithmic work ----
     # fake quantisation bytes per element: activations read 2 + write 2 (bf16) (+2 for the NVFP4
@@ -353,7 +358,7 @@ def main():
                     "max": round(per_step[-1], 4)},
         "block_loss": block_loss,
         # the same step as one HIP graph (no per-call events, no launch gaps); same results
-        "graph": {"ms_per_step": round(graph_ms, 4), "replays": args.steps, "same_loss": graph_loss == block_loss},
+        "graph": graph_res,
         "source_hash": src_hash,
         "device": device_info(torch),
     }
