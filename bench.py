@@ -19,6 +19,7 @@ REPO = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, REPO)
 
 METRIC = "ms per fwd+bwd scale-learning step per decoder block; fake-quant GB/s"
+DEFAULT_WORKLOAD = "block2560_mxfp4"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_FP4_TFLOPS = 10100.0   # MI355X dense MXFP4 MFMA
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
@@ -42,7 +43,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
-    p.add_argument("--workload", default="block2560_mxfp4")
+    p.add_argument("--workload", default=DEFAULT_WORKLOAD)
     p.add_argument("--tokens", type=int, default=0, help="override the token count (0 = the workload's)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=32768)
@@ -586,9 +587,9 @@ PROFILED = {"bwd_mfma_mx_kernel": "void focus::bwd_mfma_mx_kernel<",
             "fwd_mfma_kernel": "void focus::fwd_mfma_kernel<true, false>",
             "bwd_mfma_kernel": "void focus::bwd_mfma_kernel<"}
 TRACE_CMD = ("rocprofv3 --kernel-trace --stats -d OUT/prof_trace -o run --output-format csv -- "
-             "python3 -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration")
+             "python3 -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration{wl}")
 PMC_CMD = ("rocprofv3 --pmc {c} -d OUT/prof_{d} -o run --output-format csv -- "
-           "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --copy-calibration")
+           "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --copy-calibration{wl}")
 
 
 # one counter pass (6 SQ and 1 GRBM counters, within what one rocprofv3 pass can collect on gfx950);
@@ -601,7 +602,12 @@ PMC_MFMA = ("MfmaUtil SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_INSTS_VALU_MFM
 PMC_STALL = ("SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_WAIT_INST_LDS SQ_ACTIVE_INST_LDS SQ_ACTIVE_INST_VMEM "
              "SQ_LDS_DATA_FIFO_FULL SQ_LDS_CMD_FIFO_FULL")
 STALL_CMD = ("rocprofv3 --pmc {c} -d OUT/prof_stall -o run --output-format csv -- "
-             "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline")
+             "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline{wl}")
+
+
+def wl_arg(workload):
+    """The --workload argument of a profiling command (none for the default workload)."""
+    return "" if workload == DEFAULT_WORKLOAD else f" --workload {workload}"
 
 
 def algorithmic_bytes(kernel, M, N, K, sb):
@@ -618,11 +624,11 @@ def summarize_trace(trace_dir, workload, out_dir=None):
     import csv
     rows = [r for r in csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv")))
             if "focus::" in r["Name"]]
-    out = os.path.join(out_dir or os.path.join(REPO, "profiles"),
-                       f"step_{workload.replace('_mxfp4', '')}_{workload.split('_')[-1]}_kernel_stats.md")
+    out = os.path.join(out_dir or os.path.join(REPO, "profiles"), f"step_{workload}_kernel_stats.md")
     with open(out, "w") as f:
         f.write(f"# Kernel-trace summary: scale-learning steps of the {workload} workload\n\n")
-        f.write("Command (from the repository root on one MI355X; OUT is any output directory):\n\n    " + TRACE_CMD + "\n\n")
+        f.write("Command (from the repository root on one MI355X; OUT is any output directory):\n\n    " +
+                TRACE_CMD.format(wl=wl_arg(workload)) + "\n\n")
         f.write("The run times the default step (2 warm-up + 5 timed) and then the same step with the other forward and "
                 "backward operands, and the calls outside the step (chaining, AdamW, export); library kernels only, "
                 f"source hash `{kernel_source_hash()}`:\n\n")
@@ -658,7 +664,8 @@ def summarize_counters(fetch_dir, write_dir, workload, out_dir=None):
                                      "read for it"}}
     md = [f"# HBM-side traffic of the reconstruction GEMMs ({workload}, {w.M:,} tokens)\n",
           "Commands (one counter per run, from the repository root on one MI355X; OUT is any output directory):\n",
-          "    " + PMC_CMD.format(c="FETCH_SIZE", d="fetch"), "    " + PMC_CMD.format(c="WRITE_SIZE", d="write") + "\n",
+          "    " + PMC_CMD.format(c="FETCH_SIZE", d="fetch", wl=wl_arg(workload)),
+          "    " + PMC_CMD.format(c="WRITE_SIZE", d="write", wl=wl_arg(workload)) + "\n",
           f"Calibration with the untimed 1 GiB device copy in the same runs: FETCH_SIZE reads {fraw:.0f} KiB (scale "
           f"{fscale:.3f}), WRITE_SIZE reads {wraw:.0f} KiB (scale {wscale:.3f}). The counters count L2 misses (traffic "
           f"to the Infinity Cache / HBM), per dispatch. Algorithmic bytes: every input read and every output written "
@@ -696,7 +703,7 @@ def summarize_mfma(pmc_dir, workload, out_dir=None):
     simds = 256 * 4
     md = [f"# MFMA utilisation of the reconstruction GEMMs ({workload}, {w.M:,} tokens)\n",
           "Command (from the repository root on one MI355X; OUT is any output directory):\n",
-          "    " + PMC_CMD.format(c=PMC_MFMA, d="mfma") + "\n",
+          "    " + PMC_CMD.format(c=PMC_MFMA, d="mfma", wl=wl_arg(workload)) + "\n",
           "Per launch (one linear layer), the first launches of each kernel in the run (the default step's). "
           "`MFMA busy` is rocprofv3's MfmaUtil: cycles in which a SIMD's matrix unit is busy, summed over the "
           "1,024 SIMDs, over GPU-busy cycles x 1,024. `clock` is the GPU-busy cycle count (the counter's maximum over "
@@ -749,7 +756,7 @@ def summarize_stalls(pmc_dir, workload, out_dir=None):
             ("SQ_LDS_DATA_FIFO_FULL", "LDS data FIFO full")]
     md = [f"# Where the GEMM waves' cycles go ({workload}, {w.M:,} tokens)\n",
           "Command (from the repository root on one MI355X; OUT is any output directory):\n",
-          "    " + STALL_CMD.format(c=PMC_STALL) + "\n",
+          "    " + STALL_CMD.format(c=PMC_STALL, wl=wl_arg(workload)) + "\n",
           "Per launch (one linear layer; the first launches of each kernel, the default step's): each counter as a "
           "fraction of SQ_WAVE_CYCLES (cycles the kernel's waves are resident). With one wave per SIMD, a wave "
           "waiting to issue is mostly its next MFMA waiting for the matrix unit; waiting on counters or the barrier "
