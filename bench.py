@@ -629,9 +629,10 @@ def summarize_trace(trace_dir, workload, out_dir=None):
         f.write(f"# Kernel-trace summary: scale-learning steps of the {workload} workload\n\n")
         f.write("Command (from the repository root on one MI355X; OUT is any output directory):\n\n    " +
                 TRACE_CMD.format(wl=wl_arg(workload)) + "\n\n")
-        f.write("The run times the default step (2 warm-up + 5 timed) and then the same step with the other forward and "
-                "backward operands, and the calls outside the step (chaining, AdamW, export); library kernels only, "
-                f"source hash `{kernel_source_hash()}`:\n\n")
+        other = (" and then the same step with the other forward and backward operands" if workload.endswith("_mxfp4")
+                 else "")
+        f.write(f"The run times the step (2 warm-up + 5 timed){other}, and the calls outside the step (chaining, "
+                f"AdamW, export); library kernels only, source hash `{kernel_source_hash()}`:\n\n")
         f.write("| Kernel | Calls | Avg us | Min us | Max us | Share of GPU time |\n|---|---|---|---|---|---|\n")
         for r in rows:
             name = r["Name"].replace("(anonymous namespace)::", "").split("(")[0].replace("void ", "")
