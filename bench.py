@@ -380,8 +380,10 @@ def main():
                         for k, v in alt_kern.items()}}
     result["chain"] = chain_costs(torch, F, layers, acts, x_hat, fmt, sb, M, ws_fwd, rnd)
     result["optimizer"] = optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws_fq, rnd, c_b)
+    big = max(w.linears, key=lambda l: l.N * l.K)
     result["attainable"] = attainable(torch, ms_gemm=gemm_flops / (gemm_ms * 1e-3) / 1e12,
-                                      fq_GBps=fq_bytes / (fq_ms * 1e-3) / 1e9)
+                                      fq_GBps=fq_bytes / (fq_ms * 1e-3) / 1e9,
+                                      layer=(M, big.N, big.K) if esz == 2 else None)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens, args.cpu_sample_rows)
     print(json.dumps(result), flush=True)
@@ -508,16 +510,25 @@ def cpu_model():
     return "unknown"
 
 
-def attainable(torch, ms_gemm, fq_GBps):
+def attainable(torch, ms_gemm, fq_GBps, layer=None):
     """Measured attainable rates on this GPU as secondary denominators (not the product's code): a
-    1 GiB device copy and a large bf16 library GEMM (torch.mm, 8192^3, random data)."""
+    1 GiB device copy, a large bf16 library GEMM (torch.mm, 8192^3, random data) and, for `layer`
+    = (M, N, K), the library GEMM on that layer's forward ([M][K] x [K][N]) and backward
+    ([K][M] x [M][N]) shapes, plain products without the fused epilogues."""
     src = torch.randn(1 << 28, device="cuda").to(torch.bfloat16)
     dst = torch.empty_like(src)
     a = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
     bt = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)  # contiguous operands only
     res = {}
-    for name, fn, work in (("copy", lambda: dst.copy_(src), 2 * src.numel() * 2),
-                           ("gemm", lambda: torch.mm(a, bt), 2 * 8192 ** 3)):
+    cases = [("copy", lambda: dst.copy_(src), 2 * src.numel() * 2), ("gemm", lambda: torch.mm(a, bt), 2 * 8192 ** 3)]
+    if layer:
+        M, N, K = layer
+        xf = torch.randn(M, K, device="cuda").to(torch.bfloat16)
+        wf = torch.randn(K, N, device="cuda").to(torch.bfloat16)
+        xb = torch.randn(K, M, device="cuda").to(torch.bfloat16)
+        yb = torch.randn(M, N, device="cuda").to(torch.bfloat16)
+        cases += [("layer_fwd", lambda: torch.mm(xf, wf), 2 * M * N * K), ("layer_bwd", lambda: torch.mm(xb, yb), 2 * M * N * K)]
+    for name, fn, work in cases:
         fn()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
@@ -529,8 +540,12 @@ def attainable(torch, ms_gemm, fq_GBps):
         res[name] = work / (e0.elapsed_time(e1) / 10 * 1e-3)
     del src, dst, a, bt
     copy_GBps, gemm_TF = res["copy"] / 1e9, res["gemm"] / 1e12
-    return {"copy_GBps": round(copy_GBps, 1), "library_bf16_gemm_TFLOPs": round(gemm_TF, 1),
-            "gemm_frac_of_library": round(ms_gemm / gemm_TF, 4), "fakequant_frac_of_copy": round(fq_GBps / copy_GBps, 4)}
+    out = {"copy_GBps": round(copy_GBps, 1), "library_bf16_gemm_TFLOPs": round(gemm_TF, 1),
+           "gemm_frac_of_library": round(ms_gemm / gemm_TF, 4), "fakequant_frac_of_copy": round(fq_GBps / copy_GBps, 4)}
+    if layer:
+        out["library_layer_gemm"] = {"shape_MNK": list(layer), "fwd_TFLOPs": round(res["layer_fwd"] / 1e12, 1),
+                                     "bwd_TFLOPs": round(res["layer_bwd"] / 1e12, 1)}
+    return out
 
 
 def cpu_baseline(w, sample_tokens, sample_rows):
