@@ -19,7 +19,7 @@ REPO = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, REPO)
 
 METRIC = "ms per fwd+bwd scale-learning step per decoder block; fake-quant GB/s"
-DEFAULT_WORKLOAD = "block2560_mxfp4"
+DEFAULT_WORKLOAD = "block8192_mxfp4"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_FP4_TFLOPS = 10100.0   # MI355X dense MXFP4 MFMA
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
@@ -62,14 +62,18 @@ def parse():
 
 
 class Timer:
-    """HIP events on the current stream around each library call, grouped by kernel family."""
+    """HIP events on the current stream around each library call, grouped by kernel family. With
+    `before`, before(name) runs ahead of each call's start event (untimed), e.g. a cache flush."""
 
-    def __init__(self, torch):
+    def __init__(self, torch, before=None):
         self.torch = torch
         self.spans = {}
+        self.before = before
 
     def run(self, name, fn, units):
         t = self.torch
+        if self.before is not None:
+            self.before(name)
         a, b = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
         a.record()
         out = fn()
@@ -101,9 +105,12 @@ def kernel_source_hash(csrc_dir=None):
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(kernel: str, src_hash: str, path=None):
+def traffic_path(workload):
+    return os.path.join(REPO, "profiles", f"traffic_{workload}.json")
+
+
+def traffic_from_profile(kernel: str, src_hash: str, path):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it is current."""
-    path = path or os.path.join(REPO, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -232,6 +239,25 @@ def main():
                                                    e8m0_rounding=rnd, out=(L["gs"], L["gc"])),
                           2 * M * lin.N * lin.K)
 
+    def cold_fakequant(mx_fwd, steps):
+        """The step again with the caches flushed before every fake-quant call: a fill kernel writes a
+        1 GiB buffer (4x the 256 MB Infinity Cache, far beyond the L2s) ahead of the call's start
+        event, so each call streams its tensors from HBM. Only the fake-quant spans are used."""
+        flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        count = [0]
+
+        def before(name):
+            if name.startswith("fakequant"):
+                count[0] += 1
+                flush.fill_(float(count[0]))
+
+        for _ in range(steps):
+            timer = Timer(torch, before)
+            step(timer, mx_fwd)
+        torch.cuda.synchronize()
+        del flush
+        return timer.summary()
+
     def run(mx_fwd):
         """Warm-up, then exactly args.steps timed steps; -> (ms per step, per-family summary)."""
         for _ in range(args.warmup):
@@ -288,6 +314,8 @@ def main():
     ms_per_step, kern = run(mx_fwd)
     per_step = sorted(run.per_step)
     block_loss = float(sum(L["loss"].item() for L in layers))
+    clocks = gpu_clocks()
+    kern_cold = cold_fakequant(mx_fwd, 2)
     try:
         graph_ms, graph_loss = graph_run(mx_fwd)
         graph_res = {"ms_per_step": round(graph_ms, 4), "replays": args.steps, "same_loss": graph_loss == block_loss}
@@ -306,8 +334,8 @@ def main():
     wt_b = esz + 4.0 / B + c_b + ((0.5 + 1.0 / 32) if mx_fwd else esz)
     fq_bytes = kern["fakequant_act"]["units"] * act_b + kern["fakequant_weight"]["units"] * wt_b
     fq_ms = kern["fakequant_act"]["total_ms"] + kern["fakequant_weight"]["total_ms"]
-    gemm_flops = kern["recon_gemm_fwd"]["units"] + kern["recon_gemm_bwd"]["units"]
-    gemm_ms = kern["recon_gemm_fwd"]["total_ms"] + kern["recon_gemm_bwd"]["total_ms"]
+    fq_cold_ms = kern_cold["fakequant_act"]["total_ms"] + kern_cold["fakequant_weight"]["total_ms"]
+    fq_cold_bytes = kern_cold["fakequant_act"]["units"] * act_b + kern_cold["fakequant_weight"]["units"] * wt_b
 
     if esz == 4:  # fp32 operands: the VALU kernels
         peaks = {"recon_gemm_fwd": PEAK_FP32_TFLOPS, "recon_gemm_bwd": PEAK_FP32_TFLOPS}
@@ -327,8 +355,8 @@ def main():
         kname = {"recon_gemm_fwd": "fwd_mfma_kernel_mx" if mx_fwd else "fwd_mfma_kernel",
                  "recon_gemm_bwd": "bwd_mfma_mx_kernel" if mx_fwd else "bwd_mfma_kernel"}[dominant]
     roofline = {"bound": "alu" if esz == 4 else "mfma", "achieved": round(achieved, 2), "peak": peaks[dominant],
-                "unit": "TFLOP/s",
-                "frac": round(achieved / peaks[dominant], 4), "traffic": traffic_from_profile(kname, src_hash),
+                "unit": "TFLOP/s", "frac": round(achieved / peaks[dominant], 4),
+                "traffic": traffic_from_profile(kname, src_hash, traffic_path(w.name)),
                 "kernel": kname, "avg_launch_ms": round(d["avg_ms"], 4), "launches": d["launches"],
                 "flops_per_launch": per_launch_flops}
 
@@ -345,13 +373,18 @@ def main():
         "roofline": roofline,
         "fakequant_GBps": round(fq_bytes / (fq_ms * 1e-3) / 1e9, 1),
         "fakequant_frac_hbm": round(fq_bytes / (fq_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
-        # each family on its own: algorithmic bytes per element and GB/s against the HBM peak
+        # each family on its own: algorithmic bytes per element and GB/s against the HBM peak, in the
+        # timed step and with the caches flushed before every call
         "fakequant": {k: {"bytes_per_element": round(b, 4),
                           "GBps": round(kern[k]["units"] * b / (kern[k]["total_ms"] * 1e-3) / 1e9, 1),
-                          "frac_hbm": round(kern[k]["units"] * b / (kern[k]["total_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}
+                          "frac_hbm": round(kern[k]["units"] * b / (kern[k]["total_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+                          "cold_GBps": round(kern_cold[k]["units"] * b / (kern_cold[k]["total_ms"] * 1e-3) / 1e9, 1),
+                          "cold_frac_hbm": round(kern_cold[k]["units"] * b / (kern_cold[k]["total_ms"] * 1e-3) / 1e9
+                                                 / PEAK_HBM_GBPS, 4)}
                       for k, b in (("fakequant_act", act_b), ("fakequant_weight", wt_b))},
-        "gemm_TFLOPs": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
-        "gemm_frac_bf16": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "fakequant_cold_GBps": round(fq_cold_bytes / (fq_cold_ms * 1e-3) / 1e9, 1),
+        "fakequant_cold_frac_hbm": round(fq_cold_bytes / (fq_cold_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        # each reconstruction GEMM against the peak of the MFMA it runs on
         "gemm": gemm,
         "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "total_ms_per_step": round(v["total_ms"] / args.steps, 4),
                         "launches_per_step": v["launches"] // args.steps} for k, v in kern.items()},
@@ -361,7 +394,7 @@ def main():
         # the same step as one HIP graph (no per-call events, no launch gaps); same results
         "graph": graph_res,
         "source_hash": src_hash,
-        "device": device_info(torch),
+        "device": device_info(torch, clocks),
     }
     if mx_possible:
         # the same step with the other forward operands, same inputs: under MXFP4, X_hat and W_hat
@@ -379,10 +412,12 @@ def main():
             "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "total_ms_per_step": round(v["total_ms"] / args.steps, 4)}
                         for k, v in alt_kern.items()}}
     result["chain"] = chain_costs(torch, F, layers, acts, x_hat, fmt, sb, M, ws_fwd, rnd)
-    result["optimizer"] = optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws_fq, rnd, c_b)
+    opt = optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws_fq, rnd, c_b)
+    result["optimizer"] = {"adamw": opt["adamw"]}
+    # the deployable export of every linear (Fig. 3(d)), timed on its own outside the step
+    result["export"] = opt["export"]
     big = max(w.linears, key=lambda l: l.N * l.K)
-    result["attainable"] = attainable(torch, ms_gemm=gemm_flops / (gemm_ms * 1e-3) / 1e12,
-                                      fq_GBps=fq_bytes / (fq_ms * 1e-3) / 1e9,
+    result["attainable"] = attainable(torch, fq_GBps=fq_bytes / (fq_ms * 1e-3) / 1e9,
                                       layer=(M, big.N, big.K) if esz == 2 else None)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens, args.cpu_sample_rows)
@@ -411,6 +446,21 @@ def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, rnd, c_b, reps=5
         for L, o in zip(layers, outs):
             F.export_packed(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws, out=o, e8m0_rounding=rnd)
 
+    def export_cold():
+        """Each layer's export with the caches flushed first (a 1 GiB fill kernel), summed over layers."""
+        flush = torch.empty(1 << 28, dtype=torch.float32, device=layers[0]["W"].device)
+        spans = []
+        for i, (L, o) in enumerate(zip(layers, outs)):
+            flush.fill_(float(i + 1))
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            F.export_packed(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws, out=o, e8m0_rounding=rnd)
+            b.record()
+            spans.append((a, b))
+        torch.cuda.synchronize()
+        del flush
+        return sum(a.elapsed_time(b) for a, b in spans)
+
     res = {}
     for name, fn in (("adamw", lambda t: adam_all(t)), ("export", lambda t: export_all())):
         fn(1)
@@ -422,6 +472,7 @@ def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, rnd, c_b, reps=5
         b.record()
         torch.cuda.synchronize()
         res[name] = a.elapsed_time(b) / reps
+    res["export_cold"] = min(export_cold() for _ in range(2))
     if F.check_flags(ws) != F.OK:
         raise RuntimeError("domain error in the optimizer step")
     for L, (s, c) in zip(layers, s0):  # leave the timed state as it was
@@ -434,9 +485,13 @@ def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, rnd, c_b, reps=5
     return {"adamw": {"ms_per_block": round(res["adamw"], 4), "params": n_params, "launches": 2 * len(layers),
                       "GBps": round(adam_bytes / (res["adamw"] * 1e-3) / 1e9, 1),
                       "frac_hbm": round(adam_bytes / (res["adamw"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
-            "export": {"ms_per_block": round(res["export"], 4), "weights": n_w,
+            "export": {"ms_per_block": round(res["export"], 4), "weights": n_w, "launches": len(layers),
+                       "bytes_per_weight": round(exp_bytes / n_w, 4), "scale_layout": "row-major",
                        "GBps": round(exp_bytes / (res["export"] * 1e-3) / 1e9, 1),
-                       "frac_hbm": round(exp_bytes / (res["export"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}}
+                       "frac_hbm": round(exp_bytes / (res["export"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+                       "cold_ms_per_block": round(res["export_cold"], 4),
+                       "cold_GBps": round(exp_bytes / (res["export_cold"] * 1e-3) / 1e9, 1),
+                       "cold_frac_hbm": round(exp_bytes / (res["export_cold"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}}
 
 
 def chain_costs(torch, F, layers, acts, x_hat, fmt, sb, M, ws, rnd, reps=3):
@@ -492,11 +547,26 @@ def chain_costs(torch, F, layers, acts, x_hat, fmt, sb, M, ws, rnd, reps=3):
                        "GBps": round(T * V * 6 / (res["kl_top"] * 1e-3) / 1e9, 1)}}
 
 
-def device_info(torch):
-    """What ran the measurement: the GPU, its architecture and CU count, the HIP runtime of torch."""
+def gpu_clocks():
+    """The GPU's clocks as rocm-smi reports them (current levels of sclk, mclk, fclk, socclk), or why
+    they could not be read."""
+    import subprocess
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True, timeout=30)
+        data = json.loads(r.stdout)
+    except Exception as e:  # noqa: BLE001 (reported, never fatal)
+        return {"error": str(e)[:120]}
+    card = next(iter(data.values()), {}) if isinstance(data, dict) else {}
+    return {k: v for k, v in card.items() if "clock" in k.lower() or "clk" in k.lower()}
+
+
+def device_info(torch, clocks=None):
+    """What ran the measurement: the GPU, its architecture and CU count, the HIP runtime of torch,
+    and the clocks rocm-smi reported right after the timed steps."""
     prop = torch.cuda.get_device_properties(0)
     return {"name": prop.name, "arch": getattr(prop, "gcnArchName", ""), "compute_units": prop.multi_processor_count,
-            "memory_GiB": round(prop.total_memory / 2 ** 30, 1), "hip": torch.version.hip}
+            "memory_GiB": round(prop.total_memory / 2 ** 30, 1), "hip": torch.version.hip,
+            "clocks_after_timed_steps": clocks}
 
 
 def cpu_model():
@@ -510,7 +580,7 @@ def cpu_model():
     return "unknown"
 
 
-def attainable(torch, ms_gemm, fq_GBps, layer=None):
+def attainable(torch, fq_GBps, layer=None):
     """Measured attainable rates on this GPU as secondary denominators (not the product's code): a
     1 GiB device copy, a large bf16 library GEMM (torch.mm, 8192^3, random data) and, for `layer`
     = (M, N, K), the library GEMM on that layer's forward ([M][K] x [K][N]) and backward
@@ -541,7 +611,7 @@ def attainable(torch, ms_gemm, fq_GBps, layer=None):
     del src, dst, a, bt
     copy_GBps, gemm_TF = res["copy"] / 1e9, res["gemm"] / 1e12
     out = {"copy_GBps": round(copy_GBps, 1), "library_bf16_gemm_TFLOPs": round(gemm_TF, 1),
-           "gemm_frac_of_library": round(ms_gemm / gemm_TF, 4), "fakequant_frac_of_copy": round(fq_GBps / copy_GBps, 4)}
+           "fakequant_frac_of_copy": round(fq_GBps / copy_GBps, 4)}
     if layer:
         out["library_layer_gemm"] = {"shape_MNK": list(layer), "fwd_TFLOPs": round(res["layer_fwd"] / 1e12, 1),
                                      "bwd_TFLOPs": round(res["layer_bwd"] / 1e12, 1)}
@@ -597,10 +667,15 @@ def cpu_baseline(w, sample_tokens, sample_rows):
 # ---- rocprofv3 summaries (host only) ------------------------------------------------------------
 # Library kernels by the name bench.py reports them under, and the rocprofv3 name prefix of each.
 # The commands below write into OUT, any output directory; the summaries are made from it.
-PROFILED = {"bwd_mfma_mx_kernel": "void focus::bwd_mfma_mx_kernel<",
-            "fwd_mfma_kernel_mx": "void focus::fwd_mfma_kernel<true, true>",
-            "fwd_mfma_kernel": "void focus::fwd_mfma_kernel<true, false>",
-            "bwd_mfma_kernel": "void focus::bwd_mfma_kernel<"}
+GEMM_KERNELS = {"bwd_mfma_mx_kernel": "void focus::bwd_mfma_mx_kernel<",
+                "fwd_mfma_kernel_mx": "void focus::fwd_mfma_kernel<true, true>",
+                "fwd_mfma_kernel": "void focus::fwd_mfma_kernel<true, false>",
+                "bwd_mfma_kernel": "void focus::bwd_mfma_kernel<"}
+FAKEQUANT_KERNELS = {"fq_act_mx_kernel": "void focus::fq_act_mx_kernel<",
+                     "absmax_partial_kernel": "void focus::absmax_partial_kernel<",
+                     "fq_act_nv_kernel": "void focus::fq_act_nv_kernel<",
+                     "fq_weight_kernel": "void focus::fq_weight_kernel<"}
+PROFILED = {**GEMM_KERNELS, **FAKEQUANT_KERNELS}
 TRACE_CMD = ("rocprofv3 --kernel-trace --stats -d OUT/prof_trace -o run --output-format csv -- "
              "python3 -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration{wl}")
 PMC_CMD = ("rocprofv3 --pmc {c} -d OUT/prof_{d} -o run --output-format csv -- "
@@ -625,14 +700,35 @@ def wl_arg(workload):
     return "" if workload == DEFAULT_WORKLOAD else f" --workload {workload}"
 
 
-def algorithmic_bytes(kernel, M, N, K, sb):
-    """Bytes each input is read and each output written once, per launch (one linear)."""
-    grads = N * K // 32 * 4 + N * K // sb * 4
-    wparams = 2 * N * K + N * K // 32 * 4 + N * K // sb * 4
+def algorithmic_bytes(kernel, M, N, K, sb, fmt=0):
+    """Bytes each input is read and each output written once, per launch: one linear for the GEMMs
+    (M tokens, N x K weights); for the fake-quant kernels one [N][K] bf16 tensor as the default step
+    runs them (MXFP4: activations and weights written as packed codes + E8M0 bytes; NVFP4: as bf16)."""
+    B = 32 if fmt == 0 else 16
+    grads = N * K // B * 4 + N * K // sb * 4
+    wparams = 2 * N * K + N * K // B * 4 + N * K // sb * 4
+    packed = N * (K // 2 + K // 32)
     return {"fwd_mfma_kernel": 2 * M * K + 2 * N * K + 4 * M * N,
             "fwd_mfma_kernel_mx": (M + N) * (K // 2 + K // 32) + 4 * M * N,
             "bwd_mfma_kernel": 2 * M * N + 2 * M * K + wparams + grads,
-            "bwd_mfma_mx_kernel": 2 * M * N + M * (K // 2 + K // 32) + wparams + grads}[kernel]
+            "bwd_mfma_mx_kernel": 2 * M * N + M * (K // 2 + K // 32) + wparams + grads,
+            "fq_act_mx_kernel": 2 * N * K + packed,
+            "absmax_partial_kernel": 2 * N * K,
+            "fq_act_nv_kernel": 4 * N * K,
+            "fq_weight_kernel": wparams + (packed if fmt == 0 else 2 * N * K)}[kernel]
+
+
+def step_launches(kernel, w):
+    """How a kernel's launches in a `--steps 1 --warmup 0` run map to tensors: (launches before the
+    step, [(label, rows, K)] of the step's launches in order). The step fake-quantises the four
+    block inputs, then each linear's weights; the NVFP4 weight initialisation runs one tensor-absmax
+    pass per linear before the step."""
+    if kernel in GEMM_KERNELS:
+        return 0, [(f"{l.N}x{l.K}", l.N, l.K) for l in w.linears]
+    if kernel == "fq_weight_kernel":
+        return 0, [(f"{l.name} {l.N}x{l.K}", l.N, l.K) for l in w.linears]
+    acts = [(f"{src} {w.M}x{K}", w.M, K) for src, K in w.inputs.items()]
+    return (len(w.linears) if kernel == "absmax_partial_kernel" else 0), acts
 
 
 def summarize_trace(trace_dir, workload, out_dir=None):
@@ -669,8 +765,11 @@ def summarize_counters(fetch_dir, write_dir, workload, out_dir=None):
         # the untimed 1 GiB device copy of --copy-calibration is the run's first copy kernel
         copy = next(r for r in rows if "copyBuffer" in r["Kernel_Name"])
         scale = (1 << 30) / (float(copy["Counter_Value"]) * 1024)
-        per = {k: [float(r["Counter_Value"]) * 1024 * scale for r in rows if r["Kernel_Name"].startswith(pre)][:len(w.linears)]
-               for k, pre in PROFILED.items()}
+        per = {}
+        for k, pre in PROFILED.items():
+            skip, shapes = step_launches(k, w)
+            vals = [float(r["Counter_Value"]) * 1024 * scale for r in rows if r["Kernel_Name"].startswith(pre)]
+            per[k] = vals[skip:skip + len(shapes)]
         runs[counter] = (scale, per, float(copy["Counter_Value"]))
     fscale, fetch, fraw = runs["FETCH_SIZE"]
     wscale, write, wraw = runs["WRITE_SIZE"]
@@ -678,27 +777,29 @@ def summarize_counters(fetch_dir, write_dir, workload, out_dir=None):
     data = {"_calibration": {"copy_bytes": 1 << 30, "fetch_scale": fscale, "write_scale": wscale,
                              "note": "scales = known bytes of a 1 GiB device copy / what FETCH_SIZE and WRITE_SIZE "
                                      "read for it"}}
-    md = [f"# HBM-side traffic of the reconstruction GEMMs ({workload}, {w.M:,} tokens)\n",
+    md = [f"# HBM-side traffic of the reconstruction GEMMs and fake-quant kernels ({workload}, {w.M:,} tokens)\n",
           "Commands (one counter per run, from the repository root on one MI355X; OUT is any output directory):\n",
           "    " + PMC_CMD.format(c="FETCH_SIZE", d="fetch", wl=wl_arg(workload)),
           "    " + PMC_CMD.format(c="WRITE_SIZE", d="write", wl=wl_arg(workload)) + "\n",
           f"Calibration with the untimed 1 GiB device copy in the same runs: FETCH_SIZE reads {fraw:.0f} KiB (scale "
           f"{fscale:.3f}), WRITE_SIZE reads {wraw:.0f} KiB (scale {wscale:.3f}). The counters count L2 misses (traffic "
           f"to the Infinity Cache / HBM), per dispatch. Algorithmic bytes: every input read and every output written "
-          f"once. Source hash of the kernels: `{src}`.\n",
-          "| Kernel | Layer (N x K) | fetched MB | written MB | algorithmic MB | ratio |", "|---|---|---|---|---|---|"]
+          f"once (fake-quant kernels: the default step's outputs, packed codes + E8M0 bytes under MXFP4, bf16 "
+          f"under NVFP4). Source hash of the kernels: `{src}`.\n",
+          "| Kernel | Tensor (rows x K) | fetched MB | written MB | algorithmic MB | ratio |", "|---|---|---|---|---|---|"]
     for k in PROFILED:
         if not fetch[k]:
             continue
         n = min(len(fetch[k]), len(write[k]))
         tot = [fetch[k][i] + write[k][i] for i in range(n)]
-        data[k] = {"bytes_per_launch": sum(tot) / n, "source_hash": src, "launches": n}
-        for i, lin in enumerate(w.linears[:n]):
-            alg = algorithmic_bytes(k, w.M, lin.N, lin.K, w.sub_block)
-            md.append(f"| `{k}` | {lin.N}x{lin.K} | {fetch[k][i] / 1e6:.0f} | {write[k][i] / 1e6:.0f} | {alg / 1e6:.0f} | "
-                      f"{tot[i] / alg:.2f} |")
+        algs = [algorithmic_bytes(k, w.M, rows, K, w.sub_block, w.fmt) for _, rows, K in step_launches(k, w)[1][:n]]
+        data[k] = {"bytes_per_launch": sum(tot) / n, "algorithmic_bytes_per_launch": sum(algs) / n,
+                   "source_hash": src, "launches": n}
+        for i, (label, rows, K) in enumerate(step_launches(k, w)[1][:n]):
+            md.append(f"| `{k}` | {label} | {fetch[k][i] / 1e6:.0f} | {write[k][i] / 1e6:.0f} | {algs[i] / 1e6:.0f} | "
+                      f"{tot[i] / algs[i]:.2f} |")
     out_dir = out_dir or os.path.join(REPO, "profiles")
-    with open(os.path.join(out_dir, "traffic.json"), "w") as f:
+    with open(os.path.join(out_dir, f"traffic_{workload}.json"), "w") as f:
         json.dump(data, f, indent=1)
     out = os.path.join(out_dir, f"hbm_traffic_{workload}.md")
     with open(out, "w") as f:
@@ -734,7 +835,7 @@ def summarize_mfma(pmc_dir, workload, out_dir=None):
           f"conflict cycles / LDS-active cycles. Source hash of the kernels: `{kernel_source_hash()}`.\n",
           "| Kernel | Layer (N x K) | us | MFMA busy | clock GHz | executed / algorithmic | TFLOP/s | frac of peak | "
           "frac at the clock | LDS conflicts |", "|---|---|---|---|---|---|---|---|---|---|"]
-    for k, pre in PROFILED.items():
+    for k, pre in GEMM_KERNELS.items():
         runs = [(disp, v) for (disp, name), v in sorted(vals.items()) if name.startswith(pre)][:len(w.linears)]
         fp4 = k == "fwd_mfma_kernel_mx"
         peak = PEAK_FP4_TFLOPS if fp4 else PEAK_BF16_TFLOPS
@@ -780,7 +881,7 @@ def summarize_stalls(pmc_dir, workload, out_dir=None):
           f"memory instruction issues while an MFMA runs). Source hash of the kernels: `{kernel_source_hash()}`.\n",
           "| Kernel | Layer (N x K) | us | " + " | ".join(c for _, c in cols) + " |",
           "|---|---|---|" + "---|" * len(cols)]
-    for k, pre in PROFILED.items():
+    for k, pre in GEMM_KERNELS.items():
         runs = [v for (disp, name), v in sorted(vals.items()) if name.startswith(pre)][:len(w.linears)]
         for v, lin in zip(runs, w.linears):
             wc = max(v.get("SQ_WAVE_CYCLES", 0.0), 1.0)

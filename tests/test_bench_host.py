@@ -25,6 +25,25 @@ def test_algorithmic_bytes_per_tensor():
     # the backward reads dY, X_hat and W with its scales and coefficients, and writes both gradients
     assert bench.algorithmic_bytes("bwd_mfma_kernel", M, N, K, sb) == dy + x_bf16 + w_bf16 + s_fp + coeff + grad_s + grad_c
     assert bench.algorithmic_bytes("bwd_mfma_mx_kernel", M, N, K, sb) == dy + x_packed + w_bf16 + s_fp + coeff + grad_s + grad_c
+    # fake quantisation of one [N][K] bf16 tensor as the default steps run it
+    assert bench.algorithmic_bytes("fq_act_mx_kernel", M, N, K, sb) == w_bf16 + w_packed
+    assert bench.algorithmic_bytes("fq_weight_kernel", M, N, K, sb) == w_bf16 + s_fp + coeff + w_packed
+    nv_s = 4 * N * K // 16
+    assert bench.algorithmic_bytes("fq_weight_kernel", M, N, K, sb, fmt=1) == w_bf16 + nv_s + coeff + w_bf16
+    assert bench.algorithmic_bytes("fq_act_nv_kernel", M, N, K, sb, fmt=1) == 2 * w_bf16
+    assert bench.algorithmic_bytes("absmax_partial_kernel", M, N, K, sb, fmt=1) == w_bf16
+
+
+def test_step_launch_map():
+    from paper_2608_01847_amd import synth
+    w = synth.WORKLOADS["block8192_mxfp4"]
+    skip, shapes = bench.step_launches("fq_act_mx_kernel", w)
+    assert skip == 0 and [s[1:] for s in shapes] == [(w.M, K) for K in w.inputs.values()]
+    skip, shapes = bench.step_launches("fq_weight_kernel", w)
+    assert skip == 0 and [s[1:] for s in shapes] == [(l.N, l.K) for l in w.linears]
+    # NVFP4: the weights' tensor-absmax passes (one per linear) run before the step
+    skip, shapes = bench.step_launches("absmax_partial_kernel", synth.WORKLOADS["block2560_nvfp4"])
+    assert skip == 7 and len(shapes) == 4
 
 
 def test_source_hash_ignores_comments_not_code(tmp_path):
@@ -78,7 +97,7 @@ def test_counter_summary_scales_by_the_copy(tmp_path):
     out = tmp_path / "out"
     out.mkdir()
     bench.summarize_counters(str(tmp_path / "f"), str(tmp_path / "w"), "block2560_mxfp4", out_dir=str(out))
-    data = json.loads((out / "traffic.json").read_text())
+    data = json.loads((out / "traffic_block2560_mxfp4.json").read_text())
     assert data["_calibration"]["fetch_scale"] == pytest.approx(2.0)
     assert data["_calibration"]["write_scale"] == pytest.approx(1.0)
     want = sum(1000.0 * (i + 1) * 1024 * 2 + 10.0 * 1024 for i in range(7)) / 7
@@ -86,6 +105,27 @@ def test_counter_summary_scales_by_the_copy(tmp_path):
     assert data["bwd_mfma_mx_kernel"]["source_hash"] == bench.kernel_source_hash()
     assert "fwd_mfma_kernel" not in data  # no rows, no entry
     assert (out / "hbm_traffic_block2560_mxfp4.md").exists()
+
+
+FQ_ACT = "void focus::fq_act_mx_kernel<1, 1>(void const*, unsigned int)"
+
+
+def test_counter_summary_maps_fakequant_launches(tmp_path):
+    from paper_2608_01847_amd import synth
+    w = synth.WORKLOADS["block2560_mxfp4"]
+    # one launch per block input in the step (4), then later launches that must be ignored
+    fetch = [(1, COPY, "FETCH_SIZE", 524288.0, 10)] + [(10 + i, FQ_ACT, "FETCH_SIZE", 100.0, 10) for i in range(6)]
+    write = [(1, COPY, "WRITE_SIZE", 1048576.0, 10)] + [(10 + i, FQ_ACT, "WRITE_SIZE", 50.0, 10) for i in range(6)]
+    write_counter_csv(tmp_path / "f", fetch)
+    write_counter_csv(tmp_path / "w", write)
+    bench.summarize_counters(str(tmp_path / "f"), str(tmp_path / "w"), "block2560_mxfp4", out_dir=str(tmp_path))
+    data = json.loads((tmp_path / "traffic_block2560_mxfp4.json").read_text())
+    assert data["fq_act_mx_kernel"]["launches"] == 4
+    assert data["fq_act_mx_kernel"]["bytes_per_launch"] == pytest.approx((100.0 * 2 + 50.0) * 1024)
+    algs = [bench.algorithmic_bytes("fq_act_mx_kernel", w.M, w.M, K, 8) for K in w.inputs.values()]
+    assert data["fq_act_mx_kernel"]["algorithmic_bytes_per_launch"] == pytest.approx(sum(algs) / 4)
+    text = (tmp_path / "hbm_traffic_block2560_mxfp4.md").read_text()
+    assert sum(l.startswith("| `fq_act_mx_kernel`") for l in text.splitlines()) == 4
 
 
 def test_mfma_summary_row(tmp_path):

@@ -7,7 +7,8 @@ on the GPU with the seeded inputs at their real shapes:
     perturbed state), and for the hidden-8192 block the exported packed codes and scale bytes;
   * loss and straight-through gradients on sampled output rows (first, last, 30 seeded rows and
     rows holding injected weight outliers), against the oracle computed row by row (loss and
-    gradients of an output row depend only on that row), within 2e-2 relative;
+    gradients of an output row depend only on that row), within 2e-2 relative, at the initial
+    state (absmax S_fp, c = 1: the state the benchmark times) and at a perturbed one;
   * for the MXFP4 blocks also the packed-operand step the benchmark times there: activation codes
     and block-major E8M0 bytes without X_hat and the weights' export, bit-exact against the
     oracle's codes and scale bytes; the FP4-MFMA forward and the backward from the packed
@@ -27,6 +28,8 @@ CASES = [
     ("block2560_nvfp4", "q_proj"), ("block2560_nvfp4", "down_proj"),
     ("block4096_mxfp4", "v_proj"), ("block4096_mxfp4", "o_proj"),
     ("block8192_mxfp4", "k_proj"), ("block8192_mxfp4", "gate_proj"),
+    # the largest K of any workload (and the largest per-launch offsets)
+    ("block4096_mxfp4", "down_proj"), ("block8192_mxfp4", "down_proj"),
 ]
 
 
@@ -90,6 +93,38 @@ def test_fullsize_layer(F, O, name, layer):
     s_d, c_d, a_d = F.scales_init(W, fmt, sb)
     s_o, c_o, a_o = O.init_scales(Wh, fmt, sb)
     assert_bits_equal(s_d.cpu().numpy().view(np.uint32), s_o.view(np.uint32), "s_fp init")
+    assert np.all(c_d.cpu().numpy() == 1.0) and np.all(c_o == 1.0)
+    rows = sample_rows(lin.N, outl, 5)
+    Yr = host_f32(Y[:, torch.from_numpy(rows).cuda()])
+    X_op = xo if mx else O.gemm_operand(xo, True)  # MXFP4 operands are bf16-exact already
+
+    # the initial state: loss and gradients on the sampled rows, through the path the benchmark times
+    # (packed operands under MXFP4, bf16 operands under NVFP4)
+    announce(f"fullsize init state {name} {layer}")
+    fq0 = O.fq_weight(Wh, fmt, sb, s_o, c_o, a_o)
+    res0 = O.recon_layer(X_op, fq0.w_hat if mx else O.gemm_operand(fq0.w_hat, True), None, fq0, fmt, sb, a_o,
+                         rows=rows, y_ref_cols=Yr)
+    if mx:
+        bm = F.SCALES_BLOCK_MAJOR
+        _, xc0, xs0, _ = F.fakequant_fwd(X, fmt, sb, want_codes=True, want_scale_bytes=True, want_x_hat=False,
+                                         scale_layout=bm)
+        wc0, ws0 = F.export_packed(W, fmt, sb, s_d, c_d, a_d, scale_layout=bm)
+        dY0, loss0, col0 = F.recon_gemm_fwd_mxfp4(xc0, xs0, wc0, ws0, Y, want_col_sq=True)
+        gs0, gc0 = F.recon_gemm_bwd_mxfp4(dY0, xc0, xs0, W, sb, s_d, c_d)
+        del xc0, xs0, wc0, ws0
+    else:
+        w_hat0, _, _, _ = F.fakequant_fwd(W, fmt, sb, s_d, c_d, a_d)
+        dY0, loss0, col0 = F.recon_gemm_fwd(x_hat, w_hat0, Y, want_col_sq=True)
+        gs0, gc0, _ = F.recon_gemm_bwd(dY0, x_hat, W, fmt, sb, s_d, c_d, a_d)
+        del w_hat0
+    torch.cuda.synchronize()
+    col0 = col0.cpu().numpy()
+    assert_close(col0[rows], res0.col_sq, TOL, "col_sq (init)")
+    assert abs(loss0.item() - col0.sum() / (w.M * lin.N)) <= 1e-9 * loss0.item()
+    assert_close(host_f32(gs0)[rows], res0.grad_s, TOL, "grad_s (init)")
+    assert_close(host_f32(gc0)[rows], res0.grad_c, TOL, "grad_c (init)")
+    del dY0, res0, fq0
+
     rng = np.random.default_rng(11)
     s_o = (s_o * np.exp2(rng.uniform(-0.5, 0.5, s_o.shape))).astype(np.float32)
     c_o = rng.uniform(0.75, 1.25, c_o.shape).astype(np.float32)
@@ -108,12 +143,8 @@ def test_fullsize_layer(F, O, name, layer):
     dY, loss, col_sq = F.recon_gemm_fwd(x_hat, w_hat, Y, want_col_sq=True)
     gs, gc, _ = F.recon_gemm_bwd(dY, x_hat, W, fmt, sb, s_d, c_d, a_d)
     torch.cuda.synchronize()
-    rows = sample_rows(lin.N, outl, 5)
-    # MXFP4 operands are bf16-exact already (checked above), so rounding them would be the identity
-    X_op = xo if mx else O.gemm_operand(xo, True)
     del xo
     W_op = fq.w_hat if mx else O.gemm_operand(fq.w_hat, True)
-    Yr = host_f32(Y[:, torch.from_numpy(rows).cuda()])
     res = O.recon_layer(X_op, W_op, None, fq, fmt, sb, a_o, rows=rows, y_ref_cols=Yr)
     col = col_sq.cpu().numpy()  # float64
     assert_close(col[rows], res.col_sq, TOL, "col_sq")
