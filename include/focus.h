@@ -48,7 +48,8 @@ typedef enum {
     FOCUS_ERR_CONFIG = 4,    /* bad focus_qconfig (format, sub_block, ste_clip, scale_layout, e8m0_rounding) */
     FOCUS_ERR_WORKSPACE = 5, /* workspace NULL, misaligned or smaller than focus_workspace_size() */
     FOCUS_ERR_DOMAIN = 6,    /* focus_check_flags: a kernel met a NaN scale or a c <= 0 / non-finite */
-    FOCUS_ERR_HIP = 7        /* the HIP runtime reported an error */
+    FOCUS_ERR_HIP = 7,       /* the HIP runtime reported an error */
+    FOCUS_ERR_SCRATCH = 8    /* focus_recon_gemm_fwd_mxfp4_noalloc: the sizes need more than its fixed scratch */
 } focus_status;
 
 typedef enum { FOCUS_MXFP4 = 0, FOCUS_NVFP4 = 1 } focus_format;
@@ -172,6 +173,21 @@ focus_status focus_recon_gemm_fwd_mxfp4(const uint8_t *X_codes, const uint8_t *X
                                         const uint8_t *W_scales, int64_t M, int64_t N, int64_t K,
                                         const void *Y_ref, void *dY, double *loss_out, double *col_sq_opt,
                                         void *ws, size_t ws_bytes, focus_stream stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): focus_recon_gemm_fwd_mxfp4 without a workspace argument. Same
+ * arguments, checks, kernels and results (bit for bit); the scratch the forward needs lives in a
+ * fixed 32 MiB device array of the library, one per GPU, held until the process ends. The call
+ * allocates and frees nothing. Sizes are limited by that array:
+ *   256 + 8 * (ceil(M / 256) * N + (col_sq_opt ? 0 : N))  <=  32 MiB
+ * (every layer up to N = 16,320 at 65,536 tokens); larger sizes return FOCUS_ERR_SCRATCH and launch
+ * nothing. The array keeps the last call's contents, none of which a call reads before writing it.
+ * Calls that overlap on one GPU (on different streams, or from different threads) race on it; calls
+ * on one stream are ordered. The first call on each GPU looks up that GPU's copy of the array. */
+focus_status focus_recon_gemm_fwd_mxfp4_noalloc(const uint8_t *X_codes, const uint8_t *X_scales,
+                                                const uint8_t *W_codes, const uint8_t *W_scales, int64_t M, int64_t N,
+                                                int64_t K, const void *Y_ref, void *dY, double *loss_out,
+                                                double *col_sq_opt, focus_stream stream);
 
 /* Reconstruction GEMM backward with the fused straight-through epilogue.
  *   G = dY^T X_hat ([N][K], the reduction runs over the M tokens, fp32 accumulation) is formed

@@ -7,6 +7,7 @@
 
 #include <cmath>
 #include <initializer_list>
+#include <mutex>
 
 using namespace focus;
 
@@ -80,6 +81,63 @@ size_t bwd_ws(int fmt, int sb, int64_t M, int64_t N, int64_t K) {
         focus_status s_ = (x);        \
         if (s_ != FOCUS_OK) return s_; \
     } while (0)
+
+// argument checks shared by the two entry points of the forward from packed MXFP4 operands
+focus_status check_fwd_mx_args(const uint8_t *X_codes, const uint8_t *X_scales, const uint8_t *W_codes,
+                               const uint8_t *W_scales, int64_t M, int64_t N, int64_t K, const void *Y_ref,
+                               const void *dY, const double *loss_out) {
+    if (!X_codes || !X_scales || !W_codes || !W_scales || !dY) return FOCUS_ERR_NULL;
+    if (Y_ref && !loss_out) return FOCUS_ERR_NULL;
+    if (M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return FOCUS_ERR_SHAPE;
+    if (K % 128 != 0 || N % 8 != 0 || M % 4 != 0) return FOCUS_ERR_SHAPE;
+    if ((M > 0 && K > kMaxElems / M) || (N > 0 && K > kMaxElems / N) || (M > 0 && N > kMaxElems / M))
+        return FOCUS_ERR_SHAPE;
+    if (!all_aligned({X_codes, W_codes, Y_ref, dY})) return FOCUS_ERR_SHAPE;
+    if ((reinterpret_cast<uintptr_t>(X_scales) | reinterpret_cast<uintptr_t>(W_scales)) & 3u) return FOCUS_ERR_SHAPE;
+    return FOCUS_OK;
+}
+
+// ---- fixed device scratch of the allocation-free forward ---------------------------------------
+// 32 MiB per GPU: the kWsHeader bytes the workspace layout skips, ceil(M / 256) x N partial sums of
+// D^2 (fp64) and, when the caller passes no col_sq, N column sums. Every hidden-2560 layer at 65,536
+// tokens fits (at most 20 MB).
+constexpr size_t kNoAllocScratchBytes = size_t(32) << 20;
+
+size_t noalloc_fwd_scratch_bytes(int64_t M, int64_t N, bool have_col_sq) {
+    const size_t mtiles = (size_t)((M + kMfmaTileM - 1) / kMfmaTileM);
+    return kWsHeader + (mtiles * (size_t)N + (have_col_sq ? 0 : (size_t)N)) * sizeof(double);
+}
+
+}  // namespace
+
+// One copy per GPU, held until the process ends, shared by every call on that GPU (calls that
+// overlap on one GPU race). In host code this name stands for a host-side shadow, not a device
+// address: only the address scratch_address() looks up may reach a kernel or a copy.
+static __device__ __align__(256) double scratch[kNoAllocScratchBytes / sizeof(double)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices];
+
+// Device address of `scratch` on the current device, looked up once per device with that device
+// current (each GPU holds its own copy at its own address).
+hipError_t scratch_address(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
 
 }  // namespace
 
@@ -192,19 +250,29 @@ focus_status focus_recon_gemm_fwd_mxfp4(const uint8_t *X_codes, const uint8_t *X
                                         const uint8_t *W_scales, int64_t M, int64_t N, int64_t K,
                                         const void *Y_ref, void *dY, double *loss_out, double *col_sq_opt,
                                         void *ws, size_t ws_bytes, focus_stream stream) {
-    if (!X_codes || !X_scales || !W_codes || !W_scales || !dY) return FOCUS_ERR_NULL;
-    if (Y_ref && !loss_out) return FOCUS_ERR_NULL;
-    if (M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return FOCUS_ERR_SHAPE;
-    if (K % 128 != 0 || N % 8 != 0 || M % 4 != 0) return FOCUS_ERR_SHAPE;
-    if ((M > 0 && K > kMaxElems / M) || (N > 0 && K > kMaxElems / N) || (M > 0 && N > kMaxElems / M))
-        return FOCUS_ERR_SHAPE;
-    if (!all_aligned({X_codes, W_codes, Y_ref, dY})) return FOCUS_ERR_SHAPE;
-    if ((reinterpret_cast<uintptr_t>(X_scales) | reinterpret_cast<uintptr_t>(W_scales)) & 3u) return FOCUS_ERR_SHAPE;
+    FOCUS_TRY(check_fwd_mx_args(X_codes, X_scales, W_codes, W_scales, M, N, K, Y_ref, dY, loss_out));
     FOCUS_TRY(check_ws(ws, ws_bytes, fwd_ws(M, N, K)));
     if (M == 0 || N == 0) return FOCUS_OK;
     if (!mfma_fwd_mx_supported(M, N, K)) return FOCUS_ERR_SHAPE;
     return hip_status(launch_recon_fwd_mx(X_codes, X_scales, W_codes, W_scales, M, N, K, Y_ref, dY, loss_out,
                                           col_sq_opt, ws, (hipStream_t)stream));
+}
+
+focus_status focus_recon_gemm_fwd_mxfp4_noalloc(const uint8_t *X_codes, const uint8_t *X_scales,
+                                                const uint8_t *W_codes, const uint8_t *W_scales, int64_t M, int64_t N,
+                                                int64_t K, const void *Y_ref, void *dY, double *loss_out,
+                                                double *col_sq_opt, focus_stream stream) {
+    FOCUS_TRY(check_fwd_mx_args(X_codes, X_scales, W_codes, W_scales, M, N, K, Y_ref, dY, loss_out));
+    if (noalloc_fwd_scratch_bytes(M, N, col_sq_opt != nullptr) > kNoAllocScratchBytes) return FOCUS_ERR_SCRATCH;
+    if (M == 0 || N == 0) return FOCUS_OK;
+    if (!mfma_fwd_mx_supported(M, N, K)) return FOCUS_ERR_SHAPE;
+    void *ptr = nullptr;
+    if (scratch_address(&ptr) != hipSuccess) return FOCUS_ERR_HIP;
+    // the scratch takes the place of the workspace: its first kWsHeader bytes are left unused, then
+    // the per-(m-tile, column) partial sums and, without col_sq_opt, the column sums; the kernels
+    // write all of it before it is read, so nothing is cleared
+    return hip_status(launch_recon_fwd_mx(X_codes, X_scales, W_codes, W_scales, M, N, K, Y_ref, dY, loss_out,
+                                          col_sq_opt, ptr, (hipStream_t)stream));
 }
 
 focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const void *X_hat, int op_dtype,
@@ -363,6 +431,7 @@ const char *focus_status_string(int status) {
         case FOCUS_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
         case FOCUS_ERR_DOMAIN: return "a kernel met a NaN scale or a coefficient c <= 0 or not finite";
         case FOCUS_ERR_HIP: return "HIP runtime error";
+        case FOCUS_ERR_SCRATCH: return "the sizes need more scratch than the allocation-free call's fixed 32 MiB";
         default: return "unknown status";
     }
 }

@@ -19,10 +19,11 @@ CALL_SCALES_INIT, CALL_FAKEQUANT_FWD, CALL_FAKEQUANT_BWD = 0, 1, 2
 CALL_RECON_GEMM_FWD, CALL_RECON_GEMM_BWD, CALL_EXPORT_PACKED, CALL_ADAMW = 3, 4, 5, 6
 CALL_RECON_GEMM_DX, CALL_FAKEQUANT_ACT_BWD, CALL_KL_TOP = 7, 8, 9
 
-OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_CONFIG, ERR_WORKSPACE, ERR_DOMAIN, ERR_HIP = range(8)
+OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_CONFIG, ERR_WORKSPACE, ERR_DOMAIN, ERR_HIP, ERR_SCRATCH = range(9)
 
 EXPORTED = ("focus_workspace_size", "focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd",
-            "focus_recon_gemm_fwd", "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd",
+            "focus_recon_gemm_fwd", "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_fwd_mxfp4_noalloc",
+            "focus_recon_gemm_bwd",
             "focus_recon_gemm_bwd_mxfp4", "focus_export_packed", "focus_recon_gemm_dx", "focus_fakequant_act_bwd",
             "focus_kl_top", "focus_adamw_step", "focus_check_flags", "focus_status_string")
 
@@ -62,6 +63,7 @@ def lib() -> ctypes.CDLL:
         L.focus_fakequant_bwd.argtypes = [q, p, i64, i64, p, i32, p, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_fwd.argtypes = [p, p, i32, i64, i64, i64, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_fwd_mxfp4.argtypes = [p, p, p, p, i64, i64, i64, p, p, p, p, p, sz, p]
+        L.focus_recon_gemm_fwd_mxfp4_noalloc.argtypes = [p, p, p, p, i64, i64, i64, p, p, p, p, p]
         L.focus_recon_gemm_bwd.argtypes = [q, p, p, i32, i64, i64, i64, p, i32, p, p, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_bwd_mxfp4.argtypes = [q, p, p, p, i64, i64, i64, p, i32, p, p, p, p, p, sz, p]
         L.focus_export_packed.argtypes = [q, p, i32, i64, i64, p, p, p, p, p, p, sz, p]
@@ -73,7 +75,8 @@ def lib() -> ctypes.CDLL:
         L.focus_status_string.argtypes = [i32]
         L.focus_status_string.restype = ctypes.c_char_p
         for name in ("focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd", "focus_recon_gemm_fwd",
-                     "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_bwd", "focus_recon_gemm_bwd_mxfp4",
+                     "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_fwd_mxfp4_noalloc", "focus_recon_gemm_bwd",
+                     "focus_recon_gemm_bwd_mxfp4",
                      "focus_export_packed", "focus_adamw_step", "focus_check_flags", "focus_recon_gemm_dx", "focus_fakequant_act_bwd",
                      "focus_kl_top"):
             getattr(L, name).restype = ctypes.c_int
@@ -239,6 +242,22 @@ def recon_gemm_fwd_mxfp4(X_codes: torch.Tensor, X_scales: torch.Tensor, W_codes:
                                             _stream()),
            "focus_recon_gemm_fwd_mxfp4")
     return dY, loss_t, col_sq
+
+
+def recon_gemm_fwd_mxfp4_noalloc(X_codes: torch.Tensor, X_scales: torch.Tensor, W_codes: torch.Tensor,
+                                 W_scales: torch.Tensor, Y_ref=None, col_sq=None, out=None, loss=None):
+    """recon_gemm_fwd_mxfp4 without a workspace (the library's fixed device scratch instead). The
+    library allocates nothing; the caller passes dY (`out`), `loss` when Y_ref is given, and
+    optionally `col_sq` [N] float64. -> (dY, loss, col_sq)."""
+    M, K = X_codes.shape[0], X_codes.shape[1] * 2
+    N = W_codes.shape[0]
+    if out is None or (Y_ref is not None and loss is None):
+        raise ValueError("recon_gemm_fwd_mxfp4_noalloc: pass the outputs (out, and loss with Y_ref)")
+    _check(lib().focus_recon_gemm_fwd_mxfp4_noalloc(_ptr(X_codes), _ptr(X_scales), _ptr(W_codes), _ptr(W_scales),
+                                                    M, N, K, _ptr(Y_ref), _ptr(out), _ptr(loss), _ptr(col_sq),
+                                                    _stream()),
+           "focus_recon_gemm_fwd_mxfp4_noalloc")
+    return out, loss, col_sq
 
 
 def recon_gemm_bwd(dY: torch.Tensor, X_hat: torch.Tensor, W: torch.Tensor, fmt: int, sub_block: int, s_fp,

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_status_strings(L):
-    for s in range(8):
+    for s in range(9):
         assert focus.status_string(s) and focus.status_string(s) != "unknown status"
     assert focus.status_string(99) == "unknown status"
 
@@ -127,6 +127,23 @@ def test_argument_checks(L, cpu_only):
                1 << 30, None) == focus.ERR_SHAPE  # scale bytes not 4-byte aligned
     assert mxf(BOGUS, BOGUS, BOGUS, BOGUS, 8, 8, 128, None, BOGUS, None, None, BOGUS, 16,
                None) == focus.ERR_WORKSPACE
+    # its allocation-free variant: the same argument checks, then the fixed 32 MiB scratch bounds the sizes
+    # (256 + 8 (ceil(M / 256) N + N) bytes, the column sums dropped when the caller passes col_sq)
+    nal = L.focus_recon_gemm_fwd_mxfp4_noalloc
+    assert nal(BOGUS, BOGUS, BOGUS, BOGUS, 8, 8, 64, None, BOGUS, None, None, None) == focus.ERR_SHAPE
+    assert nal(BOGUS, BOGUS, BOGUS, BOGUS, 8, 12, 128, None, BOGUS, None, None, None) == focus.ERR_SHAPE
+    assert nal(BOGUS, None, BOGUS, BOGUS, 8, 8, 128, None, BOGUS, None, None, None) == focus.ERR_NULL
+    assert nal(BOGUS, BOGUS, BOGUS, BOGUS, 8, 8, 128, BOGUS, BOGUS, None, None, None) == focus.ERR_NULL
+    limit = 32 << 20
+    M = 65536                      # 256 m-tiles
+    n_max = (limit - 256) // 8 // (256 + 1) // 8 * 8
+    assert 256 + 8 * (256 * n_max + n_max) <= limit < 256 + 8 * (256 * (n_max + 8) + n_max + 8)
+    assert nal(BOGUS, BOGUS, BOGUS, BOGUS, M, n_max + 8, 128, BOGUS, BOGUS, BOGUS, None, None) == focus.ERR_SCRATCH
+    assert nal(BOGUS, BOGUS, BOGUS, BOGUS, M, 28672, 8192, BOGUS, BOGUS, BOGUS, BOGUS, None) == focus.ERR_SCRATCH
+    # with the caller's col_sq the N column sums leave the scratch: one more width step fits
+    n_col = (limit - 256) // 8 // 256 // 8 * 8
+    assert n_col > n_max
+    assert nal(BOGUS, BOGUS, BOGUS, BOGUS, M, n_col + 8, 128, BOGUS, BOGUS, BOGUS, BOGUS, None) == focus.ERR_SCRATCH
     # fused backward from packed MXFP4 activations
     mxb = L.focus_recon_gemm_bwd_mxfp4
     def bwd_mx(q, M=8, N=8, K=64, scales=BOGUS, ws_bytes=1 << 30, w_dt=1):
