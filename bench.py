@@ -56,6 +56,9 @@ def parse():
     p.add_argument("--no-coeff", action="store_true", help="the baseline mode: no coefficients (c = 1)")
     p.add_argument("--e8m0", choices=("ceil", "floor"), default="ceil",
                    help="MXFP4 scale rounding: up (the paper's) or the OCP floor rule")
+    p.add_argument("--step-only", action="store_true",
+                   help="time the step only (no graph replay, cold-cache pass, other operands, chaining, optimizer, "
+                        "export or attainable rates): for profiling runs")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run an untimed 1 GiB device copy first (a known-size reference for HBM counters)")
     return p.parse_args()
@@ -240,16 +243,16 @@ def main():
                           2 * M * lin.N * lin.K)
 
     def cold_fakequant(mx_fwd, steps):
-        """The step again with the caches flushed before every fake-quant call: a fill kernel writes a
-        1 GiB buffer (4x the 256 MB Infinity Cache, far beyond the L2s) ahead of the call's start
-        event, so each call streams its tensors from HBM. Only the fake-quant spans are used."""
-        flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
-        count = [0]
+        """The step again with the caches flushed before every fake-quant call: a kernel reads a 1 GiB
+        buffer (4x the 256 MB Infinity Cache, far beyond the L2s) ahead of the call's start event, so
+        each call streams its tensors from HBM. The flush reads rather than writes: written lines would
+        be written back to HBM inside the timed call. Only the fake-quant spans are used."""
+        flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        sink = torch.empty((), dtype=torch.float32, device=dev)
 
         def before(name):
             if name.startswith("fakequant"):
-                count[0] += 1
-                flush.fill_(float(count[0]))
+                torch.sum(flush, dim=0, out=sink)
 
         for _ in range(steps):
             timer = Timer(torch, before)
@@ -314,6 +317,13 @@ def main():
     ms_per_step, kern = run(mx_fwd)
     per_step = sorted(run.per_step)
     block_loss = float(sum(L["loss"].item() for L in layers))
+    if args.step_only:
+        print(json.dumps({"metric": METRIC, "value": round(ms_per_step, 4), "unit": "ms per step", "n_gpus": 1,
+                          "steps": args.steps, "warmup": args.warmup, "step_only": True, "block_loss": block_loss,
+                          "config": {"workload": w.name, "tokens": M},
+                          "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]}
+                                      for k, v in kern.items()}}), flush=True)
+        return
     clocks = gpu_clocks()
     kern_cold = cold_fakequant(mx_fwd, 2)
     try:
@@ -447,11 +457,12 @@ def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, rnd, c_b, reps=5
             F.export_packed(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws, out=o, e8m0_rounding=rnd)
 
     def export_cold():
-        """Each layer's export with the caches flushed first (a 1 GiB fill kernel), summed over layers."""
-        flush = torch.empty(1 << 28, dtype=torch.float32, device=layers[0]["W"].device)
+        """Each layer's export with the caches flushed first (a kernel reading 1 GiB), summed over layers."""
+        flush = torch.ones(1 << 28, dtype=torch.float32, device=layers[0]["W"].device)
+        sink = torch.empty((), dtype=torch.float32, device=flush.device)
         spans = []
         for i, (L, o) in enumerate(zip(layers, outs)):
-            flush.fill_(float(i + 1))
+            torch.sum(flush, dim=0, out=sink)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
             F.export_packed(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws, out=o, e8m0_rounding=rnd)
@@ -679,7 +690,7 @@ PROFILED = {**GEMM_KERNELS, **FAKEQUANT_KERNELS}
 TRACE_CMD = ("rocprofv3 --kernel-trace --stats -d OUT/prof_trace -o run --output-format csv -- "
              "python3 -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration{wl}")
 PMC_CMD = ("rocprofv3 --pmc {c} -d OUT/prof_{d} -o run --output-format csv -- "
-           "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --copy-calibration{wl}")
+           "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --step-only --copy-calibration{wl}")
 
 
 # one counter pass (6 SQ and 1 GRBM counters, within what one rocprofv3 pass can collect on gfx950);
@@ -692,7 +703,7 @@ PMC_MFMA = ("MfmaUtil SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_INSTS_VALU_MFM
 PMC_STALL = ("SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_WAIT_INST_LDS SQ_ACTIVE_INST_LDS SQ_ACTIVE_INST_VMEM "
              "SQ_LDS_DATA_FIFO_FULL SQ_LDS_CMD_FIFO_FULL")
 STALL_CMD = ("rocprofv3 --pmc {c} -d OUT/prof_stall -o run --output-format csv -- "
-             "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline{wl}")
+             "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --step-only{wl}")
 
 
 def wl_arg(workload):

@@ -25,21 +25,208 @@ __device__ __forceinline__ float group_sum(float v, int lanes) {
     return v;
 }
 
-// Index of the scale byte of the block holding element e0 of a [rows_total][K] tensor: row-major
-// [rows][K/B] (e0 / B, rows being contiguous) or block-major [K/B][rows_total].
-template <int B>
-__device__ __forceinline__ int64_t scale_index(int64_t e0, uint32_t t, uint32_t cpr, int64_t row0,
-                                               int64_t rows_total, int block_major) {
-    if (!block_major) return e0 / B;
-    const uint32_t r = t / cpr, j = t - r * cpr;
-    return (int64_t)(j * 8 / B) * rows_total + row0 + r;
+// ------------------------------------------------------------------------------------------------
+// Tiles of the streaming fake-quant kernels. A workgroup covers 64 rows x 256 elements of a
+// [rows][K] tensor; thread t takes 8-element chunk (t % 32) of rows t/32, t/32 + 8, ..., t/32 + 56, so
+// each wave reads two 512-byte row pieces per load instruction and a block (32 or 16 elements) is 4
+// or 2 adjacent lanes. All 8 chunks of a thread are loaded before any is used. The tile's scale
+// bytes are staged in LDS and leave as 4-byte words: in the block-major layout [K/B][rows] a block's
+// 64 rows are one contiguous 64-byte run, in the row-major layout [rows][K/B] a row's 8 (16) blocks
+// are 2 (4) words.
+constexpr int kTileRows = 64;
+constexpr int kTileCols = 256;
+constexpr int kRowStep = 8;   // rows between a thread's chunks (256 threads / 32 chunks per row)
+constexpr int kChunks = 8;    // chunks per thread
+
+struct Tile {
+    int64_t row;       // row of the thread's first chunk (chunk i is row + 8 i)
+    int64_t col;       // first element of the thread's chunks
+    int64_t tile_row;  // first row of the tile
+    int64_t row_end;   // one past the last row of the launch
+    int64_t kb;        // first block of the tile
+    int nrows;         // valid rows of the tile
+    int nblk;          // valid blocks of the tile
+    bool col_ok;
+};
+
+// Workgroups are handed to the 8 XCDs in turn (workgroup b to XCD b % 8); tile numbers are assigned so
+// that each XCD takes one contiguous eighth of the tiles, so neighbouring column tiles, which share the
+// 128-byte lines of a row's learnable scales, meet in one L2.
+__device__ __forceinline__ uint32_t xcd_contiguous_tile() {
+    const uint32_t G = gridDim.x, per = G / 8, rem = G % 8;
+    const uint32_t x = blockIdx.x % 8, i = blockIdx.x / 8;
+    return x < rem ? x * (per + 1) + i : rem * (per + 1) + (x - rem) * per + i;
 }
 
+template <int B>
+__device__ __forceinline__ Tile tile_of(int64_t row0, int64_t rows, int64_t K, uint32_t ctiles) {
+    Tile t;
+    const uint32_t tile = xcd_contiguous_tile();
+    const uint32_t rt = tile / ctiles, ct = tile - rt * ctiles;
+    t.tile_row = row0 + (int64_t)rt * kTileRows;
+    t.row_end = row0 + rows;
+    t.row = t.tile_row + (threadIdx.x >> 5);
+    t.col = (int64_t)ct * kTileCols + (threadIdx.x & 31) * 8;
+    t.col_ok = t.col < K;
+    t.kb = (int64_t)ct * (kTileCols / B);
+    const int64_t nr = t.row_end - t.tile_row;
+    t.nrows = nr < kTileRows ? (int)nr : kTileRows;
+    const int64_t nb = (K - (int64_t)ct * kTileCols) / B;
+    t.nblk = nb < kTileCols / B ? (int)nb : kTileCols / B;
+    return t;
+}
+
+// Raw 16 bytes of chunk i (8 bf16 values), zero where the chunk lies outside the tensor.
+__device__ __forceinline__ uint4 load_chunk_bf16(const void *X, const Tile &t, int64_t K, int i) {
+    const int64_t r = t.row + (int64_t)i * kRowStep;
+    if (!t.col_ok || r >= t.row_end) return make_uint4(0u, 0u, 0u, 0u);
+    return *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(X) + r * K + t.col);
+}
+
+__device__ __forceinline__ void unpack_bf16(const uint4 p, float v[8]) {
+    const uint32_t w[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        v[2 * i] = __uint_as_float(w[i] << 16);
+        v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+}
+
+// Writes the staged scale bytes sb[j][r] (block kb + j, row tile_row + r) to a [rows_total][nb_total]
+// (row-major) or [nb_total][rows_total] (block-major) array; one item per thread, 4-byte words where
+// the four bytes are valid and the address is word aligned, single bytes otherwise.
+template <int NBLK>
+__device__ __forceinline__ void store_tile_scales(const uint8_t (&sb)[NBLK][kTileRows], const Tile &t,
+                                                  uint8_t *out, int64_t rows_total, int64_t nb_total,
+                                                  int block_major) {
+    const int item = threadIdx.x;
+    if (block_major) {
+        // item -> block j = item / 16, rows 4 q .. 4 q + 3 with q = item % 16
+        if (item >= NBLK * 16) return;
+        const int j = item >> 4, r = (item & 15) * 4;
+        if (j >= t.nblk || r >= t.nrows) return;
+        uint8_t *dst = out + (t.kb + j) * rows_total + t.tile_row + r;
+        if (r + 4 <= t.nrows && (reinterpret_cast<uintptr_t>(dst) & 3u) == 0) {
+            *reinterpret_cast<uint32_t *>(dst) = *reinterpret_cast<const uint32_t *>(&sb[j][r]);
+        } else {
+            for (int k = 0; k < 4 && r + k < t.nrows; k++) dst[k] = sb[j][r + k];
+        }
+    } else {
+        // item -> row r = item / (NBLK / 4), blocks 4 w .. 4 w + 3
+        constexpr int WPR = NBLK / 4;
+        if (item >= kTileRows * WPR) return;
+        const int r = item / WPR, j = (item % WPR) * 4;
+        if (r >= t.nrows || j >= t.nblk) return;
+        uint8_t *dst = out + (t.tile_row + r) * nb_total + t.kb + j;
+        if (j + 4 <= t.nblk && (reinterpret_cast<uintptr_t>(dst) & 3u) == 0) {
+            const uint32_t w = (uint32_t)sb[j][r] | ((uint32_t)sb[j + 1][r] << 8) | ((uint32_t)sb[j + 2][r] << 16) |
+                               ((uint32_t)sb[j + 3][r] << 24);
+            *reinterpret_cast<uint32_t *>(dst) = w;
+        } else {
+            for (int k = 0; k < 4 && j + k < t.nblk; k++) dst[k] = sb[j + k][r];
+        }
+    }
+}
+
+// Grid of a tiled launch: row tiles x column tiles.
+__host__ __device__ inline uint32_t col_tiles(int64_t K) { return (uint32_t)((K + kTileCols - 1) / kTileCols); }
+
 // ------------------------------------------------------------------------------------------------
-// K1 / K7: weight fake quantisation with learned scales (Eq. 4, 6-8) and export (Fig. 3(d)).
-template <int FMT, int IN, int OUT>
+// K1 / K7: weight fake quantisation with learned scales (Eq. 4, 6-8) and export (Fig. 3(d)), bf16
+// weights. Per sub-block one correctly rounded reciprocal of S_q; u = W / S_q by div_by_scale when the
+// whole wave's operands are in its range (always, for weights and scales of realistic size), by true
+// division otherwise. Either way u is fl32(W / S_q) wherever the E2M1 rounding depends on it.
+// (one coefficient per chunk fits 96 VGPRs: five waves per SIMD keep more loads in flight)
+template <int FMT, int OUT, int NCOEF>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NCOEF == 1 ? 5 : 4)))
+fq_weight_kernel(const void *__restrict__ W, int64_t row0, int64_t rows, int64_t K, uint32_t ctiles,
+                      const float *__restrict__ s_fp, const float *__restrict__ c, int sb_log2,
+                      const float *__restrict__ alpha_ptr, int e8m0_floor, void *__restrict__ w_hat,
+                      uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes, int64_t rows_total,
+                      int block_major, uint32_t *flag) {
+    constexpr int B = block_of(FMT);
+    constexpr int NBLK = kTileCols / B;
+    __shared__ uint8_t sbuf[NBLK][kTileRows];
+    const Tile t = tile_of<B>(row0, rows, K, ctiles);
+    // NCOEF coefficients per 8-element chunk: 1 for sub-blocks of 8 or more, 2 or 4 for 4 or 2
+    constexpr int EPC = 8 / NCOEF;  // elements per coefficient within a chunk
+    const float alpha = FMT == kFmtNV ? *alpha_ptr : 1.0f;
+    const int64_t nb = K / B, ns = K >> sb_log2;
+    bool bad = false;
+    uint4 raw[kChunks];
+#pragma unroll
+    for (int i = 0; i < kChunks; i++) raw[i] = load_chunk_bf16(W, t, K, i);
+    float sv[kChunks], cv[kChunks][NCOEF];
+#pragma unroll
+    for (int i = 0; i < kChunks; i++) {
+        const int64_t r = t.row + (int64_t)i * kRowStep;
+        const bool ok = t.col_ok && r < t.row_end;
+        sv[i] = ok ? s_fp[r * nb + t.col / B] : 0.0f;
+#pragma unroll
+        for (int k = 0; k < NCOEF; k++) cv[i][k] = (c && ok) ? c[r * ns + (t.col >> sb_log2) + k] : 1.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < kChunks; i++) {
+        const int64_t r = t.row + (int64_t)i * kRowStep;
+        const bool ok = t.col_ok && r < t.row_end;
+        uint32_t byte;
+        bool nan_seen = false;
+        const float sdq = weight_sdq(FMT, sv[i], alpha, e8m0_floor, byte, nan_seen);
+        float sq[NCOEF], y[NCOEF];
+        bool fast = bf16x8_over_2p80(raw[i]) == 0u;
+#pragma unroll
+        for (int k = 0; k < NCOEF; k++) {
+            nan_seen |= bad_coeff(cv[i][k]);
+            sq[k] = sdq * cv[i][k];
+            y[k] = 1.0f / sq[k];
+            fast = fast && scale_in_fast_range(sq[k]);
+        }
+        if (ok) bad |= nan_seen;
+        float v[8], u[8];
+        unpack_bf16(raw[i], v);
+        uint32_t packed;
+        if (__all(fast || !ok)) {
+            // every lane in range: the codes of u straight from the FP4 conversion (u is finite and
+            // carries the sign of w)
+#pragma unroll
+            for (int e = 0; e < 8; e++) u[e] = div_by_scale(v[e], sq[e / EPC], y[e / EPC]);
+            packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u[0], u[1], 1.0f, 0);
+            packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, u[2], u[3], 1.0f, 1);
+            packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, u[4], u[5], 1.0f, 2);
+            packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, u[6], u[7], 1.0f, 3);
+            // a zero-scale block never takes this path (its S_q is out of range)
+        } else {
+            packed = 0u;
+#pragma unroll
+            for (int e = 0; e < 8; e++) packed |= quantize_element(v[e], sq[e / EPC], sdq, true).code << (4 * e);
+        }
+        if (ok) {
+            const int64_t e0 = r * K + t.col;
+            if (w_hat) {
+                float out[8];
+                e2m1_value2<0>(packed, out[0], out[1]);
+                e2m1_value2<1>(packed, out[2], out[3]);
+                e2m1_value2<2>(packed, out[4], out[5]);
+                e2m1_value2<3>(packed, out[6], out[7]);
+#pragma unroll
+                for (int e = 0; e < 8; e++) out[e] *= sdq;
+                store8(w_hat, OUT, e0, out);
+            }
+            if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+            if (scale_bytes && (t.col % B) == 0) sbuf[(t.col % kTileCols) / B][(int)(r - t.tile_row)] = (uint8_t)byte;
+        }
+    }
+    if (scale_bytes) {
+        __syncthreads();
+        store_tile_scales<NBLK>(sbuf, t, scale_bytes, rows_total, nb, block_major);
+    }
+    if (bad) raise_domain_flag(flag);
+}
+
+// fp32 weights (the 256-wide fp32 layer): one chunk per thread, true division per element.
+template <int FMT, int OUT>
 __global__ void __launch_bounds__(256)
-fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
+fq_weight_f32_kernel(const void *__restrict__ W, uint32_t nchunks, int64_t row0, int64_t K,
                  const float *__restrict__ s_fp, const float *__restrict__ c, int sb_log2,
                  const float *__restrict__ alpha_ptr, int e8m0_floor, void *__restrict__ w_hat,
                  uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes, int64_t rows_total,
@@ -47,16 +234,13 @@ fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int
     constexpr int B = block_of(FMT);
     const float alpha = FMT == kFmtNV ? *alpha_ptr : 1.0f;
     const int sb = 1 << sb_log2;
-    const int64_t nb = K / B, ns = K >> sb_log2;
+    const int64_t nb = K / B;
     bool bad = false;
-    // rows are contiguous: chunk t starts at element e0 = row0 K + 8 t, its block's scale is
-    // s_fp[e0 / B] and its first sub-block coefficient c[e0 >> log2 sb]
-    (void)cpr, (void)nb, (void)ns;
-    const int64_t e_row0 = row0 * K;
+    const int64_t e_row0 = row0 * K;  // rows are contiguous: chunk t starts at element row0 K + 8 t
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
         const int64_t e0 = e_row0 + (int64_t)t * 8;
         float v[8];
-        load8(W, IN, e0, v);
+        load8(W, kF32, e0, v);
         uint32_t byte;
         const float sdq = weight_sdq(FMT, s_fp[e0 / B], alpha, e8m0_floor, byte, bad);
         float cv[4] = {1.0f, 1.0f, 1.0f, 1.0f};
@@ -79,8 +263,10 @@ fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int
         }
         if (w_hat) store8(w_hat, OUT, e0, out);
         if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
-        if (scale_bytes && (e0 % B) == 0)
-            scale_bytes[scale_index<B>(e0, t, cpr, row0, rows_total, block_major)] = (uint8_t)byte;
+        if (scale_bytes && (e0 % B) == 0) {
+            const int64_t row = e0 / K, blk = (e0 - row * K) / B;
+            scale_bytes[block_major ? blk * rows_total + row : row * nb + blk] = (uint8_t)byte;
+        }
     }
     if (bad) raise_domain_flag(flag);
 }
@@ -90,27 +276,79 @@ fq_weight_kernel(const void *__restrict__ W, uint32_t nchunks, uint32_t cpr, int
 // S = 2^e with e = E8M0_up(fl32(amax / 6)), or with e8m0_floor the OCP rule e = floor(log2 amax) - 2;
 // u = x / S is computed as x * 2^-e, which is the same correctly rounded value because 2^-e is exact
 // for every e in [-127, 127].
-template <int IN, int OUT>
+template <int OUT>
 __global__ void __launch_bounds__(256)
-fq_act_mx_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
+fq_act_mx_kernel(const void *__restrict__ X, int64_t row0, int64_t rows, int64_t K, uint32_t ctiles,
+                      void *__restrict__ x_hat, uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes,
+                      int64_t rows_total, int block_major, int e8m0_floor, uint32_t *flag) {
+    constexpr int NBLK = kTileCols / 32;
+    __shared__ uint8_t sbuf[NBLK][kTileRows];
+    const Tile t = tile_of<32>(row0, rows, K, ctiles);
+    bool bad = false;
+    uint4 raw[kChunks];
+#pragma unroll
+    for (int i = 0; i < kChunks; i++) raw[i] = load_chunk_bf16(X, t, K, i);
+#pragma unroll
+    for (int i = 0; i < kChunks; i++) {
+        const int64_t r = t.row + (int64_t)i * kRowStep;
+        const bool ok = t.col_ok && r < t.row_end;
+        float v[8];
+        unpack_bf16(raw[i], v);
+        float amax = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; e++) amax = fmaxf(amax, __builtin_fabsf(v[e]));
+        amax = group_max(amax, 4);
+        bool nan_seen = false;
+        const int e = e8m0_floor ? e8m0_floor_exp(amax, 2, nan_seen) : e8m0_ceil_exp(amax / 6.0f, nan_seen);
+        if (ok) bad |= nan_seen;
+        const float S = exp2i(e), inv = exp2i(-e);
+        // u = x 2^-e has the sign of x, so the hardware code's sign bit is the code's; element i
+        // lands in nibble i
+        uint32_t packed = e2m1_code2<0>(0u, v[0] * inv, v[1] * inv);
+        packed = e2m1_code2<1>(packed, v[2] * inv, v[3] * inv);
+        packed = e2m1_code2<2>(packed, v[4] * inv, v[5] * inv);
+        packed = e2m1_code2<3>(packed, v[6] * inv, v[7] * inv);
+        if (ok) {
+            const int64_t e0 = r * K + t.col;
+            if (x_hat) {
+                float out[8];
+                e2m1_value2<0>(packed, out[0], out[1]);
+                e2m1_value2<1>(packed, out[2], out[3]);
+                e2m1_value2<2>(packed, out[4], out[5]);
+                e2m1_value2<3>(packed, out[6], out[7]);
+#pragma unroll
+                for (int k = 0; k < 8; k++) out[k] *= S;
+                store8(x_hat, OUT, e0, out);
+            }
+            if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+            if (scale_bytes && (t.col % 32) == 0) sbuf[(t.col % kTileCols) / 32][(int)(r - t.tile_row)] = (uint8_t)(e + 127);
+        }
+    }
+    if (scale_bytes) {
+        __syncthreads();
+        store_tile_scales<NBLK>(sbuf, t, scale_bytes, rows_total, K / 32, block_major);
+    }
+    if (bad) raise_domain_flag(flag);
+}
+
+// fp32 activations: one chunk per thread (the same arithmetic).
+template <int OUT>
+__global__ void __launch_bounds__(256)
+fq_act_mx_f32_kernel(const void *__restrict__ X, uint32_t nchunks, int64_t row0, int64_t K,
                  void *__restrict__ x_hat, uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes,
                  int64_t rows_total, int block_major, int e8m0_floor, uint32_t *flag) {
-    // Rows are contiguous, so chunk t (8 elements) starts at element row0 K + 8 t. Launched with one
-    // chunk per thread (the loop is a guard).
     const int64_t e_row0 = row0 * K;
     bool bad = false;
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
         const int64_t e0 = e_row0 + (int64_t)t * 8;
         float v[8];
-        load8(X, IN, e0, v);
+        load8(X, kF32, e0, v);
         float amax = 0.0f;
 #pragma unroll
         for (int i = 0; i < 8; i++) amax = fmaxf(amax, __builtin_fabsf(v[i]));
         amax = group_max(amax, 4);
         const int e = e8m0_floor ? e8m0_floor_exp(amax, 2, bad) : e8m0_ceil_exp(amax / 6.0f, bad);
         const float S = exp2i(e), inv = exp2i(-e);
-        // u = x 2^-e has the sign of x, so the hardware code's sign bit is the code's; element i
-        // lands in nibble i
         uint32_t packed = e2m1_code2<0>(0u, v[0] * inv, v[1] * inv);
         packed = e2m1_code2<1>(packed, v[2] * inv, v[3] * inv);
         packed = e2m1_code2<2>(packed, v[4] * inv, v[5] * inv);
@@ -124,8 +362,10 @@ fq_act_mx_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
         for (int i = 0; i < 8; i++) out[i] *= S;
         if (x_hat) store8(x_hat, OUT, e0, out);
         if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
-        if (scale_bytes && (t & 3u) == 0)
-            scale_bytes[scale_index<32>(e0, t, cpr, row0, rows_total, block_major)] = (uint8_t)(e + 127);
+        if (scale_bytes && (t & 3u) == 0) {
+            const int64_t row = e0 / K, blk = (e0 - row * K) / 32;
+            scale_bytes[block_major ? blk * rows_total + row : row * (K / 32) + blk] = (uint8_t)(e + 127);
+        }
     }
     if (bad) raise_domain_flag(flag);
 }
@@ -182,12 +422,82 @@ tensor_alpha_kernel(const float *__restrict__ partial, int npart, float *__restr
 }
 
 // K2 (NVFP4) pass 2: block of 16 = 2 lanes; Delta = Q_E4M3(fl32(amax / fl32(alpha * 6))),
-// S = fl32(alpha * Delta), u = fl32(x / S) (a true division: S is not a power of two).
-template <int IN, int OUT>
+// S = fl32(alpha * Delta), u = fl32(x / S): S is not a power of two, so u comes from one correctly
+// rounded reciprocal per block and div_by_scale when the wave's operands are in its range, else from a
+// true division.
+template <int OUT>
 __global__ void __launch_bounds__(256)
-fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int64_t row0, int64_t K,
+fq_act_nv_kernel(const void *__restrict__ X, int64_t row0, int64_t rows, int64_t K, uint32_t ctiles,
                  const float *__restrict__ alpha_slot, void *__restrict__ x_hat, uint8_t *__restrict__ codes,
                  uint8_t *__restrict__ scale_bytes, int64_t rows_total, int block_major, uint32_t *flag) {
+    constexpr int NBLK = kTileCols / 16;
+    __shared__ uint8_t sbuf[NBLK][kTileRows];
+    const Tile t = tile_of<16>(row0, rows, K, ctiles);
+    const float alpha = *alpha_slot;
+    const float alpha6 = alpha * 6.0f;
+    bool bad = false;
+    uint4 raw[kChunks];
+#pragma unroll
+    for (int i = 0; i < kChunks; i++) raw[i] = load_chunk_bf16(X, t, K, i);
+#pragma unroll
+    for (int i = 0; i < kChunks; i++) {
+        const int64_t r = t.row + (int64_t)i * kRowStep;
+        const bool ok = t.col_ok && r < t.row_end;
+        float v[8];
+        unpack_bf16(raw[i], v);
+        float amax = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; e++) amax = fmaxf(amax, __builtin_fabsf(v[e]));
+        amax = group_max(amax, 2);
+        bool nan_seen = false;
+        const uint32_t byte = e4m3_code(amax / alpha6, nan_seen);
+        if (ok) bad |= nan_seen;
+        const float S = alpha * e4m3_value(byte);
+        const float y = 1.0f / S;
+        const bool fast = bf16x8_over_2p80(raw[i]) == 0u && scale_in_fast_range(S);
+        uint32_t packed;
+        if (__all(fast || !ok)) {
+            float u[8];
+#pragma unroll
+            for (int e = 0; e < 8; e++) u[e] = div_by_scale(v[e], S, y);
+            packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u[0], u[1], 1.0f, 0);
+            packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, u[2], u[3], 1.0f, 1);
+            packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, u[4], u[5], 1.0f, 2);
+            packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, u[6], u[7], 1.0f, 3);
+        } else {
+            packed = 0u;
+#pragma unroll
+            for (int e = 0; e < 8; e++) packed |= quantize_element(v[e], S, S, true).code << (4 * e);
+        }
+        if (ok) {
+            const int64_t e0 = r * K + t.col;
+            if (x_hat) {
+                float out[8];
+                e2m1_value2<0>(packed, out[0], out[1]);
+                e2m1_value2<1>(packed, out[2], out[3]);
+                e2m1_value2<2>(packed, out[4], out[5]);
+                e2m1_value2<3>(packed, out[6], out[7]);
+#pragma unroll
+                for (int e = 0; e < 8; e++) out[e] *= S;
+                store8(x_hat, OUT, e0, out);
+            }
+            if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+            if (scale_bytes && (t.col % 16) == 0) sbuf[(t.col % kTileCols) / 16][(int)(r - t.tile_row)] = (uint8_t)byte;
+        }
+    }
+    if (scale_bytes) {
+        __syncthreads();
+        store_tile_scales<NBLK>(sbuf, t, scale_bytes, rows_total, K / 16, block_major);
+    }
+    if (bad) raise_domain_flag(flag);
+}
+
+// fp32 activations: one chunk per thread, true division per element.
+template <int OUT>
+__global__ void __launch_bounds__(256)
+fq_act_nv_f32_kernel(const void *__restrict__ X, uint32_t nchunks, int64_t row0, int64_t K,
+                     const float *__restrict__ alpha_slot, void *__restrict__ x_hat, uint8_t *__restrict__ codes,
+                     uint8_t *__restrict__ scale_bytes, int64_t rows_total, int block_major, uint32_t *flag) {
     const float alpha = *alpha_slot;
     const float alpha6 = alpha * 6.0f;
     const int64_t e_row0 = row0 * K;  // rows are contiguous: chunk t starts at e_row0 + 8 t
@@ -195,7 +505,7 @@ fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
         const int64_t e0 = e_row0 + (int64_t)t * 8;
         float v[8];
-        load8(X, IN, e0, v);
+        load8(X, kF32, e0, v);
         float amax = 0.0f;
 #pragma unroll
         for (int i = 0; i < 8; i++) amax = fmaxf(amax, __builtin_fabsf(v[i]));
@@ -212,8 +522,10 @@ fq_act_nv_kernel(const void *__restrict__ X, uint32_t nchunks, uint32_t cpr, int
         }
         if (x_hat) store8(x_hat, OUT, e0, out);
         if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
-        if (scale_bytes && (t & 1u) == 0)
-            scale_bytes[scale_index<16>(e0, t, cpr, row0, rows_total, block_major)] = (uint8_t)byte;
+        if (scale_bytes && (t & 1u) == 0) {
+            const int64_t row = e0 / K, blk = (e0 - row * K) / 16;
+            scale_bytes[block_major ? blk * rows_total + row : row * (K / 16) + blk] = (uint8_t)byte;
+        }
     }
     if (bad) raise_domain_flag(flag);
 }
@@ -372,20 +684,41 @@ static int log2i(int v) {
     return l;
 }
 
+// Tiled launches: row ranges of whole 64-row tiles, each launch below 2^30 workgroups.
+template <typename F>
+static hipError_t for_tile_ranges(int64_t rows, int64_t K, F &&launch) {
+    const uint32_t ct = col_tiles(K);
+    const int64_t max_rows = std::max<int64_t>(1, (int64_t(1) << 30) / ct) * kTileRows;
+    for (int64_t r0 = 0; r0 < rows; r0 += max_rows) {
+        const int64_t nr = std::min(max_rows, rows - r0);
+        const uint32_t grid = (uint32_t)((nr + kTileRows - 1) / kTileRows) * ct;
+        launch(r0, nr, ct, grid);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64_t rows, int64_t K,
                             const float *s_fp, const float *c, int sb, const float *alpha, int e8m0_floor,
                             void *w_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, uint32_t *flag,
                             hipStream_t st) {
     const int sbl = log2i(sb);
+    if (in_dt == kBF16) {
+        return for_tile_ranges(rows, K, [&](int64_t r0, int64_t nr, uint32_t ct, uint32_t grid) {
+#define FQW(F, O, NC) fq_weight_kernel<F, O, NC><<<grid, 256, 0, st>>>(W, r0, nr, K, ct, s_fp, c, sbl, alpha, e8m0_floor, w_hat, codes, scale_bytes, rows, block_major, flag)
+#define FQW_NC(F, O) if (sb >= 8) FQW(F, O, 1); else if (sb == 4) FQW(F, O, 2); else FQW(F, O, 4)
+            if (fmt == kFmtMX) { if (out_dt == kBF16) FQW_NC(kFmtMX, kBF16); else FQW_NC(kFmtMX, kF32); }
+            else { if (out_dt == kBF16) FQW_NC(kFmtNV, kBF16); else FQW_NC(kFmtNV, kF32); }
+#undef FQW_NC
+#undef FQW
+        });
+    }
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-#define FQW(F, I, O) fq_weight_kernel<F, I, O><<<grid, 256, 0, st>>>(W, n, cpr, r0, K, s_fp, c, sbl, alpha, e8m0_floor, w_hat, codes, scale_bytes, rows, block_major, flag)
-        if (fmt == kFmtMX) {
-            if (in_dt == kBF16) { if (out_dt == kBF16) FQW(kFmtMX, kBF16, kBF16); else FQW(kFmtMX, kBF16, kF32); }
-            else { if (out_dt == kBF16) FQW(kFmtMX, kF32, kBF16); else FQW(kFmtMX, kF32, kF32); }
-        } else {
-            if (in_dt == kBF16) { if (out_dt == kBF16) FQW(kFmtNV, kBF16, kBF16); else FQW(kFmtNV, kBF16, kF32); }
-            else { if (out_dt == kBF16) FQW(kFmtNV, kF32, kBF16); else FQW(kFmtNV, kF32, kF32); }
-        }
+        (void)cpr;
+#define FQW(F, O) fq_weight_f32_kernel<F, O><<<grid, 256, 0, st>>>(W, n, r0, K, s_fp, c, sbl, alpha, e8m0_floor, w_hat, codes, scale_bytes, rows, block_major, flag)
+        if (fmt == kFmtMX) { if (out_dt == kBF16) FQW(kFmtMX, kBF16); else FQW(kFmtMX, kF32); }
+        else { if (out_dt == kBF16) FQW(kFmtNV, kBF16); else FQW(kFmtNV, kF32); }
 #undef FQW
     });
 }
@@ -404,20 +737,32 @@ hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t 
                          void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, int e8m0_floor,
                          float *alpha_out, float *partial, uint32_t *flag, hipStream_t st) {
     if (fmt == kFmtMX) {
+        if (in_dt == kBF16)
+            return for_tile_ranges(rows, K, [&](int64_t r0, int64_t nr, uint32_t ct, uint32_t grid) {
+#define FQA(O) fq_act_mx_kernel<O><<<grid, 256, 0, st>>>(X, r0, nr, K, ct, x_hat, codes, scale_bytes, rows, block_major, e8m0_floor, flag)
+                if (out_dt == kBF16) FQA(kBF16); else FQA(kF32);
+#undef FQA
+            });
         return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-#define FQA(I, O) fq_act_mx_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, x_hat, codes, scale_bytes, rows, block_major, e8m0_floor, flag)
-            if (in_dt == kBF16) { if (out_dt == kBF16) FQA(kBF16, kBF16); else FQA(kBF16, kF32); }
-            else { if (out_dt == kBF16) FQA(kF32, kBF16); else FQA(kF32, kF32); }
+            (void)cpr;
+#define FQA(O) fq_act_mx_f32_kernel<O><<<grid, 256, 0, st>>>(X, n, r0, K, x_hat, codes, scale_bytes, rows, block_major, e8m0_floor, flag)
+            if (out_dt == kBF16) FQA(kBF16); else FQA(kF32);
 #undef FQA
         });
     }
     hipError_t e = launch_tensor_alpha(in_dt, X, rows * K, partial, alpha_out, st);
     if (e != hipSuccess) return e;
     const float *slot = partial + kAbsmaxParts;
+    if (in_dt == kBF16)
+        return for_tile_ranges(rows, K, [&](int64_t r0, int64_t nr, uint32_t ct, uint32_t grid) {
+#define FQN(O) fq_act_nv_kernel<O><<<grid, 256, 0, st>>>(X, r0, nr, K, ct, slot, x_hat, codes, scale_bytes, rows, block_major, flag)
+            if (out_dt == kBF16) FQN(kBF16); else FQN(kF32);
+#undef FQN
+        });
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
-#define FQN(I, O) fq_act_nv_kernel<I, O><<<grid, 256, 0, st>>>(X, n, cpr, r0, K, slot, x_hat, codes, scale_bytes, rows, block_major, flag)
-        if (in_dt == kBF16) { if (out_dt == kBF16) FQN(kBF16, kBF16); else FQN(kBF16, kF32); }
-        else { if (out_dt == kBF16) FQN(kF32, kBF16); else FQN(kF32, kF32); }
+        (void)cpr;
+#define FQN(O) fq_act_nv_f32_kernel<O><<<grid, 256, 0, st>>>(X, n, r0, K, slot, x_hat, codes, scale_bytes, rows, block_major, flag)
+        if (out_dt == kBF16) FQN(kBF16); else FQN(kF32);
 #undef FQN
     });
 }

@@ -188,6 +188,34 @@ __device__ __forceinline__ Quantized quantize_element(float x, float sq, float s
     return r;
 }
 
+// ---- division by a quantisation scale without a per-element divide -----------------------------
+// u = fl32(a / b) from y = fl32(1 / b), one correctly rounded division per scale, by Markstein's
+// method (P. Markstein, IBM J. Res. Dev. 34(1), 1990): q0 = fl(a y), then twice q <- fl(q - r y) with
+// the residual r = q b - a formed exactly by an FMA. The first correction leaves a quotient within one
+// unit in the last place of a / b; from such a quotient and the correctly rounded reciprocal, the second
+// gives the correctly rounded quotient (Markstein's theorem). That needs every intermediate away from
+// overflow and underflow, which holds when 2^-40 <= b <= 2^40, |a| <= 2^80 and |a / b| >= 2^-4. Below
+// 2^-4 the result stays within a few units of the last place of a / b, far under the smallest E2M1
+// midpoint (0.25), with the sign of a; zeros keep their sign. Callers take this path only when every
+// lane's operands are in that range (scale_in_fast_range, and a finite bf16 weight of at most 2^80).
+__device__ __forceinline__ float div_by_scale(float a, float b, float y) {
+    const float q0 = a * y;
+    const float r0 = __builtin_fmaf(q0, b, -a);
+    const float q1 = __builtin_fmaf(-r0, y, q0);
+    const float r1 = __builtin_fmaf(q1, b, -a);
+    return __builtin_fmaf(-r1, y, q1);
+}
+
+__device__ __forceinline__ bool scale_in_fast_range(float b) { return b >= 0x1p-40f && b <= 0x1p40f; }
+
+// Nonzero when one of 8 bf16 values (four packed pairs) is not finite or exceeds 2^80 in magnitude
+// (bits 0x6780): adding 0x187F to a 15-bit magnitude sets its bit 15 exactly when the magnitude
+// exceeds 0x6780, and both halves of a word are tested at once (no carry crosses them).
+__device__ __forceinline__ uint32_t bf16x8_over_2p80(uint4 p) {
+    constexpr uint32_t M = 0x7FFF7FFFu, C = 0x187F187Fu;
+    return (((p.x & M) + C) | ((p.y & M) + C) | ((p.z & M) + C) | ((p.w & M) + C)) & 0x80008000u;
+}
+
 // Dequantisation scale of one weight block from its learnable copy (Eq. 4): MXFP4 2^E8M0(s), rounded
 // up (default) or down (e8m0_floor, the OCP rule), NVFP4 fl32(alpha * Q_E4M3(s)). Also returns the
 // exported scale byte.
