@@ -27,7 +27,9 @@
  *   - Sizes of 0 are valid no-ops. Each dimension must be below 2^31 and rows*K below 2^46.
  *   - Tensor pointers must be 16-byte aligned (they are read and written with vector accesses);
  *     a misaligned pointer is rejected with FOCUS_ERR_SHAPE.
- *   - Results are deterministic: no atomics; every reduction has a fixed order.
+ *   - Results are deterministic: every floating-point reduction has a fixed order and no kernel of
+ *     the scale-learning step uses atomics. The only atomics in the library are integer additions
+ *     to focus_kl_top's radix-select histogram in LDS, whose counts do not depend on their order.
  */
 #ifndef FOCUS_H
 #define FOCUS_H
@@ -146,7 +148,11 @@ focus_status focus_fakequant_bwd(const focus_qconfig *q, const float *G, int64_t
                                  const float *alpha, float *grad_s, float *grad_c,
                                  void *ws, size_t ws_bytes, focus_stream stream);
 
-/* Reconstruction GEMM forward with the MSE epilogue.
+/* Reconstruction GEMM forward with the MSE epilogue: the forward of one scale-learning step
+ * (Sec. 4.1: the fake-quantised layer is run on calibration tokens and compared with the
+ * full-precision model). The loss here is the per-layer mean squared error to the full-precision
+ * output Y_ref, a layer-local stand-in for the paper's end-to-end KL-Top objective (Sec. 4.1); dY is
+ * the gradient the backward consumes, and focus_kl_top provides the end-to-end one.
  *   X_hat [M][K], W_hat [N][K] in op_dtype (FOCUS_BF16: bf16 MFMA with fp32 accumulation;
  *   FOCUS_F32: fp32), Y_hat = X_hat W_hat^T.
  *   Y_ref == NULL: plain GEMM, Y_hat is written to dY [M][N] (op_dtype).
@@ -159,7 +165,7 @@ focus_status focus_recon_gemm_fwd(const void *X_hat, const void *W_hat, int op_d
                                   void *ws, size_t ws_bytes, focus_stream stream);
 
 /* Reconstruction GEMM forward from packed MXFP4 operands, with the same epilogue and outputs as
- * focus_recon_gemm_fwd (Y_ref and dY bf16). Under MXFP4, X_hat and W_hat are exactly FP4 codes
+ * focus_recon_gemm_fwd (Y_ref and dY bf16; the same per-layer MSE stand-in for Sec. 4.1's KL-Top). Under MXFP4, X_hat and W_hat are exactly FP4 codes
  * times E8M0 block scales along K (Sec. 3.1, Eq. 1 and 3), so Y_hat = X_hat W_hat^T is computed from
  * that representation with the block-scaled FP4 MFMA: every product is exact and the sums are
  * accumulated in fp32, i.e. the same result as the bf16 path up to the accumulation order.
@@ -189,7 +195,10 @@ focus_status focus_recon_gemm_fwd_mxfp4_noalloc(const uint8_t *X_codes, const ui
                                                 int64_t K, const void *Y_ref, void *dY, double *loss_out,
                                                 double *col_sq_opt, focus_stream stream);
 
-/* Reconstruction GEMM backward with the fused straight-through epilogue.
+/* Reconstruction GEMM backward with the fused straight-through epilogue: the gradient of the loss
+ * with respect to the block scales and the coefficients, through the straight-through estimator on
+ * every non-differentiable operation (Sec. 3.2) applied to W_hat = Q_E2M1(W / (S_dq c)) S_dq
+ * (Eq. 6-7, and Eq. 8 per sub-block).
  *   G = dY^T X_hat ([N][K], the reduction runs over the M tokens, fp32 accumulation) is formed
  *   tile by tile and reduced at once into grad_s [N][K/B] and grad_c [N][K/sub_block] exactly as
  *   in focus_fakequant_bwd, from W [N][K] (w_dtype), s_fp, c (NULL = ones) and alpha (NVFP4).
@@ -202,8 +211,9 @@ focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const 
                                   const float *alpha, float *grad_s, float *grad_c, float *G_out_opt,
                                   void *ws, size_t ws_bytes, focus_stream stream);
 
-/* Reconstruction GEMM backward with the fused straight-through epilogue, X_hat given as packed
- * MXFP4 (MXFP4 only: FOCUS_ERR_CONFIG for NVFP4). Under MXFP4, X_hat is exactly an E2M1 code times
+/* Reconstruction GEMM backward with the fused straight-through epilogue (Sec. 3.2 STE through
+ * Eq. 6-8, as focus_recon_gemm_bwd), X_hat given as packed MXFP4 (MXFP4 only: FOCUS_ERR_CONFIG for
+ * NVFP4). Under MXFP4, X_hat is exactly an E2M1 code times
  * its block's E8M0 power of two (Sec. 3.1, Eq. 1 and 3); the library rebuilds the bf16 operand from
  * that representation without loss, so grad_s and grad_c are those of focus_recon_gemm_bwd on the
  * bf16 X_hat up to the fp32 accumulation order.
