@@ -666,53 +666,18 @@ __device__ __forceinline__ void ste_epilogue(const f32x16_t (&acc)[4][4], int64_
             });
             float tc[4][2];  // per group of 8 k: this lane's sums of G m w over elements 0-1 / 2-3
             float ts[4];     // per group of 8 k: this lane's sum of G (q - m u)
-            // S_q of elements 0-1 / 2-3 of each group and its correctly rounded reciprocal; the quotient
-            // u = w / S_q by div_by_scale when every lane's operands are in its range (a ragged tile's
-            // zero scales are not), by true division otherwise: the same u, q and m either way
-            float sq[4][2], y[4][2];
-            bool fast = true;
             static_for<4>([&](auto g) {
                 const float sd = sdq[(8 * g) / B];
                 const float cv0 = cv[i][g][0], cv1 = cv[i][g][1];
                 bad = bad || (n_ok && kb + 8 * g < K32 && has_c && (bad_coeff(cv0) || bad_coeff(cv1)));
-                sq[g][0] = sd * cv0;
-                sq[g][1] = sd * cv1;
-                y[g][0] = 1.0f / sq[g][0];
-                y[g][1] = sb_log2 == 1 ? 1.0f / sq[g][1] : y[g][0];
-                fast = fast && scale_in_fast_range(sq[g][0]) && scale_in_fast_range(sq[g][1]);
-                static_for<4>([&](auto e) { fast = fast && __builtin_fabsf(wv[i][g][e]) <= 0x1p80f; });
+                tc[g][0] = tc[g][1] = ts[g] = 0.0f;
+                static_for<4>([&](auto e) {
+                    float a1, a2;
+                    ste_terms(acc[i][j][(int)(4 * g + e)], wv[i][g][e], sd, e < 2 ? cv0 : cv1, ste_clip != 0, a1, a2);
+                    tc[g][e >> 1] += a1;
+                    ts[g] += a2;
+                });
             });
-            if (__all(fast)) {
-                static_for<4>([&](auto g) {
-                    float u[4], q[4];
-                    static_for<4>([&](auto e) { u[e] = div_by_scale(wv[i][g][e], sq[g][e >> 1], y[g][e >> 1]); });
-                    // u is finite with the sign of w: the FP4 conversion gives the signed code, the
-                    // decode its grid value q
-                    uint32_t codes = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u[0], u[1], 1.0f, 0);
-                    codes = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(codes, u[2], u[3], 1.0f, 1);
-                    e2m1_value2<0>(codes, q[0], q[1]);
-                    e2m1_value2<1>(codes, q[2], q[3]);
-                    tc[g][0] = tc[g][1] = ts[g] = 0.0f;
-                    static_for<4>([&](auto e) {
-                        const float G = acc[i][j][(int)(4 * g + e)];
-                        const bool m = ste_clip == 0 || __builtin_fabsf(u[e]) <= 6.0f;
-                        tc[g][e >> 1] += m ? G * wv[i][g][e] : 0.0f;
-                        ts[g] += G * (q[e] - (m ? u[e] : 0.0f));
-                    });
-                });
-            } else {
-                static_for<4>([&](auto g) {
-                    const float sd = sdq[(8 * g) / B];
-                    tc[g][0] = tc[g][1] = ts[g] = 0.0f;
-                    static_for<4>([&](auto e) {
-                        float a1, a2;
-                        ste_terms(acc[i][j][(int)(4 * g + e)], wv[i][g][e], sd, e < 2 ? cv[i][g][0] : cv[i][g][1],
-                                  ste_clip != 0, a1, a2);
-                        tc[g][e >> 1] += a1;
-                        ts[g] += a2;
-                    });
-                });
-            }
             // ---- sub-block sums of G m w (scaled by -1/c^2 after the split reduction) ----
             if (sb <= 4) {
                 // a sub-block lies inside one lane's 4 consecutive k
