@@ -318,6 +318,12 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     lds_char *const lsm = (lds_char *)smem;
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
     const int64_t pitch = MX ? K / 2 : K * 2;  // bytes of an operand row
+    // MX scale loads: lane L brings rows 128 (L / 32) + 32 (L % 4) + 4 ((L / 4) % 8) .. + 3 of its wave's
+    // block (a permutation of the 64 four-row words), see load_scales; sc_sel picks byte lr % 4 of a
+    // word of the first block into byte 0 and of the second block into byte 2 (0x0c: a zero byte)
+    const uint32_t sc_row = ((uint32_t)lane >> 5) * 128u + ((uint32_t)lane & 3u) * 32u + (((uint32_t)lane >> 2) & 7u) * 4u;
+    const uint32_t sc_b = (uint32_t)lr & 3u;
+    const uint32_t sc_sel = sc_b | 0x0C00u | ((4u + sc_b) << 16) | 0x0C000000u;
     FwdDma dma;  // X and W rows have the same length, so one set of offsets serves both
     dma.init(pitch, wave_u, lane);
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(static_cast<const char *>(X) + m0 * pitch, (M - m0) * pitch);
@@ -353,7 +359,7 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
         else if (i < 8) dma.issue_one(rb, base, bad, st + kFwdOpBytes, wave_u, i - 4);
         else {
             const uint32_t blk = (uint32_t)j * 4u + wave_u;
-            const uint32_t so = blk * (uint32_t)(i == 8 ? M : N) + (uint32_t)(i == 8 ? m0 : n0) + 4u * lane;
+            const uint32_t so = blk * (uint32_t)(i == 8 ? M : N) + (uint32_t)(i == 8 ? m0 : n0) + sc_row;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(i == 8 ? rxs : rws, st + kFwdStageBytes + (i - 8) * 1024 + wave_u * 256, 4,
                                                      (int)so, 0, 0, 0);
         }
@@ -382,15 +388,22 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
         }
     };
     // MX mode: this lane's scales (rows of its X / W fragments) of a stage, byte 0 / 2 holding the
-    // scale of the first / second 64 k it covers (lane half lh takes the odd 32-k block of each 64)
+    // scale of the first / second 64 k it covers (lane half lh takes the odd 32-k block of each 64).
+    // A fragment row is 32 h + 32 i + lr (h the wave's half of the tile, i = 0..3), and the scale
+    // loads place the 4-byte words (4 consecutive rows of a block) so that the words of rows
+    // 128 h + 32 i + 4 a .. + 3, i = 0..3, are adjacent: 16 bytes at (8 h + a) 16. A lane reads
+    // those 16 bytes of its two blocks and picks byte lr % 4 of each word.
     auto load_scales = [&](const char *st, uint32_t (&sa)[4], uint32_t (&sb)[4]) {
-        const uint8_t *sx = reinterpret_cast<const uint8_t *>(st + kFwdStageBytes) + lh * 256;
-        const uint8_t *sw = sx + 1024;
+        typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
+        const char *sx = st + kFwdStageBytes + lh * 256;
+        const char *sw = sx + 1024;
+        const uint32_t qa = (uint32_t)(wm * 8 + (lr >> 2)) * 16u, qb = (uint32_t)(wn * 8 + (lr >> 2)) * 16u;
+        const u32x4v xa = *reinterpret_cast<const u32x4v *>(sx + qa), xc = *reinterpret_cast<const u32x4v *>(sx + 512 + qa);
+        const u32x4v wa = *reinterpret_cast<const u32x4v *>(sw + qb), wc = *reinterpret_cast<const u32x4v *>(sw + 512 + qb);
 #pragma unroll
         for (int i = 0; i < 4; i++) {
-            const int ra_ = wm * 128 + i * 32 + lr, rb_ = wn * 128 + i * 32 + lr;
-            sa[i] = (uint32_t)sx[ra_] | ((uint32_t)sx[512 + ra_] << 16);
-            sb[i] = (uint32_t)sw[rb_] | ((uint32_t)sw[512 + rb_] << 16);
+            sa[i] = __builtin_amdgcn_perm(xc[i], xa[i], sc_sel);
+            sb[i] = __builtin_amdgcn_perm(wc[i], wa[i], sc_sel);
         }
     };
     auto mfma = [&](auto i, auto j, const Frags &fr, const uint32_t (&sa)[4], const uint32_t (&sb)[4], auto half) {
