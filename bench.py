@@ -54,6 +54,8 @@ def parse():
                         "workload's format and shapes allow it, else bf16")
     p.add_argument("--sub-block", type=int, default=0, help="elements per coefficient c (0 = the workload's)")
     p.add_argument("--no-coeff", action="store_true", help="the baseline mode: no coefficients (c = 1)")
+    p.add_argument("--weights-per-layer", action="store_true",
+                   help="fake-quantise each linear's weights with its own call instead of one grouped call")
     p.add_argument("--e8m0", choices=("ceil", "floor"), default="ceil",
                    help="MXFP4 scale rounding: up (the paper's) or the OCP floor rule")
     p.add_argument("--step-only", action="store_true",
@@ -194,6 +196,23 @@ def main():
     ws_bwd = F.workspace(max(F.workspace_size(F.CALL_RECON_GEMM_BWD, q, M, l.N, l.K) for l in w.linears))
     torch.cuda.synchronize()
 
+    n_weights = sum(l.N * l.K for l in w.linears)
+    # the weight pass: every linear's fake quantisation in one grouped call (one launch), or with
+    # --weights-per-layer one call per linear
+    group_mx = [dict(W=L["W"], s_fp=L["s"], c=L["cf"], alpha=L["a"], codes=L.get("Wc"), scale_bytes=L.get("Ws"))
+                for L in layers]
+    group_bf = [dict(W=L["W"], s_fp=L["s"], c=L["cf"], alpha=L["a"], W_hat=L["W_hat"]) for L in layers]
+
+    def weight_pass(timer, mx_fwd):
+        if mx_fwd:
+            # the forward's weight operand is the deployable export: codes + E8M0 bytes, no bf16 W_hat
+            timer.run("fakequant_weight", lambda: F.fakequant_weights(group_mx, fmt, sb, ws=ws_fq,
+                                                                      scale_layout=F.SCALES_BLOCK_MAJOR,
+                                                                      e8m0_rounding=rnd), n_weights)
+        else:
+            timer.run("fakequant_weight", lambda: F.fakequant_weights(group_bf, fmt, sb, ws=ws_fq, e8m0_rounding=rnd),
+                      n_weights)
+
     def step(timer, mx_fwd):
         for src, x in acts.items():
             rows, K = x.shape
@@ -207,26 +226,29 @@ def main():
             else:
                 timer.run("fakequant_act", lambda: F.fakequant_fwd(x, fmt, sb, ws=ws_fq, out=x_hat[src], e8m0_rounding=rnd),
                           rows * K)
+        if not args.weights_per_layer:
+            weight_pass(timer, mx_fwd)
         for L in layers:
             lin = L["lin"]
             xh = x_hat[lin.source]
             dY = dY_buf[:M * lin.N].view(M, lin.N)
-            if mx_fwd:
-                # the forward's weight operand is the deployable export: codes + E8M0 bytes, no bf16 W_hat
+            if mx_fwd and args.weights_per_layer:
                 timer.run("fakequant_weight",
                           lambda: F.export_packed(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws_fq,
                                                   out=(L["Wc"], L["Ws"]), scale_layout=F.SCALES_BLOCK_MAJOR,
                                                   e8m0_rounding=rnd),
                           lin.N * lin.K)
+            elif args.weights_per_layer:
+                timer.run("fakequant_weight",
+                          lambda: F.fakequant_fwd(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws_fq, out=L["W_hat"],
+                                                  e8m0_rounding=rnd),
+                          lin.N * lin.K)
+            if mx_fwd:
                 timer.run("recon_gemm_fwd",
                           lambda: F.recon_gemm_fwd_mxfp4(x_codes[lin.source], x_scales[lin.source], L["Wc"], L["Ws"],
                                                          L["Y"], ws=ws_fwd, out=dY, loss=L["loss"]),
                           2 * M * lin.N * lin.K)
             else:
-                timer.run("fakequant_weight",
-                          lambda: F.fakequant_fwd(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws_fq, out=L["W_hat"],
-                                                  e8m0_rounding=rnd),
-                          lin.N * lin.K)
                 timer.run("recon_gemm_fwd",
                           lambda: F.recon_gemm_fwd(xh, L["W_hat"], L["Y"], ws=ws_fwd, out=dY, loss=L["loss"]),
                           2 * M * lin.N * lin.K)
@@ -452,28 +474,33 @@ def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, rnd, c_b, reps=5
             F.adamw_step(L["s"], L["gs"], ms, vs, t, lr_s, log2_domain=True, ws=ws)
             F.adamw_step(L["c"], L["gc"], mc, vc, t, lr_c, log2_domain=True, ws=ws)
 
+    group = [dict(W=L["W"], s_fp=L["s"], c=L["cf"], alpha=L["a"], codes=o[0], scale_bytes=o[1])
+             for L, o in zip(layers, outs)]
+
     def export_all():
+        # one grouped call: every linear's export in one launch
+        F.fakequant_weights(group, fmt, sb, ws=ws, e8m0_rounding=rnd)
+
+    def export_per_layer():
         for L, o in zip(layers, outs):
             F.export_packed(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws, out=o, e8m0_rounding=rnd)
 
     def export_cold():
-        """Each layer's export with the caches flushed first (a kernel reading 1 GiB), summed over layers."""
+        """The grouped export with the caches flushed first (a kernel reading 1 GiB)."""
         flush = torch.ones(1 << 28, dtype=torch.float32, device=layers[0]["W"].device)
         sink = torch.empty((), dtype=torch.float32, device=flush.device)
-        spans = []
-        for i, (L, o) in enumerate(zip(layers, outs)):
-            torch.sum(flush, dim=0, out=sink)
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            F.export_packed(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws, out=o, e8m0_rounding=rnd)
-            b.record()
-            spans.append((a, b))
+        torch.sum(flush, dim=0, out=sink)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        export_all()
+        b.record()
         torch.cuda.synchronize()
         del flush
-        return sum(a.elapsed_time(b) for a, b in spans)
+        return a.elapsed_time(b)
 
     res = {}
-    for name, fn in (("adamw", lambda t: adam_all(t)), ("export", lambda t: export_all())):
+    for name, fn in (("adamw", lambda t: adam_all(t)), ("export", lambda t: export_all()),
+                     ("export_per_layer", lambda t: export_per_layer())):
         fn(1)
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
@@ -496,7 +523,8 @@ def optimizer_and_export(torch, F, layers, fmt, sb, B, esz, ws, rnd, c_b, reps=5
     return {"adamw": {"ms_per_block": round(res["adamw"], 4), "params": n_params, "launches": 2 * len(layers),
                       "GBps": round(adam_bytes / (res["adamw"] * 1e-3) / 1e9, 1),
                       "frac_hbm": round(adam_bytes / (res["adamw"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
-            "export": {"ms_per_block": round(res["export"], 4), "weights": n_w, "launches": len(layers),
+            "export": {"ms_per_block": round(res["export"], 4), "weights": n_w, "launches": 1,
+                       "per_layer_calls_ms_per_block": round(res["export_per_layer"], 4),
                        "bytes_per_weight": round(exp_bytes / n_w, 4), "scale_layout": "row-major",
                        "GBps": round(exp_bytes / (res["export"] * 1e-3) / 1e9, 1),
                        "frac_hbm": round(exp_bytes / (res["export"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
@@ -685,7 +713,8 @@ GEMM_KERNELS = {"bwd_mfma_mx_kernel": "void focus::bwd_mfma_mx_kernel<",
 FAKEQUANT_KERNELS = {"fq_act_mx_kernel": "void focus::fq_act_mx_kernel<",
                      "absmax_partial_kernel": "void focus::absmax_partial_kernel<",
                      "fq_act_nv_kernel": "void focus::fq_act_nv_kernel<",
-                     "fq_weight_kernel": "void focus::fq_weight_kernel<"}
+                     "fq_weight_kernel": "void focus::fq_weight_kernel<",
+                     "fq_weight_group_kernel": "void focus::fq_weight_group_kernel<"}
 PROFILED = {**GEMM_KERNELS, **FAKEQUANT_KERNELS}
 TRACE_CMD = ("rocprofv3 --kernel-trace --stats -d OUT/prof_trace -o run --output-format csv -- "
              "python3 -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration{wl}")
@@ -729,15 +758,27 @@ def algorithmic_bytes(kernel, M, N, K, sb, fmt=0):
             "fq_weight_kernel": wparams + (packed if fmt == 0 else 2 * N * K)}[kernel]
 
 
+def launch_algorithmic_bytes(kernel, w, shape):
+    """algorithmic_bytes of one launch as step_launches lists it; a grouped weight launch covers every
+    linear of the block (its shape entry lists them)."""
+    label, rows, K = shape
+    if kernel == "fq_weight_group_kernel":
+        return sum(algorithmic_bytes("fq_weight_kernel", w.M, n, k, w.sub_block, w.fmt) for n, k in rows)
+    return algorithmic_bytes(kernel, w.M, rows, K, w.sub_block, w.fmt)
+
+
 def step_launches(kernel, w):
     """How a kernel's launches in a `--steps 1 --warmup 0` run map to tensors: (launches before the
     step, [(label, rows, K)] of the step's launches in order). The step fake-quantises the four
-    block inputs, then each linear's weights; the NVFP4 weight initialisation runs one tensor-absmax
-    pass per linear before the step."""
+    block inputs, then the weights of all linears in one grouped launch (or, with --weights-per-layer,
+    each linear's weights); the NVFP4 weight initialisation runs one tensor-absmax pass per linear before
+    the step."""
     if kernel in GEMM_KERNELS:
         return 0, [(f"{l.N}x{l.K}", l.N, l.K) for l in w.linears]
-    if kernel == "fq_weight_kernel":
+    if kernel == "fq_weight_kernel":  # one call per linear (--weights-per-layer)
         return 0, [(f"{l.name} {l.N}x{l.K}", l.N, l.K) for l in w.linears]
+    if kernel == "fq_weight_group_kernel":  # the default step: all linears in one launch
+        return 0, [(f"all {len(w.linears)} linears", [(l.N, l.K) for l in w.linears], None)]
     acts = [(f"{src} {w.M}x{K}", w.M, K) for src, K in w.inputs.items()]
     return (len(w.linears) if kernel == "absmax_partial_kernel" else 0), acts
 
@@ -803,7 +844,7 @@ def summarize_counters(fetch_dir, write_dir, workload, out_dir=None):
             continue
         n = min(len(fetch[k]), len(write[k]))
         tot = [fetch[k][i] + write[k][i] for i in range(n)]
-        algs = [algorithmic_bytes(k, w.M, rows, K, w.sub_block, w.fmt) for _, rows, K in step_launches(k, w)[1][:n]]
+        algs = [launch_algorithmic_bytes(k, w, sh) for sh in step_launches(k, w)[1][:n]]
         data[k] = {"bytes_per_launch": sum(tot) / n, "algorithmic_bytes_per_launch": sum(algs) / n,
                    "source_hash": src, "launches": n}
         for i, (label, rows, K) in enumerate(step_launches(k, w)[1][:n]):

@@ -98,7 +98,8 @@ typedef enum {
     FOCUS_CALL_ADAMW = 6,
     FOCUS_CALL_RECON_GEMM_DX = 7,
     FOCUS_CALL_FAKEQUANT_ACT_BWD = 8,
-    FOCUS_CALL_KL_TOP = 9
+    FOCUS_CALL_KL_TOP = 9,
+    FOCUS_CALL_FAKEQUANT_WEIGHTS = 10
 } focus_call;
 
 /* Workspace bytes a call needs for the given sizes (M = tokens, N = rows / out features,
@@ -237,6 +238,37 @@ focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dt
                                  const float *s_fp, const float *c, const float *alpha,
                                  uint8_t *packed, uint8_t *scale_bytes,
                                  void *ws, size_t ws_bytes, focus_stream stream);
+
+/* One linear layer of focus_fakequant_weights: the tensors focus_fakequant_fwd takes in weight mode. */
+typedef struct {
+    const void *W;          /* [rows][K] frozen weights (the call's w_dtype) */
+    int64_t rows, K;
+    const float *s_fp;      /* [rows][K/B] learned scales */
+    const float *c;         /* [rows][K/sub_block] coefficients, or NULL (every c = 1) */
+    const float *alpha;     /* NVFP4: the frozen tensor scale (device fp32 [1]); not read for MXFP4 */
+    void *W_hat;            /* [rows][K] fake-quantised weights (what_dtype), or NULL */
+    uint8_t *codes;         /* [rows][K/2] packed codes, or NULL */
+    uint8_t *scale_bytes;   /* scale bytes in q->scale_layout, or NULL */
+} focus_weight_layer;
+
+#define FOCUS_MAX_WEIGHT_LAYERS 16
+
+/* Weight fake quantisation (Sec. 3.2 Eq. 4, Sec. 3.3 Eq. 6-7, Sec. 3.4 Eq. 8) of up to
+ * FOCUS_MAX_WEIGHT_LAYERS linear layers under one q, e.g. all the linears of the decoder block being
+ * calibrated. Each layer's W_hat, codes and scale bytes are bit for bit those that focus_fakequant_fwd
+ * in weight mode writes for it (with W_hat NULL: those of focus_export_packed, Fig. 3(d)); bf16
+ * weights go out in one launch for the whole group, so small layers cost no launch and tail latency
+ * of their own (fp32 weights: one launch per layer).
+ *   layers: HOST array of n_layers entries, read during the call (the tensors stay device memory
+ *     owned by the caller); every layer is checked as focus_fakequant_fwd checks a weight-mode call
+ *     (W_hat and codes both NULL is FOCUS_ERR_NULL), and one failed check launches nothing.
+ *   n_layers: 0 .. FOCUS_MAX_WEIGHT_LAYERS (0 is a no-op; more is FOCUS_ERR_SHAPE). Layers may
+ *     differ in rows and K; a layer with rows == 0 is skipped.
+ *   ws: focus_workspace_size(FOCUS_CALL_FAKEQUANT_WEIGHTS, q, 0, 0, 0) bytes (the domain flag, which a
+ *     NaN scale or a bad coefficient of any layer raises). */
+focus_status focus_fakequant_weights(const focus_qconfig *q, int w_dtype, int what_dtype,
+                                     const focus_weight_layer *layers, int n_layers,
+                                     void *ws, size_t ws_bytes, focus_stream stream);
 
 /* Input gradient of a linear layer for end-to-end chaining (Sec. 3.2: the whole quantised model is
  * trained end to end, so the gradient reaching a layer's output flows on to its input):

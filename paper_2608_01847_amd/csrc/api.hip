@@ -162,6 +162,7 @@ size_t focus_workspace_size(int call, const focus_qconfig *q, int64_t M, int64_t
             return kWsHeader + (kAbsmaxParts + 64) * sizeof(float);  // partial maxima + tensor scale slot
         case FOCUS_CALL_FAKEQUANT_BWD:
         case FOCUS_CALL_EXPORT_PACKED:
+        case FOCUS_CALL_FAKEQUANT_WEIGHTS:
             return kWsHeader;
         case FOCUS_CALL_RECON_GEMM_FWD:
             if (M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return 0;
@@ -333,6 +334,29 @@ focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dt
     if (N == 0 || K == 0) return FOCUS_OK;
     return hip_status(launch_fq_weight(q->format, w_dtype, w_dtype, W, N, K, s_fp, c, q->sub_block, alpha,
                                        floor_of(q), nullptr, packed, scale_bytes, q->scale_layout, flag_of(ws), (hipStream_t)stream));
+}
+
+focus_status focus_fakequant_weights(const focus_qconfig *q, int w_dtype, int what_dtype,
+                                     const focus_weight_layer *layers, int n_layers, void *ws, size_t ws_bytes,
+                                     focus_stream stream) {
+    FOCUS_TRY(check_q(q));
+    if (n_layers < 0 || n_layers > FOCUS_MAX_WEIGHT_LAYERS) return FOCUS_ERR_SHAPE;
+    if (n_layers > 0 && !layers) return FOCUS_ERR_NULL;
+    if (!dtype_ok(w_dtype) || !dtype_ok(what_dtype)) return FOCUS_ERR_DTYPE;
+    WeightLayer L[FOCUS_MAX_WEIGHT_LAYERS];
+    for (int i = 0; i < n_layers; i++) {
+        const focus_weight_layer &l = layers[i];
+        if (l.rows != 0 && (!l.W || !l.s_fp || (!l.W_hat && !l.codes))) return FOCUS_ERR_NULL;
+        if (l.rows != 0 && q->format == FOCUS_NVFP4 && !l.alpha) return FOCUS_ERR_NULL;
+        FOCUS_TRY(check_rows_k(l.rows, l.K, block_of(q->format)));
+        if (!all_aligned({l.W, l.W_hat, l.codes})) return FOCUS_ERR_SHAPE;
+        L[i] = WeightLayer{l.W, l.rows, l.K, l.s_fp, l.c, q->format == FOCUS_NVFP4 ? l.alpha : nullptr,
+                           l.W_hat, l.codes, l.scale_bytes};
+    }
+    FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_FAKEQUANT_WEIGHTS, q, 0, 0, 0)));
+    if (n_layers == 0) return FOCUS_OK;
+    return hip_status(launch_fq_weight_group(q->format, w_dtype, what_dtype, L, n_layers, q->sub_block, floor_of(q),
+                                             q->scale_layout, flag_of(ws), (hipStream_t)stream));
 }
 
 focus_status focus_recon_gemm_dx(const void *dY, const void *W_hat, int op_dtype, int64_t M, int64_t N, int64_t K,

@@ -59,9 +59,9 @@ __device__ __forceinline__ uint32_t xcd_contiguous_tile() {
 }
 
 template <int B>
-__device__ __forceinline__ Tile tile_of(int64_t row0, int64_t rows, int64_t K, uint32_t ctiles) {
+__device__ __forceinline__ Tile tile_of(int64_t row0, int64_t rows, int64_t K, uint32_t ctiles,
+                                        uint32_t tile = xcd_contiguous_tile()) {
     Tile t;
-    const uint32_t tile = xcd_contiguous_tile();
     const uint32_t rt = tile / ctiles, ct = tile - rt * ctiles;
     t.tile_row = row0 + (int64_t)rt * kTileRows;
     t.row_end = row0 + rows;
@@ -130,6 +130,25 @@ __device__ __forceinline__ void store_tile_scales(const uint8_t (&sb)[NBLK][kTil
 
 // Grid of a tiled launch: row tiles x column tiles.
 __host__ __device__ inline uint32_t col_tiles(int64_t K) { return (uint32_t)((K + kTileCols - 1) / kTileCols); }
+constexpr uint32_t kMaxTiledGrid = 1u << 23;
+
+// Arguments of the tiled weight kernels for one layer: rows [row0, row0 + nrows) of a [rows][K] tensor
+// (a launch may cover part of a tensor) with its scales, coefficients and outputs.
+struct WeightJob {
+    const void *W;
+    const float *s_fp, *c, *alpha;
+    void *w_hat;
+    uint8_t *codes, *scale_bytes;
+    int64_t row0, nrows, rows, K;
+    uint32_t ctiles;
+};
+// Several layers of one launch (passed by value in the kernel arguments), layer l's tiles numbered
+// from first[l].
+struct WeightGroup {
+    WeightJob job[kMaxWeightLayers];
+    uint32_t first[kMaxWeightLayers];
+    int n;
+};
 
 // ------------------------------------------------------------------------------------------------
 // K1 / K7: weight fake quantisation with learned scales (Eq. 4, 6-8) and export (Fig. 3(d)), bf16
@@ -138,19 +157,22 @@ __host__ __device__ inline uint32_t col_tiles(int64_t K) { return (uint32_t)((K 
 // division otherwise. Either way u is fl32(W / S_q) wherever the E2M1 rounding depends on it.
 // (one coefficient per chunk fits 96 VGPRs: five waves per SIMD keep more loads in flight)
 template <int FMT, int OUT, int NCOEF>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NCOEF == 1 ? 5 : 4)))
-fq_weight_kernel(const void *__restrict__ W, int64_t row0, int64_t rows, int64_t K, uint32_t ctiles,
-                      const float *__restrict__ s_fp, const float *__restrict__ c, int sb_log2,
-                      const float *__restrict__ alpha_ptr, int e8m0_floor, void *__restrict__ w_hat,
-                      uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes, int64_t rows_total,
-                      int block_major, uint32_t *flag) {
+__device__ __forceinline__ void fq_weight_tile(const WeightJob &j, uint32_t tile, int sb_log2, int e8m0_floor,
+                                               int block_major, uint32_t *flag) {
+    const void *__restrict__ W = j.W;
+    const float *__restrict__ s_fp = j.s_fp;
+    const float *__restrict__ c = j.c;
+    void *__restrict__ w_hat = j.w_hat;
+    uint8_t *__restrict__ codes = j.codes;
+    uint8_t *__restrict__ scale_bytes = j.scale_bytes;
+    const int64_t K = j.K, rows_total = j.rows;
     constexpr int B = block_of(FMT);
     constexpr int NBLK = kTileCols / B;
     __shared__ uint8_t sbuf[NBLK][kTileRows];
-    const Tile t = tile_of<B>(row0, rows, K, ctiles);
+    const Tile t = tile_of<B>(j.row0, j.nrows, K, j.ctiles, tile);
     // NCOEF coefficients per 8-element chunk: 1 for sub-blocks of 8 or more, 2 or 4 for 4 or 2
     constexpr int EPC = 8 / NCOEF;  // elements per coefficient within a chunk
-    const float alpha = FMT == kFmtNV ? *alpha_ptr : 1.0f;
+    const float alpha = FMT == kFmtNV ? *j.alpha : 1.0f;
     const int64_t nb = K / B, ns = K >> sb_log2;
     bool bad = false;
     uint4 raw[kChunks];
@@ -221,6 +243,24 @@ fq_weight_kernel(const void *__restrict__ W, int64_t row0, int64_t rows, int64_t
         store_tile_scales<NBLK>(sbuf, t, scale_bytes, rows_total, nb, block_major);
     }
     if (bad) raise_domain_flag(flag);
+}
+
+
+template <int FMT, int OUT, int NCOEF>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NCOEF == 1 ? 5 : 4)))
+fq_weight_kernel(WeightJob j, int sb_log2, int e8m0_floor, int block_major, uint32_t *flag) {
+    fq_weight_tile<FMT, OUT, NCOEF>(j, xcd_contiguous_tile(), sb_log2, e8m0_floor, block_major, flag);
+}
+
+// The same for several layers in one launch: their tiles are numbered one layer after the other
+// (layer l's from g.first[l]), so one grid covers them all.
+template <int FMT, int OUT, int NCOEF>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NCOEF == 1 ? 5 : 4)))
+fq_weight_group_kernel(WeightGroup g, int sb_log2, int e8m0_floor, int block_major, uint32_t *flag) {
+    const uint32_t tile = xcd_contiguous_tile();
+    int l = 0;
+    for (int i = 1; i < g.n; i++) l = tile >= g.first[i] ? i : l;
+    fq_weight_tile<FMT, OUT, NCOEF>(g.job[l], tile - g.first[l], sb_log2, e8m0_floor, block_major, flag);
 }
 
 // fp32 weights (the 256-wide fp32 layer): one chunk per thread, true division per element.
@@ -684,11 +724,12 @@ static int log2i(int v) {
     return l;
 }
 
-// Tiled launches: row ranges of whole 64-row tiles, each launch below 2^30 workgroups.
+// Tiled launches: row ranges of whole 64-row tiles, each launch at most kMaxTiledGrid workgroups (its
+// work-item count, 256 per workgroup, then stays below 2^32).
 template <typename F>
 static hipError_t for_tile_ranges(int64_t rows, int64_t K, F &&launch) {
     const uint32_t ct = col_tiles(K);
-    const int64_t max_rows = std::max<int64_t>(1, (int64_t(1) << 30) / ct) * kTileRows;
+    const int64_t max_rows = std::max<int64_t>(1, (int64_t)kMaxTiledGrid / ct) * kTileRows;
     for (int64_t r0 = 0; r0 < rows; r0 += max_rows) {
         const int64_t nr = std::min(max_rows, rows - r0);
         const uint32_t grid = (uint32_t)((nr + kTileRows - 1) / kTileRows) * ct;
@@ -706,7 +747,8 @@ hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64
     const int sbl = log2i(sb);
     if (in_dt == kBF16) {
         return for_tile_ranges(rows, K, [&](int64_t r0, int64_t nr, uint32_t ct, uint32_t grid) {
-#define FQW(F, O, NC) fq_weight_kernel<F, O, NC><<<grid, 256, 0, st>>>(W, r0, nr, K, ct, s_fp, c, sbl, alpha, e8m0_floor, w_hat, codes, scale_bytes, rows, block_major, flag)
+            const WeightJob j{W, s_fp, c, alpha, w_hat, codes, scale_bytes, r0, nr, rows, K, ct};
+#define FQW(F, O, NC) fq_weight_kernel<F, O, NC><<<grid, 256, 0, st>>>(j, sbl, e8m0_floor, block_major, flag)
 #define FQW_NC(F, O) if (sb >= 8) FQW(F, O, 1); else if (sb == 4) FQW(F, O, 2); else FQW(F, O, 4)
             if (fmt == kFmtMX) { if (out_dt == kBF16) FQW_NC(kFmtMX, kBF16); else FQW_NC(kFmtMX, kF32); }
             else { if (out_dt == kBF16) FQW_NC(kFmtNV, kBF16); else FQW_NC(kFmtNV, kF32); }
@@ -721,6 +763,45 @@ hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64
         else { if (out_dt == kBF16) FQW(kFmtNV, kBF16); else FQW(kFmtNV, kF32); }
 #undef FQW
     });
+}
+
+hipError_t launch_fq_weight_group(int fmt, int in_dt, int out_dt, const WeightLayer *L, int n, int sb,
+                                  int e8m0_floor, int block_major, uint32_t *flag, hipStream_t st) {
+    auto one_by_one = [&]() {
+        for (int i = 0; i < n; i++) {
+            if (L[i].rows == 0 || L[i].K == 0) continue;
+            const hipError_t e = launch_fq_weight(fmt, in_dt, out_dt, L[i].W, L[i].rows, L[i].K, L[i].s_fp, L[i].c, sb,
+                                                  L[i].alpha, e8m0_floor, L[i].w_hat, L[i].codes, L[i].scale_bytes,
+                                                  block_major, flag, st);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    };
+    if (in_dt != kBF16 || n > kMaxWeightLayers) return one_by_one();
+    WeightGroup g{};
+    int m = 0;
+    uint64_t total = 0;
+    for (int i = 0; i < n; i++) {
+        if (L[i].rows == 0 || L[i].K == 0) continue;
+        const uint32_t ct = col_tiles(L[i].K);
+        g.job[m] = WeightJob{L[i].W, L[i].s_fp, L[i].c, L[i].alpha, L[i].w_hat, L[i].codes, L[i].scale_bytes,
+                             0, L[i].rows, L[i].rows, L[i].K, ct};
+        g.first[m] = (uint32_t)std::min<uint64_t>(total, kMaxTiledGrid);
+        total += (uint64_t)((L[i].rows + kTileRows - 1) / kTileRows) * ct;
+        m++;
+    }
+    if (m == 0) return hipSuccess;
+    if (total > kMaxTiledGrid) return one_by_one();
+    g.n = m;
+    const uint32_t grid = (uint32_t)total;
+    const int sbl = log2i(sb);
+#define FQG(F, O, NC) fq_weight_group_kernel<F, O, NC><<<grid, 256, 0, st>>>(g, sbl, e8m0_floor, block_major, flag)
+#define FQG_NC(F, O) if (sb >= 8) FQG(F, O, 1); else if (sb == 4) FQG(F, O, 2); else FQG(F, O, 4)
+    if (fmt == kFmtMX) { if (out_dt == kBF16) FQG_NC(kFmtMX, kBF16); else FQG_NC(kFmtMX, kF32); }
+    else { if (out_dt == kBF16) FQG_NC(kFmtNV, kBF16); else FQG_NC(kFmtNV, kF32); }
+#undef FQG_NC
+#undef FQG
+    return hipGetLastError();
 }
 
 // NVFP4 tensor scale: kAbsmaxParts partial maxima, then alpha into partial[kAbsmaxParts]

@@ -17,20 +17,27 @@ MXFP4, NVFP4 = 0, 1
 F32, BF16 = 0, 1
 CALL_SCALES_INIT, CALL_FAKEQUANT_FWD, CALL_FAKEQUANT_BWD = 0, 1, 2
 CALL_RECON_GEMM_FWD, CALL_RECON_GEMM_BWD, CALL_EXPORT_PACKED, CALL_ADAMW = 3, 4, 5, 6
-CALL_RECON_GEMM_DX, CALL_FAKEQUANT_ACT_BWD, CALL_KL_TOP = 7, 8, 9
+CALL_RECON_GEMM_DX, CALL_FAKEQUANT_ACT_BWD, CALL_KL_TOP, CALL_FAKEQUANT_WEIGHTS = 7, 8, 9, 10
+MAX_WEIGHT_LAYERS = 16
 
 OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_CONFIG, ERR_WORKSPACE, ERR_DOMAIN, ERR_HIP, ERR_SCRATCH = range(9)
 
 EXPORTED = ("focus_workspace_size", "focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd",
             "focus_recon_gemm_fwd", "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_fwd_mxfp4_noalloc",
             "focus_recon_gemm_bwd",
-            "focus_recon_gemm_bwd_mxfp4", "focus_export_packed", "focus_recon_gemm_dx", "focus_fakequant_act_bwd",
-            "focus_kl_top", "focus_adamw_step", "focus_check_flags", "focus_status_string")
+            "focus_recon_gemm_bwd_mxfp4", "focus_export_packed", "focus_fakequant_weights", "focus_recon_gemm_dx",
+            "focus_fakequant_act_bwd", "focus_kl_top", "focus_adamw_step", "focus_check_flags", "focus_status_string")
 
 
 class QConfig(ctypes.Structure):
     _fields_ = [("format", ctypes.c_int32), ("sub_block", ctypes.c_int32),
                 ("ste_clip", ctypes.c_int32), ("scale_layout", ctypes.c_int32), ("e8m0_rounding", ctypes.c_int32)]
+
+
+class WeightLayer(ctypes.Structure):
+    _fields_ = [("W", ctypes.c_void_p), ("rows", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("s_fp", ctypes.c_void_p), ("c", ctypes.c_void_p), ("alpha", ctypes.c_void_p),
+                ("W_hat", ctypes.c_void_p), ("codes", ctypes.c_void_p), ("scale_bytes", ctypes.c_void_p)]
 
 
 class AdamWConfig(ctypes.Structure):
@@ -67,6 +74,7 @@ def lib() -> ctypes.CDLL:
         L.focus_recon_gemm_bwd.argtypes = [q, p, p, i32, i64, i64, i64, p, i32, p, p, p, p, p, p, p, sz, p]
         L.focus_recon_gemm_bwd_mxfp4.argtypes = [q, p, p, p, i64, i64, i64, p, i32, p, p, p, p, p, sz, p]
         L.focus_export_packed.argtypes = [q, p, i32, i64, i64, p, p, p, p, p, p, sz, p]
+        L.focus_fakequant_weights.argtypes = [q, i32, i32, ctypes.POINTER(WeightLayer), i32, p, sz, p]
         L.focus_recon_gemm_dx.argtypes = [p, p, i32, i64, i64, i64, p, p, sz, p]
         L.focus_fakequant_act_bwd.argtypes = [q, p, i32, i64, i64, p, i32, p, p, sz, p]
         L.focus_kl_top.argtypes = [p, p, i32, i64, i64, i32, p, p, p, sz, p]
@@ -77,7 +85,7 @@ def lib() -> ctypes.CDLL:
         for name in ("focus_scales_init", "focus_fakequant_fwd", "focus_fakequant_bwd", "focus_recon_gemm_fwd",
                      "focus_recon_gemm_fwd_mxfp4", "focus_recon_gemm_fwd_mxfp4_noalloc", "focus_recon_gemm_bwd",
                      "focus_recon_gemm_bwd_mxfp4",
-                     "focus_export_packed", "focus_adamw_step", "focus_check_flags", "focus_recon_gemm_dx", "focus_fakequant_act_bwd",
+                     "focus_export_packed", "focus_fakequant_weights", "focus_adamw_step", "focus_check_flags", "focus_recon_gemm_dx", "focus_fakequant_act_bwd",
                      "focus_kl_top"):
             getattr(L, name).restype = ctypes.c_int
         _LIB = L
@@ -315,6 +323,29 @@ def export_packed(W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha
                                      _ptr(packed), _ptr(sbytes), _ptr(ws), ws.numel(), _stream()),
            "focus_export_packed")
     return packed, sbytes
+
+
+def fakequant_weights(layers, fmt: int, sub_block: int, w_dtype=None, what_dtype=None, ws=None,
+                      scale_layout: int = SCALES_ROW_MAJOR, e8m0_rounding: int = 0) -> None:
+    """Weight fake quantisation of several layers in one call (focus_fakequant_weights). `layers` is a
+    sequence of dicts with keys W, s_fp and optionally c, alpha, W_hat, codes, scale_bytes (device
+    tensors; the outputs are written in place). w_dtype / what_dtype default to the first layer's W /
+    W_hat dtype."""
+    q = qconfig(fmt, sub_block, 1, scale_layout, e8m0_rounding)
+    arr = (WeightLayer * max(1, len(layers)))()
+    for i, l in enumerate(layers):
+        W = l["W"]
+        arr[i] = WeightLayer(_ptr(W), W.shape[0], W.shape[1], _ptr(l["s_fp"]), _ptr(l.get("c")), _ptr(l.get("alpha")),
+                             _ptr(l.get("W_hat")), _ptr(l.get("codes")), _ptr(l.get("scale_bytes")))
+    if w_dtype is None:
+        w_dtype = _dt(layers[0]["W"]) if layers else BF16
+    if what_dtype is None:
+        wh = next((l["W_hat"] for l in layers if l.get("W_hat") is not None), None)
+        what_dtype = _dt(wh) if wh is not None else w_dtype
+    device = layers[0]["W"].device if layers else "cuda"
+    ws = _ws(ws, CALL_FAKEQUANT_WEIGHTS, q, 0, 0, 0, device)
+    _check(lib().focus_fakequant_weights(ctypes.byref(q), w_dtype, what_dtype, arr, len(layers), _ptr(ws), ws.numel(),
+                                         _stream()), "focus_fakequant_weights")
 
 
 def recon_gemm_dx(dY: torch.Tensor, W_hat: torch.Tensor, ws=None, out=None) -> torch.Tensor:

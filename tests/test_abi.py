@@ -184,3 +184,44 @@ def test_argument_checks(L, cpu_only):
     assert adam(good, ws_bytes=8) == focus.ERR_WORKSPACE
     assert focus.workspace_size(focus.CALL_ADAMW, focus.qconfig(focus.MXFP4, 8)) == 256
     assert L.focus_check_flags(None, None) == focus.ERR_WORKSPACE
+
+
+def test_grouped_weight_argument_checks(L, cpu_only):
+    """focus_fakequant_weights checks the group size, then every layer as focus_fakequant_fwd checks a
+    weight-mode call, then the workspace; a bad layer anywhere in the table fails the whole call."""
+    mx, nv = focus.qconfig(focus.MXFP4, 8), focus.qconfig(focus.NVFP4, 8)
+    assert focus.workspace_size(focus.CALL_FAKEQUANT_WEIGHTS, mx) == 256
+
+    def table(n, over=None):
+        arr = (focus.WeightLayer * max(n, 1))()
+        for i in range(n):
+            arr[i] = focus.WeightLayer(BOGUS.value, 4, 64, BOGUS.value, None, None, None, BOGUS.value, BOGUS.value)
+        for (i, field), v in (over or {}).items():
+            setattr(arr[i], field, v)
+        return arr
+
+    def call(q, arr, n, w_dt=1, wh_dt=1, ws=BOGUS, ws_bytes=1 << 20):
+        return L.focus_fakequant_weights(ctypes.byref(q), w_dt, wh_dt, arr, n, ws, ws_bytes, None)
+
+    n = focus.MAX_WEIGHT_LAYERS
+    assert call(mx, table(n + 1), n + 1) == focus.ERR_SHAPE
+    assert call(mx, table(1), -1) == focus.ERR_SHAPE
+    assert L.focus_fakequant_weights(ctypes.byref(mx), 1, 1, None, 2, BOGUS, 1 << 20, None) == focus.ERR_NULL
+    assert call(focus.qconfig(2, 8), table(2), 2) == focus.ERR_CONFIG
+    assert call(mx, table(2), 2, w_dt=7) == focus.ERR_DTYPE
+    assert call(mx, table(2), 2, wh_dt=7) == focus.ERR_DTYPE
+    # a bad last layer fails the call
+    assert call(mx, table(n, {(n - 1, "K"): 48}), n) == focus.ERR_SHAPE
+    assert call(mx, table(n, {(n - 1, "rows"): 1 << 31}), n) == focus.ERR_SHAPE
+    assert call(mx, table(3, {(2, "W"): None}), 3) == focus.ERR_NULL
+    assert call(mx, table(3, {(1, "s_fp"): None}), 3) == focus.ERR_NULL
+    assert call(mx, table(3, {(1, "codes"): None}), 3) == focus.ERR_NULL   # W_hat and codes both NULL
+    assert call(mx, table(3, {(0, "W"): BOGUS.value + 8}), 3) == focus.ERR_SHAPE  # not 16-byte aligned
+    assert call(nv, table(3), 3) == focus.ERR_NULL                           # NVFP4 needs alpha
+    assert call(mx, table(3), 3, ws=None) == focus.ERR_WORKSPACE
+    assert call(mx, table(3), 3, ws_bytes=16) == focus.ERR_WORKSPACE
+    # no layers, or only empty layers (NULL pointers allowed): nothing is launched
+    assert call(mx, table(0), 0) == focus.OK
+    empty = table(2, {(0, "rows"): 0, (0, "W"): None, (0, "s_fp"): None, (0, "codes"): None,
+                        (1, "rows"): 0, (1, "W"): None})
+    assert call(mx, empty, 2) == focus.OK

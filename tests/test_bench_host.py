@@ -41,6 +41,12 @@ def test_step_launch_map():
     assert skip == 0 and [s[1:] for s in shapes] == [(w.M, K) for K in w.inputs.values()]
     skip, shapes = bench.step_launches("fq_weight_kernel", w)
     assert skip == 0 and [s[1:] for s in shapes] == [(l.N, l.K) for l in w.linears]
+    # the default step's grouped weight launch covers every linear: its bytes are their sum
+    skip, shapes = bench.step_launches("fq_weight_group_kernel", w)
+    assert skip == 0 and len(shapes) == 1 and shapes[0][1] == [(l.N, l.K) for l in w.linears]
+    per_layer = sum(bench.algorithmic_bytes("fq_weight_kernel", w.M, l.N, l.K, w.sub_block, w.fmt) for l in w.linears)
+    assert bench.launch_algorithmic_bytes("fq_weight_group_kernel", w, shapes[0]) == per_layer
+    assert "fq_weight_group_kernel" in bench.PROFILED
     # NVFP4: the weights' tensor-absmax passes (one per linear) run before the step
     skip, shapes = bench.step_launches("absmax_partial_kernel", synth.WORKLOADS["block2560_nvfp4"])
     assert skip == 7 and len(shapes) == 4

@@ -187,6 +187,20 @@ int main() {
     expect(focus_adamw_step(&bad, 1, 16, P, P, P, P, B, 256, nullptr), FOCUS_ERR_CONFIG, "adamw beta");
     expect(focus_adamw_step(&ok, 1, -1, P, P, P, P, B, 256, nullptr), FOCUS_ERR_SHAPE, "adamw n");
     expect(focus_check_flags(nullptr, nullptr), FOCUS_ERR_WORKSPACE, "flags");
+    // grouped weight fake quantisation: the host copies the layer table; every layer is checked
+    focus_weight_layer lay[FOCUS_MAX_WEIGHT_LAYERS + 1];
+    for (int i = 0; i <= FOCUS_MAX_WEIGHT_LAYERS; i++)
+        lay[i] = focus_weight_layer{B, 4, 64, P, nullptr, nullptr, nullptr, static_cast<uint8_t *>(B), static_cast<uint8_t *>(B)};
+    expect(focus_fakequant_weights(&mx, 1, 1, lay, FOCUS_MAX_WEIGHT_LAYERS + 1, B, 256, nullptr), FOCUS_ERR_SHAPE,
+           "group too many layers");
+    expect(focus_fakequant_weights(&mx, 1, 1, nullptr, 2, B, 256, nullptr), FOCUS_ERR_NULL, "group table");
+    lay[FOCUS_MAX_WEIGHT_LAYERS - 1].K = 48;
+    expect(focus_fakequant_weights(&mx, 1, 1, lay, FOCUS_MAX_WEIGHT_LAYERS, B, 256, nullptr), FOCUS_ERR_SHAPE,
+           "group last layer K");
+    lay[FOCUS_MAX_WEIGHT_LAYERS - 1].K = 64;
+    expect(focus_fakequant_weights(&nv, 1, 1, lay, 3, B, 256, nullptr), FOCUS_ERR_NULL, "group nv alpha");
+    expect(focus_fakequant_weights(&mx, 1, 1, lay, 3, B, 16, nullptr), FOCUS_ERR_WORKSPACE, "group ws");
+    expect(focus_fakequant_weights(&mx, 1, 1, lay, 0, B, 256, nullptr), FOCUS_OK, "group empty");
     std::printf("abi %s (%d failures)\n", fails ? "FAILED" : "ok", fails);
     return fails != 0;
 }
