@@ -180,13 +180,14 @@ def main():
         print("--fwd-operands mxfp4 needs an MXFP4 workload whose shapes the FP4 forward takes", file=sys.stderr)
         sys.exit(2)
     mx_primary = args.fwd_operands == "mxfp4" or (args.fwd_operands == "auto" and mx_possible)
-    if mx_possible:  # packed operands of an MXFP4 forward: codes [rows][K/2] and E8M0 bytes [rows][K/32]
-        # (scale bytes block-major, [K/32][rows], the layout the MXFP4 forward reads)
+    if mx_possible:  # packed operands of the MXFP4 GEMMs, in the layouts they read: activation codes
+        # [M][K/2], weight codes in K-slabs [K/128][N][64], E8M0 bytes block-major [K/32][rows]
+        slab = F.CODES_K_SLAB
         x_codes = {src: torch.empty(M, x.shape[1] // 2, dtype=torch.uint8, device=dev) for src, x in acts.items()}
         x_scales = {src: torch.empty(x.shape[1] // 32, M, dtype=torch.uint8, device=dev) for src, x in acts.items()}
         for L in layers:
             N_, K_ = L["W"].shape
-            L["Wc"] = torch.empty(N_, K_ // 2, dtype=torch.uint8, device=dev)
+            L["Wc"] = torch.empty(*F.codes_shape(N_, K_, slab), dtype=torch.uint8, device=dev)
             L["Ws"] = torch.empty(K_ // 32, N_, dtype=torch.uint8, device=dev)
     max_n = max(l.N for l in w.linears)
     dY_buf = torch.empty(M * max_n, dtype=acts[w.linears[0].source].dtype, device=dev)
@@ -208,7 +209,8 @@ def main():
             # the forward's weight operand is the deployable export: codes + E8M0 bytes, no bf16 W_hat
             timer.run("fakequant_weight", lambda: F.fakequant_weights(group_mx, fmt, sb, ws=ws_fq,
                                                                       scale_layout=F.SCALES_BLOCK_MAJOR,
-                                                                      e8m0_rounding=rnd), n_weights)
+                                                                      e8m0_rounding=rnd, code_layout=F.CODES_K_SLAB),
+                      n_weights)
         else:
             timer.run("fakequant_weight", lambda: F.fakequant_weights(group_bf, fmt, sb, ws=ws_fq, e8m0_rounding=rnd),
                       n_weights)
@@ -236,7 +238,7 @@ def main():
                 timer.run("fakequant_weight",
                           lambda: F.export_packed(L["W"], fmt, sb, L["s"], L["cf"], L["a"], ws=ws_fq,
                                                   out=(L["Wc"], L["Ws"]), scale_layout=F.SCALES_BLOCK_MAJOR,
-                                                  e8m0_rounding=rnd),
+                                                  e8m0_rounding=rnd, code_layout=F.CODES_K_SLAB),
                           lin.N * lin.K)
             elif args.weights_per_layer:
                 timer.run("fakequant_weight",

@@ -74,15 +74,25 @@ typedef enum { FOCUS_F32 = 0, FOCUS_BF16 = 1 } focus_dtype;
  *               activation blocks take e = floor(log2 amax) - 2 (2 = exponent of E2M1's largest
  *               value, elements above 6 S saturate) and focus_scales_init sets S_fp = fl32(amax / 4),
  *               whose floor exponent is that same OCP exponent. The straight-through derivative of
- *               Q_E8M0 is 1 in both modes. */
+ *               Q_E8M0 is 1 in both modes.
+ *   code_layout : layout of the packed codes that focus_fakequant_fwd, focus_export_packed and
+ *               focus_fakequant_weights write: FOCUS_CODES_ROW_MAJOR (0) [rows][K/2], the deployable
+ *               layout and that of the MXFP4 GEMMs' X operand; FOCUS_CODES_K_SLAB (1) [K/128][rows][64],
+ *               slab s holding every row's 64 bytes of k = 128 s .. 128 s + 127 (a GEMM step's tile of
+ *               the operand is then one contiguous run), the layout of focus_recon_gemm_fwd_mxfp4's W
+ *               operand; it needs K % 128 == 0 wherever codes are written. Byte order within a row's
+ *               64 bytes is the row-major one. Other calls ignore it.
+ * A zero-initialised trailing field keeps the defaults (row-major codes). */
 typedef enum { FOCUS_SCALES_ROW_MAJOR = 0, FOCUS_SCALES_BLOCK_MAJOR = 1 } focus_scale_layout;
 typedef enum { FOCUS_E8M0_CEIL = 0, FOCUS_E8M0_FLOOR = 1 } focus_e8m0_rounding;
+typedef enum { FOCUS_CODES_ROW_MAJOR = 0, FOCUS_CODES_K_SLAB = 1 } focus_code_layout;
 typedef struct {
     int32_t format;
     int32_t sub_block;
     int32_t ste_clip;
     int32_t scale_layout;
     int32_t e8m0_rounding;
+    int32_t code_layout;
 } focus_qconfig;
 
 typedef void *focus_stream; /* a hipStream_t */
@@ -126,8 +136,10 @@ focus_status focus_scales_init(const focus_qconfig *q, const void *W, int w_dtyp
  *   (Sec. 3.2 dynamic activation quantisation): MXFP4 S = 2^E8M0(fl32(amax/6)); NVFP4 alpha_x =
  *   fl32(max|X| / 2688) over the whole X (1 if X is all zero), S = fl32(alpha_x * Q_E4M3(fl32(amax /
  *   fl32(alpha_x * 6)))); alpha_x is written to *alpha_out_opt when it is non-NULL.
- * Optional outputs: codes_opt [rows][K/2] packed FP4 codes (code = sign<<3 | magnitude index, the
- *   even-k code in the low nibble); scale_bytes_opt [rows][K/B] (E8M0 byte e+127, or E4M3 byte).
+ * Optional outputs: codes_opt, packed FP4 codes (code = sign<<3 | magnitude index, the even-k code in
+ *   the low nibble) in q->code_layout ([rows][K/2] or K-slabs [K/128][rows][64]; the slabs need
+ *   K % 128 == 0, FOCUS_ERR_SHAPE otherwise); scale_bytes_opt in q->scale_layout (E8M0 byte e+127, or
+ *   E4M3 byte).
  *   X_hat may be NULL when codes_opt is not (the packed form alone, e.g. for the MXFP4 GEMMs);
  *   X_hat and codes_opt both NULL is FOCUS_ERR_NULL. With rows == 0 nothing is read or written and
  *   X, X_hat and codes_opt may be NULL.
@@ -170,8 +182,11 @@ focus_status focus_recon_gemm_fwd(const void *X_hat, const void *W_hat, int op_d
  * times E8M0 block scales along K (Sec. 3.1, Eq. 1 and 3), so Y_hat = X_hat W_hat^T is computed from
  * that representation with the block-scaled FP4 MFMA: every product is exact and the sums are
  * accumulated in fp32, i.e. the same result as the bf16 path up to the accumulation order.
- *   X_codes [M][K/2], W_codes [N][K/2]: two E2M1 codes per byte, even k in the low nibble (the
- *     codes_opt / packed layout of focus_fakequant_fwd and focus_export_packed), 16-byte aligned;
+ *   X_codes [M][K/2] (FOCUS_CODES_ROW_MAJOR) and W_codes in K-slabs [K/128][N][64]
+ *     (FOCUS_CODES_K_SLAB of focus_export_packed / focus_fakequant_weights / focus_fakequant_fwd):
+ *     two E2M1 codes per byte, even k in the low nibble, 16-byte aligned. The weights, exported once
+ *     per step, come in the layout that gives each GEMM step one contiguous run of W; the activation
+ *     codes stay row-major, the layout the backward reads fastest (token-major tiles);
  *   X_scales [K/32][M], W_scales [K/32][N]: E8M0 bytes (e + 127) in the block-major layout
  *     (FOCUS_SCALES_BLOCK_MAJOR of focus_fakequant_fwd / focus_export_packed), 4-byte aligned.
  *   Requires K % 128 == 0, M % 4 == 0 and N % 8 == 0 (FOCUS_ERR_SHAPE otherwise). The workspace is
@@ -220,8 +235,9 @@ focus_status focus_recon_gemm_bwd(const focus_qconfig *q, const void *dY, const 
  * bf16 X_hat up to the fp32 accumulation order.
  *   dY [M][N] bf16; X_codes [M][K/2] (two codes per byte, even k in the low nibble) and X_scales
  *   [K/32][M] (E8M0 bytes, block-major): the codes_opt / scale_bytes_opt outputs of
- *   focus_fakequant_fwd in activation mode with FOCUS_SCALES_BLOCK_MAJOR. W, s_fp, c, grad_s, grad_c
- *   as in focus_recon_gemm_bwd. Requires M % 4 == 0 and N % 8 == 0 (FOCUS_ERR_SHAPE otherwise); dY,
+ *   focus_fakequant_fwd in activation mode with FOCUS_CODES_ROW_MAJOR and FOCUS_SCALES_BLOCK_MAJOR. W,
+ *   s_fp, c, grad_s, grad_c as in focus_recon_gemm_bwd. Requires M % 4 == 0 and N % 8 == 0
+ *   (FOCUS_ERR_SHAPE otherwise); dY,
  *   X_codes and W 16-byte aligned, X_scales 4-byte aligned. The workspace is that of
  *   FOCUS_CALL_RECON_GEMM_BWD. A scale byte 255 (NaN, never written by the library) makes its
  *   block's values NaN. With M == 0 the gradients are zero and dY, X_codes, X_scales may be NULL. */
@@ -232,8 +248,9 @@ focus_status focus_recon_gemm_bwd_mxfp4(const focus_qconfig *q, const void *dY, 
                                         focus_stream stream);
 
 /* Export of the deployable tensor (Fig. 3(d): only FP4 codes and dequantisation scales are kept;
- * the coefficients and S_q are discarded): packed [N][K/2] codes as in focus_fakequant_fwd and
- * scale_bytes [N][K/B]. The NVFP4 tensor scale is the caller's frozen alpha. */
+ * the coefficients and S_q are discarded): packed codes and scale bytes as in focus_fakequant_fwd,
+ * in q->code_layout and q->scale_layout (the deployable defaults: [N][K/2] and [N][K/B]). The NVFP4
+ * tensor scale is the caller's frozen alpha. */
 focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dtype, int64_t N, int64_t K,
                                  const float *s_fp, const float *c, const float *alpha,
                                  uint8_t *packed, uint8_t *scale_bytes,
@@ -247,7 +264,7 @@ typedef struct {
     const float *c;         /* [rows][K/sub_block] coefficients, or NULL (every c = 1) */
     const float *alpha;     /* NVFP4: the frozen tensor scale (device fp32 [1]); not read for MXFP4 */
     void *W_hat;            /* [rows][K] fake-quantised weights (what_dtype), or NULL */
-    uint8_t *codes;         /* [rows][K/2] packed codes, or NULL */
+    uint8_t *codes;         /* packed codes in q->code_layout, or NULL */
     uint8_t *scale_bytes;   /* scale bytes in q->scale_layout, or NULL */
 } focus_weight_layer;
 

@@ -25,7 +25,15 @@ focus_status check_q(const focus_qconfig *q) {
     if (q->scale_layout != FOCUS_SCALES_ROW_MAJOR && q->scale_layout != FOCUS_SCALES_BLOCK_MAJOR) return FOCUS_ERR_CONFIG;
     if (q->e8m0_rounding != FOCUS_E8M0_CEIL && q->e8m0_rounding != FOCUS_E8M0_FLOOR) return FOCUS_ERR_CONFIG;
     if (q->e8m0_rounding == FOCUS_E8M0_FLOOR && q->format != FOCUS_MXFP4) return FOCUS_ERR_CONFIG;
+    if (q->code_layout != FOCUS_CODES_ROW_MAJOR && q->code_layout != FOCUS_CODES_K_SLAB) return FOCUS_ERR_CONFIG;
     return FOCUS_OK;
+}
+
+int slab_of(const focus_qconfig *q) { return q->code_layout == FOCUS_CODES_K_SLAB ? 1 : 0; }
+
+// codes in K-slabs of 128 elements need whole slabs
+focus_status check_code_layout(const focus_qconfig *q, const void *codes, int64_t K) {
+    return codes && slab_of(q) && K % 128 != 0 ? FOCUS_ERR_SHAPE : FOCUS_OK;
 }
 
 int floor_of(const focus_qconfig *q) { return q->e8m0_rounding == FOCUS_E8M0_FLOOR ? 1 : 0; }
@@ -202,15 +210,17 @@ focus_status focus_fakequant_fwd(const focus_qconfig *q, const void *X, int x_dt
     if (!weight_mode && (c || alpha)) return FOCUS_ERR_CONFIG;
     if (!dtype_ok(x_dtype) || !dtype_ok(xhat_dtype)) return FOCUS_ERR_DTYPE;
     FOCUS_TRY(check_rows_k(rows, K, block_of(q->format)));
+    FOCUS_TRY(check_code_layout(q, codes_opt, K));
     if (!all_aligned({X, X_hat, codes_opt})) return FOCUS_ERR_SHAPE;
     FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_FAKEQUANT_FWD, q, 0, rows, K)));
     if (rows == 0 || K == 0) return FOCUS_OK;
     hipStream_t st = (hipStream_t)stream;
     if (weight_mode)
         return hip_status(launch_fq_weight(q->format, x_dtype, xhat_dtype, X, rows, K, s_fp, c, q->sub_block,
-                                           alpha, floor_of(q), X_hat, codes_opt, scale_bytes_opt, q->scale_layout, flag_of(ws), st));
+                                           alpha, floor_of(q), X_hat, codes_opt, scale_bytes_opt, q->scale_layout,
+                                           slab_of(q), flag_of(ws), st));
     return hip_status(launch_fq_act(q->format, x_dtype, xhat_dtype, X, rows, K, X_hat, codes_opt,
-                                    scale_bytes_opt, q->scale_layout, floor_of(q), alpha_out_opt, partials_of(ws),
+                                    scale_bytes_opt, q->scale_layout, slab_of(q), floor_of(q), alpha_out_opt, partials_of(ws),
                                     flag_of(ws), st));
 }
 
@@ -329,11 +339,13 @@ focus_status focus_export_packed(const focus_qconfig *q, const void *W, int w_dt
     if (q->format == FOCUS_NVFP4 && !alpha) return FOCUS_ERR_NULL;
     if (!dtype_ok(w_dtype)) return FOCUS_ERR_DTYPE;
     FOCUS_TRY(check_rows_k(N, K, block_of(q->format)));
+    FOCUS_TRY(check_code_layout(q, packed, K));
     if (!all_aligned({W, packed})) return FOCUS_ERR_SHAPE;
     FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_EXPORT_PACKED, q, 0, N, K)));
     if (N == 0 || K == 0) return FOCUS_OK;
     return hip_status(launch_fq_weight(q->format, w_dtype, w_dtype, W, N, K, s_fp, c, q->sub_block, alpha,
-                                       floor_of(q), nullptr, packed, scale_bytes, q->scale_layout, flag_of(ws), (hipStream_t)stream));
+                                       floor_of(q), nullptr, packed, scale_bytes, q->scale_layout, slab_of(q), flag_of(ws),
+                                       (hipStream_t)stream));
 }
 
 focus_status focus_fakequant_weights(const focus_qconfig *q, int w_dtype, int what_dtype,
@@ -349,6 +361,7 @@ focus_status focus_fakequant_weights(const focus_qconfig *q, int w_dtype, int wh
         if (l.rows != 0 && (!l.W || !l.s_fp || (!l.W_hat && !l.codes))) return FOCUS_ERR_NULL;
         if (l.rows != 0 && q->format == FOCUS_NVFP4 && !l.alpha) return FOCUS_ERR_NULL;
         FOCUS_TRY(check_rows_k(l.rows, l.K, block_of(q->format)));
+        FOCUS_TRY(check_code_layout(q, l.codes, l.K));
         if (!all_aligned({l.W, l.W_hat, l.codes})) return FOCUS_ERR_SHAPE;
         L[i] = WeightLayer{l.W, l.rows, l.K, l.s_fp, l.c, q->format == FOCUS_NVFP4 ? l.alpha : nullptr,
                            l.W_hat, l.codes, l.scale_bytes};
@@ -356,7 +369,7 @@ focus_status focus_fakequant_weights(const focus_qconfig *q, int w_dtype, int wh
     FOCUS_TRY(check_ws(ws, ws_bytes, focus_workspace_size(FOCUS_CALL_FAKEQUANT_WEIGHTS, q, 0, 0, 0)));
     if (n_layers == 0) return FOCUS_OK;
     return hip_status(launch_fq_weight_group(q->format, w_dtype, what_dtype, L, n_layers, q->sub_block, floor_of(q),
-                                             q->scale_layout, flag_of(ws), (hipStream_t)stream));
+                                             q->scale_layout, slab_of(q), flag_of(ws), (hipStream_t)stream));
 }
 
 focus_status focus_recon_gemm_dx(const void *dY, const void *W_hat, int op_dtype, int64_t M, int64_t N, int64_t K,

@@ -132,6 +132,12 @@ __device__ __forceinline__ void store_tile_scales(const uint8_t (&sb)[NBLK][kTil
 __host__ __device__ inline uint32_t col_tiles(int64_t K) { return (uint32_t)((K + kTileCols - 1) / kTileCols); }
 constexpr uint32_t kMaxTiledGrid = 1u << 23;
 
+// Byte offset of the 4-byte word of packed codes holding elements col .. col + 7 of row r (col % 8 == 0)
+// of a [rows][K] tensor: row-major [rows][K/2], or K-slabs [K/128][rows][64] (code_slab).
+__device__ __forceinline__ int64_t code_word_off(int64_t r, int64_t col, int64_t K, int64_t rows, int code_slab) {
+    return code_slab ? ((col >> 7) * rows + r) * 64 + ((col & 127) >> 1) : (r * K + col) >> 1;
+}
+
 // Arguments of the tiled weight kernels for one layer: rows [row0, row0 + nrows) of a [rows][K] tensor
 // (a launch may cover part of a tensor) with its scales, coefficients and outputs.
 struct WeightJob {
@@ -158,7 +164,7 @@ struct WeightGroup {
 // (one coefficient per chunk fits 96 VGPRs: five waves per SIMD keep more loads in flight)
 template <int FMT, int OUT, int NCOEF>
 __device__ __forceinline__ void fq_weight_tile(const WeightJob &j, uint32_t tile, int sb_log2, int e8m0_floor,
-                                               int block_major, uint32_t *flag) {
+                                               int block_major, int code_slab, uint32_t *flag) {
     const void *__restrict__ W = j.W;
     const float *__restrict__ s_fp = j.s_fp;
     const float *__restrict__ c = j.c;
@@ -170,6 +176,9 @@ __device__ __forceinline__ void fq_weight_tile(const WeightJob &j, uint32_t tile
     constexpr int NBLK = kTileCols / B;
     __shared__ uint8_t sbuf[NBLK][kTileRows];
     const Tile t = tile_of<B>(j.row0, j.nrows, K, j.ctiles, tile);
+    // packed-code word of the thread's chunk 0, and the step to its next chunk (8 rows further)
+    const int64_t cw0 = code_word_off(t.row, t.col, K, rows_total, code_slab);
+    const int64_t cws = code_slab ? (int64_t)kRowStep * 64 : (int64_t)kRowStep * K / 2;
     // NCOEF coefficients per 8-element chunk: 1 for sub-blocks of 8 or more, 2 or 4 for 4 or 2
     constexpr int EPC = 8 / NCOEF;  // elements per coefficient within a chunk
     const float alpha = FMT == kFmtNV ? *j.alpha : 1.0f;
@@ -234,7 +243,7 @@ __device__ __forceinline__ void fq_weight_tile(const WeightJob &j, uint32_t tile
                 for (int e = 0; e < 8; e++) out[e] *= sdq;
                 store8(w_hat, OUT, e0, out);
             }
-            if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+            if (codes) *reinterpret_cast<uint32_t *>(codes + cw0 + i * cws) = packed;
             if (scale_bytes && (t.col % B) == 0) sbuf[(t.col % kTileCols) / B][(int)(r - t.tile_row)] = (uint8_t)byte;
         }
     }
@@ -248,19 +257,19 @@ __device__ __forceinline__ void fq_weight_tile(const WeightJob &j, uint32_t tile
 
 template <int FMT, int OUT, int NCOEF>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NCOEF == 1 ? 5 : 4)))
-fq_weight_kernel(WeightJob j, int sb_log2, int e8m0_floor, int block_major, uint32_t *flag) {
-    fq_weight_tile<FMT, OUT, NCOEF>(j, xcd_contiguous_tile(), sb_log2, e8m0_floor, block_major, flag);
+fq_weight_kernel(WeightJob j, int sb_log2, int e8m0_floor, int block_major, int code_slab, uint32_t *flag) {
+    fq_weight_tile<FMT, OUT, NCOEF>(j, xcd_contiguous_tile(), sb_log2, e8m0_floor, block_major, code_slab, flag);
 }
 
 // The same for several layers in one launch: their tiles are numbered one layer after the other
 // (layer l's from g.first[l]), so one grid covers them all.
 template <int FMT, int OUT, int NCOEF>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NCOEF == 1 ? 5 : 4)))
-fq_weight_group_kernel(WeightGroup g, int sb_log2, int e8m0_floor, int block_major, uint32_t *flag) {
+fq_weight_group_kernel(WeightGroup g, int sb_log2, int e8m0_floor, int block_major, int code_slab, uint32_t *flag) {
     const uint32_t tile = xcd_contiguous_tile();
     int l = 0;
     for (int i = 1; i < g.n; i++) l = tile >= g.first[i] ? i : l;
-    fq_weight_tile<FMT, OUT, NCOEF>(g.job[l], tile - g.first[l], sb_log2, e8m0_floor, block_major, flag);
+    fq_weight_tile<FMT, OUT, NCOEF>(g.job[l], tile - g.first[l], sb_log2, e8m0_floor, block_major, code_slab, flag);
 }
 
 // fp32 weights (the 256-wide fp32 layer): one chunk per thread, true division per element.
@@ -270,7 +279,7 @@ fq_weight_f32_kernel(const void *__restrict__ W, uint32_t nchunks, int64_t row0,
                  const float *__restrict__ s_fp, const float *__restrict__ c, int sb_log2,
                  const float *__restrict__ alpha_ptr, int e8m0_floor, void *__restrict__ w_hat,
                  uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes, int64_t rows_total,
-                 int block_major, uint32_t *flag) {
+                 int block_major, int code_slab, uint32_t *flag) {
     constexpr int B = block_of(FMT);
     const float alpha = FMT == kFmtNV ? *alpha_ptr : 1.0f;
     const int sb = 1 << sb_log2;
@@ -302,7 +311,7 @@ fq_weight_f32_kernel(const void *__restrict__ W, uint32_t nchunks, int64_t row0,
             packed |= z.code << (4 * i);
         }
         if (w_hat) store8(w_hat, OUT, e0, out);
-        if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+        if (codes) *reinterpret_cast<uint32_t *>(codes + (code_slab ? code_word_off(e0 / K, e0 % K, K, rows_total, 1) : e0 / 2)) = packed;
         if (scale_bytes && (e0 % B) == 0) {
             const int64_t row = e0 / K, blk = (e0 - row * K) / B;
             scale_bytes[block_major ? blk * rows_total + row : row * nb + blk] = (uint8_t)byte;
@@ -320,10 +329,13 @@ template <int OUT>
 __global__ void __launch_bounds__(256)
 fq_act_mx_kernel(const void *__restrict__ X, int64_t row0, int64_t rows, int64_t K, uint32_t ctiles,
                       void *__restrict__ x_hat, uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes,
-                      int64_t rows_total, int block_major, int e8m0_floor, uint32_t *flag) {
+                      int64_t rows_total, int block_major, int code_slab, int e8m0_floor, uint32_t *flag) {
     constexpr int NBLK = kTileCols / 32;
     __shared__ uint8_t sbuf[NBLK][kTileRows];
     const Tile t = tile_of<32>(row0, rows, K, ctiles);
+    // packed-code word of the thread's chunk 0, and the step to its next chunk (8 rows further)
+    const int64_t cw0 = code_word_off(t.row, t.col, K, rows_total, code_slab);
+    const int64_t cws = code_slab ? (int64_t)kRowStep * 64 : (int64_t)kRowStep * K / 2;
     bool bad = false;
     uint4 raw[kChunks];
 #pragma unroll
@@ -360,7 +372,7 @@ fq_act_mx_kernel(const void *__restrict__ X, int64_t row0, int64_t rows, int64_t
                 for (int k = 0; k < 8; k++) out[k] *= S;
                 store8(x_hat, OUT, e0, out);
             }
-            if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+            if (codes) *reinterpret_cast<uint32_t *>(codes + cw0 + i * cws) = packed;
             if (scale_bytes && (t.col % 32) == 0) sbuf[(t.col % kTileCols) / 32][(int)(r - t.tile_row)] = (uint8_t)(e + 127);
         }
     }
@@ -376,7 +388,7 @@ template <int OUT>
 __global__ void __launch_bounds__(256)
 fq_act_mx_f32_kernel(const void *__restrict__ X, uint32_t nchunks, int64_t row0, int64_t K,
                  void *__restrict__ x_hat, uint8_t *__restrict__ codes, uint8_t *__restrict__ scale_bytes,
-                 int64_t rows_total, int block_major, int e8m0_floor, uint32_t *flag) {
+                 int64_t rows_total, int block_major, int code_slab, int e8m0_floor, uint32_t *flag) {
     const int64_t e_row0 = row0 * K;
     bool bad = false;
     for (uint32_t t = blockIdx.x * 256u + threadIdx.x; t < nchunks; t += gridDim.x * 256u) {
@@ -401,7 +413,7 @@ fq_act_mx_f32_kernel(const void *__restrict__ X, uint32_t nchunks, int64_t row0,
 #pragma unroll
         for (int i = 0; i < 8; i++) out[i] *= S;
         if (x_hat) store8(x_hat, OUT, e0, out);
-        if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+        if (codes) *reinterpret_cast<uint32_t *>(codes + (code_slab ? code_word_off(e0 / K, e0 % K, K, rows_total, 1) : e0 / 2)) = packed;
         if (scale_bytes && (t & 3u) == 0) {
             const int64_t row = e0 / K, blk = (e0 - row * K) / 32;
             scale_bytes[block_major ? blk * rows_total + row : row * (K / 32) + blk] = (uint8_t)(e + 127);
@@ -469,10 +481,13 @@ template <int OUT>
 __global__ void __launch_bounds__(256)
 fq_act_nv_kernel(const void *__restrict__ X, int64_t row0, int64_t rows, int64_t K, uint32_t ctiles,
                  const float *__restrict__ alpha_slot, void *__restrict__ x_hat, uint8_t *__restrict__ codes,
-                 uint8_t *__restrict__ scale_bytes, int64_t rows_total, int block_major, uint32_t *flag) {
+                 uint8_t *__restrict__ scale_bytes, int64_t rows_total, int block_major, int code_slab, uint32_t *flag) {
     constexpr int NBLK = kTileCols / 16;
     __shared__ uint8_t sbuf[NBLK][kTileRows];
     const Tile t = tile_of<16>(row0, rows, K, ctiles);
+    // packed-code word of the thread's chunk 0, and the step to its next chunk (8 rows further)
+    const int64_t cw0 = code_word_off(t.row, t.col, K, rows_total, code_slab);
+    const int64_t cws = code_slab ? (int64_t)kRowStep * 64 : (int64_t)kRowStep * K / 2;
     const float alpha = *alpha_slot;
     const float alpha6 = alpha * 6.0f;
     bool bad = false;
@@ -521,7 +536,7 @@ fq_act_nv_kernel(const void *__restrict__ X, int64_t row0, int64_t rows, int64_t
                 for (int e = 0; e < 8; e++) out[e] *= S;
                 store8(x_hat, OUT, e0, out);
             }
-            if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+            if (codes) *reinterpret_cast<uint32_t *>(codes + cw0 + i * cws) = packed;
             if (scale_bytes && (t.col % 16) == 0) sbuf[(t.col % kTileCols) / 16][(int)(r - t.tile_row)] = (uint8_t)byte;
         }
     }
@@ -537,7 +552,7 @@ template <int OUT>
 __global__ void __launch_bounds__(256)
 fq_act_nv_f32_kernel(const void *__restrict__ X, uint32_t nchunks, int64_t row0, int64_t K,
                      const float *__restrict__ alpha_slot, void *__restrict__ x_hat, uint8_t *__restrict__ codes,
-                     uint8_t *__restrict__ scale_bytes, int64_t rows_total, int block_major, uint32_t *flag) {
+                     uint8_t *__restrict__ scale_bytes, int64_t rows_total, int block_major, int code_slab, uint32_t *flag) {
     const float alpha = *alpha_slot;
     const float alpha6 = alpha * 6.0f;
     const int64_t e_row0 = row0 * K;  // rows are contiguous: chunk t starts at e_row0 + 8 t
@@ -561,7 +576,7 @@ fq_act_nv_f32_kernel(const void *__restrict__ X, uint32_t nchunks, int64_t row0,
             packed |= z.code << (4 * i);
         }
         if (x_hat) store8(x_hat, OUT, e0, out);
-        if (codes) *reinterpret_cast<uint32_t *>(codes + e0 / 2) = packed;
+        if (codes) *reinterpret_cast<uint32_t *>(codes + (code_slab ? code_word_off(e0 / K, e0 % K, K, rows_total, 1) : e0 / 2)) = packed;
         if (scale_bytes && (t & 1u) == 0) {
             const int64_t row = e0 / K, blk = (e0 - row * K) / 16;
             scale_bytes[block_major ? blk * rows_total + row : row * (K / 16) + blk] = (uint8_t)byte;
@@ -742,13 +757,13 @@ static hipError_t for_tile_ranges(int64_t rows, int64_t K, F &&launch) {
 
 hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64_t rows, int64_t K,
                             const float *s_fp, const float *c, int sb, const float *alpha, int e8m0_floor,
-                            void *w_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, uint32_t *flag,
-                            hipStream_t st) {
+                            void *w_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, int code_slab,
+                            uint32_t *flag, hipStream_t st) {
     const int sbl = log2i(sb);
     if (in_dt == kBF16) {
         return for_tile_ranges(rows, K, [&](int64_t r0, int64_t nr, uint32_t ct, uint32_t grid) {
             const WeightJob j{W, s_fp, c, alpha, w_hat, codes, scale_bytes, r0, nr, rows, K, ct};
-#define FQW(F, O, NC) fq_weight_kernel<F, O, NC><<<grid, 256, 0, st>>>(j, sbl, e8m0_floor, block_major, flag)
+#define FQW(F, O, NC) fq_weight_kernel<F, O, NC><<<grid, 256, 0, st>>>(j, sbl, e8m0_floor, block_major, code_slab, flag)
 #define FQW_NC(F, O) if (sb >= 8) FQW(F, O, 1); else if (sb == 4) FQW(F, O, 2); else FQW(F, O, 4)
             if (fmt == kFmtMX) { if (out_dt == kBF16) FQW_NC(kFmtMX, kBF16); else FQW_NC(kFmtMX, kF32); }
             else { if (out_dt == kBF16) FQW_NC(kFmtNV, kBF16); else FQW_NC(kFmtNV, kF32); }
@@ -758,7 +773,7 @@ hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64
     }
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
         (void)cpr;
-#define FQW(F, O) fq_weight_f32_kernel<F, O><<<grid, 256, 0, st>>>(W, n, r0, K, s_fp, c, sbl, alpha, e8m0_floor, w_hat, codes, scale_bytes, rows, block_major, flag)
+#define FQW(F, O) fq_weight_f32_kernel<F, O><<<grid, 256, 0, st>>>(W, n, r0, K, s_fp, c, sbl, alpha, e8m0_floor, w_hat, codes, scale_bytes, rows, block_major, code_slab, flag)
         if (fmt == kFmtMX) { if (out_dt == kBF16) FQW(kFmtMX, kBF16); else FQW(kFmtMX, kF32); }
         else { if (out_dt == kBF16) FQW(kFmtNV, kBF16); else FQW(kFmtNV, kF32); }
 #undef FQW
@@ -766,13 +781,13 @@ hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64
 }
 
 hipError_t launch_fq_weight_group(int fmt, int in_dt, int out_dt, const WeightLayer *L, int n, int sb,
-                                  int e8m0_floor, int block_major, uint32_t *flag, hipStream_t st) {
+                                  int e8m0_floor, int block_major, int code_slab, uint32_t *flag, hipStream_t st) {
     auto one_by_one = [&]() {
         for (int i = 0; i < n; i++) {
             if (L[i].rows == 0 || L[i].K == 0) continue;
             const hipError_t e = launch_fq_weight(fmt, in_dt, out_dt, L[i].W, L[i].rows, L[i].K, L[i].s_fp, L[i].c, sb,
                                                   L[i].alpha, e8m0_floor, L[i].w_hat, L[i].codes, L[i].scale_bytes,
-                                                  block_major, flag, st);
+                                                  block_major, code_slab, flag, st);
             if (e != hipSuccess) return e;
         }
         return hipSuccess;
@@ -795,7 +810,7 @@ hipError_t launch_fq_weight_group(int fmt, int in_dt, int out_dt, const WeightLa
     g.n = m;
     const uint32_t grid = (uint32_t)total;
     const int sbl = log2i(sb);
-#define FQG(F, O, NC) fq_weight_group_kernel<F, O, NC><<<grid, 256, 0, st>>>(g, sbl, e8m0_floor, block_major, flag)
+#define FQG(F, O, NC) fq_weight_group_kernel<F, O, NC><<<grid, 256, 0, st>>>(g, sbl, e8m0_floor, block_major, code_slab, flag)
 #define FQG_NC(F, O) if (sb >= 8) FQG(F, O, 1); else if (sb == 4) FQG(F, O, 2); else FQG(F, O, 4)
     if (fmt == kFmtMX) { if (out_dt == kBF16) FQG_NC(kFmtMX, kBF16); else FQG_NC(kFmtMX, kF32); }
     else { if (out_dt == kBF16) FQG_NC(kFmtNV, kBF16); else FQG_NC(kFmtNV, kF32); }
@@ -815,18 +830,18 @@ static hipError_t launch_tensor_alpha(int in_dt, const void *X, int64_t n, float
 }
 
 hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t rows, int64_t K,
-                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, int e8m0_floor,
+                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, int code_slab, int e8m0_floor,
                          float *alpha_out, float *partial, uint32_t *flag, hipStream_t st) {
     if (fmt == kFmtMX) {
         if (in_dt == kBF16)
             return for_tile_ranges(rows, K, [&](int64_t r0, int64_t nr, uint32_t ct, uint32_t grid) {
-#define FQA(O) fq_act_mx_kernel<O><<<grid, 256, 0, st>>>(X, r0, nr, K, ct, x_hat, codes, scale_bytes, rows, block_major, e8m0_floor, flag)
+#define FQA(O) fq_act_mx_kernel<O><<<grid, 256, 0, st>>>(X, r0, nr, K, ct, x_hat, codes, scale_bytes, rows, block_major, code_slab, e8m0_floor, flag)
                 if (out_dt == kBF16) FQA(kBF16); else FQA(kF32);
 #undef FQA
             });
         return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
             (void)cpr;
-#define FQA(O) fq_act_mx_f32_kernel<O><<<grid, 256, 0, st>>>(X, n, r0, K, x_hat, codes, scale_bytes, rows, block_major, e8m0_floor, flag)
+#define FQA(O) fq_act_mx_f32_kernel<O><<<grid, 256, 0, st>>>(X, n, r0, K, x_hat, codes, scale_bytes, rows, block_major, code_slab, e8m0_floor, flag)
             if (out_dt == kBF16) FQA(kBF16); else FQA(kF32);
 #undef FQA
         });
@@ -836,13 +851,13 @@ hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t 
     const float *slot = partial + kAbsmaxParts;
     if (in_dt == kBF16)
         return for_tile_ranges(rows, K, [&](int64_t r0, int64_t nr, uint32_t ct, uint32_t grid) {
-#define FQN(O) fq_act_nv_kernel<O><<<grid, 256, 0, st>>>(X, r0, nr, K, ct, slot, x_hat, codes, scale_bytes, rows, block_major, flag)
+#define FQN(O) fq_act_nv_kernel<O><<<grid, 256, 0, st>>>(X, r0, nr, K, ct, slot, x_hat, codes, scale_bytes, rows, block_major, code_slab, flag)
             if (out_dt == kBF16) FQN(kBF16); else FQN(kF32);
 #undef FQN
         });
     return for_row_ranges(rows, K, [&](int64_t r0, uint32_t n, uint32_t cpr, uint32_t grid) {
         (void)cpr;
-#define FQN(O) fq_act_nv_f32_kernel<O><<<grid, 256, 0, st>>>(X, n, r0, K, slot, x_hat, codes, scale_bytes, rows, block_major, flag)
+#define FQN(O) fq_act_nv_f32_kernel<O><<<grid, 256, 0, st>>>(X, n, r0, K, slot, x_hat, codes, scale_bytes, rows, block_major, code_slab, flag)
         if (out_dt == kBF16) FQN(kBF16); else FQN(kF32);
 #undef FQN
     });

@@ -37,7 +37,8 @@ bool mfma_fwd_supported(int64_t M, int64_t N, int64_t K);
 bool mfma_bwd_supported(int64_t M, int64_t N, int64_t K);
 hipError_t launch_fwd_mfma(const void *X, const void *W, int64_t M, int64_t N, int64_t K, const void *Yref,
                            void *dY, float dscale, double *colpart, hipStream_t st);
-// the same product from packed MXFP4 operands (codes [rows][K/2], E8M0 bytes [rows][K/32]; K % 128 == 0)
+// the same product from packed MXFP4 operands (X codes [M][K/2], W codes in K-slabs [K/128][N][64],
+// block-major E8M0 bytes [K/32][rows]; K % 128 == 0)
 bool mfma_fwd_mx_supported(int64_t M, int64_t N, int64_t K);
 hipError_t launch_fwd_mfma_mx(const void *Xc, const void *Xs, const void *Wc, const void *Ws, int64_t M, int64_t N,
                               int64_t K, const void *Yref, void *dY, float dscale, double *colpart, hipStream_t st);

@@ -280,11 +280,12 @@ __device__ __forceinline__ void static_for(F &&f) {
 
 // ------------------------------------------------------------------------------------------------
 // Forward reconstruction GEMM, Y_hat = X_hat W_hat^T with the MSE epilogue (or the plain product).
-// Operands are bf16 (MX == false) or packed MXFP4 (MX == true): codes [rows][K / 2] (two per byte,
-// even k in the low nibble) and E8M0 scale bytes [rows][K / 32], exactly the values X_hat and W_hat
-// hold under MXFP4, multiplied by the block-scaled FP4 MFMA. Both modes stage 64 bytes of each
-// operand row per step (32 bf16 or 128 FP4 k), so the LDS geometry, swizzle, pipeline and epilogue
-// are shared.
+// Operands are bf16 (MX == false) or packed MXFP4 (MX == true): codes (two per byte, even k in the low
+// nibble; X row-major [M][K / 2], W in K-slabs [K / 128][N][64]) and block-major E8M0 scale bytes
+// [K / 32][rows], exactly the values X_hat and W_hat hold under MXFP4, multiplied by the block-scaled
+// FP4 MFMA. Both modes stage 64 bytes of each operand row per step (32 bf16 or 128 FP4 k), so the LDS
+// geometry, swizzle, pipeline and epilogue are shared; in MX mode a step's W tile is one contiguous
+// 16 KB run of its K-slab.
 template <bool MSE, bool MX>
 __global__ void __launch_bounds__(kThreads, 1)
 fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const uint8_t *__restrict__ Xs,
@@ -324,8 +325,14 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     const uint32_t sc_row = ((uint32_t)lane >> 5) * 128u + ((uint32_t)lane & 3u) * 32u + (((uint32_t)lane >> 2) & 7u) * 4u;
     const uint32_t sc_b = (uint32_t)lr & 3u;
     const uint32_t sc_sel = sc_b | 0x0C00u | ((4u + sc_b) << 16) | 0x0C000000u;
-    FwdDma dma;  // X and W rows have the same length, so one set of offsets serves both
+    FwdDma dma;  // X and W rows have the same length, so one set of offsets serves both (bf16; X codes)
     dma.init(pitch, wave_u, lane);
+    // MX: step j's W tile is rows n0 .. n0 + 255 of K-slab j, 64 bytes each, one contiguous run; rows
+    // past N are outside the resource and read as zeros
+    FwdDma dmaw;
+    dmaw.init(64, wave_u, lane);
+    const char *const ws_base = static_cast<const char *>(W) + n0 * 64;
+    const int64_t w_slab = N * 64;
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(static_cast<const char *>(X) + m0 * pitch, (M - m0) * pitch);
     const __amdgpu_buffer_rsrc_t rb = make_rsrc(static_cast<const char *>(W) + n0 * pitch, (N - n0) * pitch);
     // block-major scale bytes [K/32][rows]: a step's 4 blocks of the tile's 256 rows are 4 runs of 256
@@ -356,6 +363,8 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     auto issue_op = [&](lds_char *st, int64_t j, int i) {
         const uint32_t base = (uint32_t)j * 64u, bad = dma.step_bad(pitch, base);  // 64 row bytes per step
         if (i < 4) dma.issue_one(ra, base, bad, st, wave_u, i);
+        else if (MX && i < 8)
+            dmaw.issue_one(make_rsrc(ws_base + j * w_slab, (N - n0) * 64), 0u, 0u, st + kFwdOpBytes, wave_u, i - 4);
         else if (i < 8) dma.issue_one(rb, base, bad, st + kFwdOpBytes, wave_u, i - 4);
         else {
             const uint32_t blk = (uint32_t)j * 4u + wave_u;

@@ -14,8 +14,8 @@ constexpr size_t kWsHeader = 256;     // workspace bytes reserved for the domain
 
 hipError_t launch_fq_weight(int fmt, int in_dt, int out_dt, const void *W, int64_t rows, int64_t K,
                             const float *s_fp, const float *c, int sb, const float *alpha, int e8m0_floor,
-                            void *w_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, uint32_t *flag,
-                            hipStream_t st);
+                            void *w_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, int code_slab,
+                            uint32_t *flag, hipStream_t st);
 // One layer of a grouped weight fake quantisation (the arguments of launch_fq_weight).
 struct WeightLayer {
     const void *W;
@@ -28,9 +28,9 @@ constexpr int kMaxWeightLayers = 16;
 // All layers in one launch where their tiles fit one grid (bf16 weights), else one launch per layer;
 // layer outputs are those of launch_fq_weight either way.
 hipError_t launch_fq_weight_group(int fmt, int in_dt, int out_dt, const WeightLayer *layers, int n, int sb,
-                                  int e8m0_floor, int block_major, uint32_t *flag, hipStream_t st);
+                                  int e8m0_floor, int block_major, int code_slab, uint32_t *flag, hipStream_t st);
 hipError_t launch_fq_act(int fmt, int in_dt, int out_dt, const void *X, int64_t rows, int64_t K,
-                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, int e8m0_floor,
+                         void *x_hat, uint8_t *codes, uint8_t *scale_bytes, int block_major, int code_slab, int e8m0_floor,
                          float *alpha_out, float *partial, uint32_t *flag, hipStream_t st);
 hipError_t launch_scales_init(int fmt, int in_dt, const void *W, int64_t rows, int64_t K, float *s_fp,
                               float *c, int sb, int e8m0_floor, float *alpha_out, float *partial, hipStream_t st);

@@ -31,7 +31,8 @@ EXPORTED = ("focus_workspace_size", "focus_scales_init", "focus_fakequant_fwd", 
 
 class QConfig(ctypes.Structure):
     _fields_ = [("format", ctypes.c_int32), ("sub_block", ctypes.c_int32),
-                ("ste_clip", ctypes.c_int32), ("scale_layout", ctypes.c_int32), ("e8m0_rounding", ctypes.c_int32)]
+                ("ste_clip", ctypes.c_int32), ("scale_layout", ctypes.c_int32), ("e8m0_rounding", ctypes.c_int32),
+                ("code_layout", ctypes.c_int32)]
 
 
 class WeightLayer(ctypes.Structure):
@@ -98,11 +99,24 @@ def status_string(status: int) -> str:
 
 SCALES_ROW_MAJOR, SCALES_BLOCK_MAJOR = 0, 1
 E8M0_CEIL, E8M0_FLOOR = 0, 1
+CODES_ROW_MAJOR, CODES_K_SLAB = 0, 1
 
 
 def qconfig(fmt: int, sub_block: int, ste_clip: int = 1, scale_layout: int = SCALES_ROW_MAJOR,
-            e8m0_rounding: int = 0) -> QConfig:
-    return QConfig(fmt, sub_block, ste_clip, scale_layout, e8m0_rounding)
+            e8m0_rounding: int = 0, code_layout: int = CODES_ROW_MAJOR) -> QConfig:
+    return QConfig(fmt, sub_block, ste_clip, scale_layout, e8m0_rounding, code_layout)
+
+
+def codes_shape(rows: int, K: int, code_layout: int = CODES_ROW_MAJOR) -> tuple:
+    """Shape of a packed-code tensor: [rows][K/2], or K-slabs [K/128][rows][64]."""
+    return (rows, K // 2) if code_layout == CODES_ROW_MAJOR else (K // 128, rows, 64)
+
+
+def _slab_dims(codes: torch.Tensor) -> tuple:
+    """(rows, K) of codes in K-slabs [K/128][rows][64], the layout of the MXFP4 forward's W operand."""
+    if codes.dim() != 3 or codes.shape[2] != 64:
+        raise ValueError("the MXFP4 forward takes W codes in K-slabs [K/128][N][64] (code_layout=CODES_K_SLAB)")
+    return codes.shape[1], codes.shape[0] * 128
 
 
 def block_size(fmt: int) -> int:
@@ -172,21 +186,22 @@ def fakequant_fwd(X: torch.Tensor, fmt: int, sub_block: int = 8, s_fp=None, c=No
                   out_dtype=None, want_codes: bool = False, want_scale_bytes: bool = False,
                   want_alpha: bool = False, ste_clip: int = 1, ws=None, out=None, codes_out=None,
                   scales_out=None, scale_layout: int = SCALES_ROW_MAJOR, e8m0_rounding: int = 0,
-                  want_x_hat: bool = True):
+                  want_x_hat: bool = True, code_layout: int = CODES_ROW_MAJOR):
     """Fake quantisation forward. Weight mode when s_fp is given, dynamic activation mode otherwise.
     codes_out / scales_out: preallocated code and scale-byte outputs (they imply want_codes /
-    want_scale_bytes). scale_layout: [rows][K/B] (row-major) or [K/B][rows] (block-major).
-    want_x_hat=False (with codes) writes the packed form only.
+    want_scale_bytes). scale_layout: [rows][K/B] (row-major) or [K/B][rows] (block-major); code_layout:
+    [rows][K/2] (row-major) or [K/128][rows][64] (K-slabs). want_x_hat=False (with codes) writes the
+    packed form only.
 
     Returns (x_hat or None, packed_codes or None, scale_bytes or None, alpha_x or None)."""
     rows, K = X.shape
-    q = qconfig(fmt, sub_block, ste_clip, scale_layout, e8m0_rounding)
+    q = qconfig(fmt, sub_block, ste_clip, scale_layout, e8m0_rounding, code_layout)
     out_dtype = out_dtype or X.dtype
     x_hat = out if out is not None else (torch.empty(rows, K, dtype=out_dtype, device=X.device) if want_x_hat
                                          else None)
     codes = codes_out
     if codes is None and want_codes:
-        codes = torch.empty(rows, K // 2, dtype=torch.uint8, device=X.device)
+        codes = torch.empty(*codes_shape(rows, K, code_layout), dtype=torch.uint8, device=X.device)
     sbytes = scales_out
     if sbytes is None and want_scale_bytes:
         shape = (rows, K // block_size(fmt)) if scale_layout == SCALES_ROW_MAJOR else (K // block_size(fmt), rows)
@@ -234,10 +249,10 @@ def recon_gemm_fwd(X_hat: torch.Tensor, W_hat: torch.Tensor, Y_ref=None, want_co
 
 def recon_gemm_fwd_mxfp4(X_codes: torch.Tensor, X_scales: torch.Tensor, W_codes: torch.Tensor, W_scales: torch.Tensor,
                          Y_ref=None, want_col_sq: bool = False, ws=None, out=None, loss=None):
-    """The forward from packed MXFP4 operands (codes [rows][K/2], block-major E8M0 bytes [K/32][rows])
-    -> as recon_gemm_fwd."""
+    """The forward from packed MXFP4 operands (X codes [M][K/2], W codes in K-slabs [K/128][N][64],
+    block-major E8M0 bytes [K/32][rows]) -> as recon_gemm_fwd."""
     M, K = X_codes.shape[0], X_codes.shape[1] * 2
-    N = W_codes.shape[0]
+    N = _slab_dims(W_codes)[0]
     dev = X_codes.device
     dY = out if out is not None else torch.empty(M, N, dtype=torch.bfloat16, device=dev)
     loss_t = None
@@ -258,7 +273,7 @@ def recon_gemm_fwd_mxfp4_noalloc(X_codes: torch.Tensor, X_scales: torch.Tensor, 
     library allocates nothing; the caller passes dY (`out`), `loss` when Y_ref is given, and
     optionally `col_sq` [N] float64. -> (dY, loss, col_sq)."""
     M, K = X_codes.shape[0], X_codes.shape[1] * 2
-    N = W_codes.shape[0]
+    N = _slab_dims(W_codes)[0]
     if out is None or (Y_ref is not None and loss is None):
         raise ValueError("recon_gemm_fwd_mxfp4_noalloc: pass the outputs (out, and loss with Y_ref)")
     _check(lib().focus_recon_gemm_fwd_mxfp4_noalloc(_ptr(X_codes), _ptr(X_scales), _ptr(W_codes), _ptr(W_scales),
@@ -308,12 +323,13 @@ def recon_gemm_bwd_mxfp4(dY: torch.Tensor, X_codes: torch.Tensor, X_scales: torc
 
 
 def export_packed(W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha=None, ws=None, out=None,
-                  scale_layout: int = SCALES_ROW_MAJOR, e8m0_rounding: int = 0):
-    """Deployable export -> (packed codes [N][K/2], scale bytes [N][K/B] or, block-major, [K/B][N])."""
+                  scale_layout: int = SCALES_ROW_MAJOR, e8m0_rounding: int = 0, code_layout: int = CODES_ROW_MAJOR):
+    """Deployable export -> (packed codes [N][K/2] or, in K-slabs, [K/128][N][64]; scale bytes [N][K/B] or,
+    block-major, [K/B][N])."""
     N, K = W.shape
-    q = qconfig(fmt, sub_block, 1, scale_layout, e8m0_rounding)
+    q = qconfig(fmt, sub_block, 1, scale_layout, e8m0_rounding, code_layout)
     if out is None:
-        packed = torch.empty(N, K // 2, dtype=torch.uint8, device=W.device)
+        packed = torch.empty(*codes_shape(N, K, code_layout), dtype=torch.uint8, device=W.device)
         shape = (N, K // block_size(fmt)) if scale_layout == SCALES_ROW_MAJOR else (K // block_size(fmt), N)
         sbytes = torch.empty(*shape, dtype=torch.uint8, device=W.device)
     else:
@@ -326,12 +342,13 @@ def export_packed(W: torch.Tensor, fmt: int, sub_block: int, s_fp, c=None, alpha
 
 
 def fakequant_weights(layers, fmt: int, sub_block: int, w_dtype=None, what_dtype=None, ws=None,
-                      scale_layout: int = SCALES_ROW_MAJOR, e8m0_rounding: int = 0) -> None:
+                      scale_layout: int = SCALES_ROW_MAJOR, e8m0_rounding: int = 0,
+                      code_layout: int = CODES_ROW_MAJOR) -> None:
     """Weight fake quantisation of several layers in one call (focus_fakequant_weights). `layers` is a
     sequence of dicts with keys W, s_fp and optionally c, alpha, W_hat, codes, scale_bytes (device
     tensors; the outputs are written in place). w_dtype / what_dtype default to the first layer's W /
     W_hat dtype."""
-    q = qconfig(fmt, sub_block, 1, scale_layout, e8m0_rounding)
+    q = qconfig(fmt, sub_block, 1, scale_layout, e8m0_rounding, code_layout)
     arr = (WeightLayer * max(1, len(layers)))()
     for i, l in enumerate(layers):
         W = l["W"]

@@ -45,6 +45,15 @@ def device_bits(t: torch.Tensor) -> np.ndarray:
     return host_bits16(t) if t.dtype == torch.bfloat16 else host_bits32(t)
 
 
+def to_k_slabs(codes):
+    """Packed codes [rows][K/2] rearranged into K-slabs [K/128][rows][64] (data movement only)."""
+    rows, half = codes.shape
+    assert half % 64 == 0
+    if isinstance(codes, torch.Tensor):
+        return codes.reshape(rows, half // 64, 64).transpose(0, 1).contiguous()
+    return np.ascontiguousarray(np.asarray(codes).reshape(rows, half // 64, 64).transpose(1, 0, 2))
+
+
 def assert_bits_equal(got: np.ndarray, ref: np.ndarray, what: str) -> None:
     got = np.asarray(got)
     ref = np.asarray(ref)

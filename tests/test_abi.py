@@ -80,6 +80,13 @@ def test_argument_checks(L, cpu_only):
     assert fq_fwd(L, focus.QConfig(0, 8, 1, 5)) == focus.ERR_CONFIG  # no such scale layout
     assert fq_fwd(L, focus.QConfig(0, 8, 1, 0, 2)) == focus.ERR_CONFIG  # no such E8M0 rounding
     assert fq_fwd(L, focus.QConfig(1, 8, 1, 0, 1), K=64) == focus.ERR_CONFIG  # floor E8M0 is MXFP4 only
+    assert fq_fwd(L, focus.QConfig(0, 8, 1, 0, 0, 2)) == focus.ERR_CONFIG  # no such code layout
+    slab = focus.qconfig(focus.MXFP4, 8, code_layout=focus.CODES_K_SLAB)
+    # K-slab codes need whole slabs of 128 elements (only where codes are written)
+    assert L.focus_fakequant_fwd(ctypes.byref(slab), BOGUS, 1, 4, 96, None, None, None, BOGUS, 1, BOGUS, None, None,
+                                 BOGUS, 1 << 20, None) == focus.ERR_SHAPE
+    assert L.focus_export_packed(ctypes.byref(slab), BOGUS, 1, 4, 96, BOGUS, None, None, BOGUS, BOGUS, BOGUS, 1 << 20,
+                                 None) == focus.ERR_SHAPE
     assert fq_fwd(L, mx, X=None) == focus.ERR_NULL
     # an empty tensor may come as NULL pointers (nothing is launched)
     assert L.focus_fakequant_fwd(ctypes.byref(mx), None, 1, 0, 64, None, None, None, None, 1, None, None, None,
@@ -146,7 +153,7 @@ def test_argument_checks(L, cpu_only):
     assert nal(BOGUS, BOGUS, BOGUS, BOGUS, M, n_col + 8, 128, BOGUS, BOGUS, BOGUS, BOGUS, None) == focus.ERR_SCRATCH
     # fused backward from packed MXFP4 activations
     mxb = L.focus_recon_gemm_bwd_mxfp4
-    def bwd_mx(q, M=8, N=8, K=64, scales=BOGUS, ws_bytes=1 << 30, w_dt=1):
+    def bwd_mx(q, M=8, N=8, K=128, scales=BOGUS, ws_bytes=1 << 30, w_dt=1):
         return mxb(ctypes.byref(q), BOGUS, BOGUS, scales, M, N, K, BOGUS, w_dt, BOGUS, None, BOGUS, BOGUS, BOGUS,
                    ws_bytes, None)
     assert bwd_mx(nv) == focus.ERR_CONFIG                   # MXFP4 only
@@ -218,6 +225,12 @@ def test_grouped_weight_argument_checks(L, cpu_only):
     assert call(mx, table(3, {(1, "codes"): None}), 3) == focus.ERR_NULL   # W_hat and codes both NULL
     assert call(mx, table(3, {(0, "W"): BOGUS.value + 8}), 3) == focus.ERR_SHAPE  # not 16-byte aligned
     assert call(nv, table(3), 3) == focus.ERR_NULL                           # NVFP4 needs alpha
+    slab = focus.qconfig(focus.MXFP4, 8, code_layout=focus.CODES_K_SLAB)
+    assert call(slab, table(3, {(1, "K"): 96}), 3) == focus.ERR_SHAPE        # K-slab codes need K % 128 == 0
+    # a layer that writes no codes may have any K: the call gets as far as the workspace check
+    w_hat_only = table(3, {(0, "K"): 128, (2, "K"): 128, (1, "K"): 96, (1, "codes"): None,
+                           (1, "W_hat"): BOGUS.value})
+    assert call(slab, w_hat_only, 3, ws_bytes=16) == focus.ERR_WORKSPACE
     assert call(mx, table(3), 3, ws=None) == focus.ERR_WORKSPACE
     assert call(mx, table(3), 3, ws_bytes=16) == focus.ERR_WORKSPACE
     # no layers, or only empty layers (NULL pointers allowed): nothing is launched

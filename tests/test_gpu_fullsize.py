@@ -18,7 +18,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_common import announce, assert_bits_equal, assert_close, host_f32, require_gpu
+from gpu_common import announce, assert_bits_equal, assert_close, host_f32, require_gpu, to_k_slabs
 
 pytestmark = pytest.mark.gpu
 
@@ -108,7 +108,7 @@ def test_fullsize_layer(F, O, name, layer):
         bm = F.SCALES_BLOCK_MAJOR
         _, xc0, xs0, _ = F.fakequant_fwd(X, fmt, sb, want_codes=True, want_scale_bytes=True, want_x_hat=False,
                                          scale_layout=bm)
-        wc0, ws0 = F.export_packed(W, fmt, sb, s_d, c_d, a_d, scale_layout=bm)
+        wc0, ws0 = F.export_packed(W, fmt, sb, s_d, c_d, a_d, scale_layout=bm, code_layout=F.CODES_K_SLAB)
         dY0, loss0, col0 = F.recon_gemm_fwd_mxfp4(xc0, xs0, wc0, ws0, Y, want_col_sq=True)
         gs0, gc0 = F.recon_gemm_bwd_mxfp4(dY0, xc0, xs0, W, sb, s_d, c_d)
         del xc0, xs0, wc0, ws0
@@ -160,12 +160,12 @@ def test_fullsize_layer(F, O, name, layer):
     bm = F.SCALES_BLOCK_MAJOR
     _, xc, xs, _ = F.fakequant_fwd(X, fmt, sb, want_codes=True, want_scale_bytes=True, want_x_hat=False,
                                    scale_layout=bm)
-    wc, ws = F.export_packed(W, fmt, sb, s_d, c_d, a_d, scale_layout=bm)
+    wc, ws = F.export_packed(W, fmt, sb, s_d, c_d, a_d, scale_layout=bm, code_layout=F.CODES_K_SLAB)
     _, xcodes_o, xbytes_o, _ = O.fq_act(host_f32(X), fmt)
     assert_bits_equal(xc.cpu().numpy(), O.pack_codes(xcodes_o), "activation codes")
     assert_bits_equal(xs.cpu().numpy(), np.ascontiguousarray(xbytes_o.T), "activation scale bytes (block-major)")
     del xcodes_o, xbytes_o
-    assert_bits_equal(wc.cpu().numpy(), O.pack_codes(fq.codes), "weight codes")
+    assert_bits_equal(wc.cpu().numpy(), to_k_slabs(O.pack_codes(fq.codes)), "weight codes (K-slabs)")
     assert_bits_equal(ws.cpu().numpy(), np.ascontiguousarray(fq.scale_bytes.T), "weight scale bytes (block-major)")
     dYm, lossm, colm = F.recon_gemm_fwd_mxfp4(xc, xs, wc, ws, Y, want_col_sq=True)
     gsm, gcm = F.recon_gemm_bwd_mxfp4(dYm, xc, xs, W, sb, s_d, c_d)

@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_common import announce, assert_bits_equal, assert_close, host_f32, require_gpu
+from gpu_common import announce, assert_bits_equal, assert_close, host_f32, require_gpu, to_k_slabs
 
 pytestmark = pytest.mark.gpu
 
@@ -61,7 +61,7 @@ def test_packed_step_init_state(F, O, oracle_acts, layer):
     _, xc, xs, _ = F.fakequant_fwd(X, fmt, sb, want_codes=True, want_scale_bytes=True, want_x_hat=False,
                                    scale_layout=bm)
     s_d, c_d, a_d = F.scales_init(W, fmt, sb)
-    wc, ws = F.export_packed(W, fmt, sb, s_d, c_d, a_d, scale_layout=bm)
+    wc, ws = F.export_packed(W, fmt, sb, s_d, c_d, a_d, scale_layout=bm, code_layout=F.CODES_K_SLAB)
     dY, loss, col = F.recon_gemm_fwd_mxfp4(xc, xs, wc, ws, Y, want_col_sq=True)
     gs, gc = F.recon_gemm_bwd_mxfp4(dY, xc, xs, W, sb, s_d, c_d)
     torch.cuda.synchronize()
@@ -80,7 +80,7 @@ def test_packed_step_init_state(F, O, oracle_acts, layer):
     s_o, c_o, a_o = O.init_scales(Wh, fmt, sb)
     assert_bits_equal(s_d.cpu().numpy().view(np.uint32), s_o.view(np.uint32), "s_fp init")
     fq = O.fq_weight(Wh, fmt, sb, s_o, c_o, a_o)
-    assert_bits_equal(wc.cpu().numpy(), O.pack_codes(fq.codes), "weight codes")
+    assert_bits_equal(wc.cpu().numpy(), to_k_slabs(O.pack_codes(fq.codes)), "weight codes (K-slabs)")
     assert_bits_equal(ws.cpu().numpy(), np.ascontiguousarray(fq.scale_bytes.T), "weight scale bytes (block-major)")
 
     rows = sample_rows(lin.N, outl, 7)

@@ -39,12 +39,12 @@ def layer_step(F, w, lin, packed):
     if packed:
         xc = torch.empty(M, K // 2, dtype=torch.uint8, device="cuda")
         xs = torch.empty(K // 32, M, dtype=torch.uint8, device="cuda")
-        wc = torch.empty(N, K // 2, dtype=torch.uint8, device="cuda")
+        wc = torch.empty(*F.codes_shape(N, K, F.CODES_K_SLAB), dtype=torch.uint8, device="cuda")
         wsb = torch.empty(K // 32, N, dtype=torch.uint8, device="cuda")
 
         def step():
             F.fakequant_fwd(X, fmt, sb, ws=ws_fq, want_x_hat=False, codes_out=xc, scales_out=xs, scale_layout=bm)
-            F.export_packed(W, fmt, sb, s, c, a, ws=ws_fq, out=(wc, wsb), scale_layout=bm)
+            F.export_packed(W, fmt, sb, s, c, a, ws=ws_fq, out=(wc, wsb), scale_layout=bm, code_layout=F.CODES_K_SLAB)
             F.recon_gemm_fwd_mxfp4(xc, xs, wc, wsb, Y, ws=ws_fwd, out=out["dY"], loss=out["loss"])
             F.recon_gemm_bwd_mxfp4(out["dY"], xc, xs, W, sb, s, c, ws=ws_bwd, out=(out["gs"], out["gc"]))
     else:

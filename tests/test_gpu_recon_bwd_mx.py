@@ -166,7 +166,7 @@ def test_packed_step_is_deterministic(F):
         _, xc, xs, _ = F.fakequant_fwd(X, MX, 8, want_codes=True, want_scale_bytes=True, want_x_hat=False,
                                        scale_layout=bm)
         s, c, a = F.scales_init(W, MX, 8)
-        wc, ws = F.export_packed(W, MX, 8, s, c, a, scale_layout=bm)
+        wc, ws = F.export_packed(W, MX, 8, s, c, a, scale_layout=bm, code_layout=F.CODES_K_SLAB)
         dY, loss, col = F.recon_gemm_fwd_mxfp4(xc, xs, wc, ws, Y, want_col_sq=True)
         gs, gc = F.recon_gemm_bwd_mxfp4(dY, xc, xs, W, 8, s, c)
         outs.append([t.cpu().clone() for t in (dY, loss, col, gs, gc)])

@@ -20,7 +20,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_common import announce, assert_close, host_f32, require_gpu
+from gpu_common import to_k_slabs, announce, assert_close, host_f32, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -47,11 +47,12 @@ def perturb(seed, s_fp, c):
 
 
 def device_operands(F, X, W, sb, s_d, c_d, a_d):
-    """bf16 X_hat, W_hat and the packed codes + block-major scale bytes of both, from the library."""
-    bm = F.SCALES_BLOCK_MAJOR
+    """bf16 X_hat, W_hat and the packed operands of both (X codes row-major, W codes in K-slabs, scale bytes
+    block-major), from the library."""
+    bm, slab = F.SCALES_BLOCK_MAJOR, F.CODES_K_SLAB
     x_hat, xc, xs, _ = F.fakequant_fwd(X, MX, sb, want_codes=True, want_scale_bytes=True, scale_layout=bm)
     w_hat, wc, ws, _ = F.fakequant_fwd(W, MX, sb, s_d, c_d, a_d, want_codes=True, want_scale_bytes=True,
-                                       scale_layout=bm)
+                                       scale_layout=bm, code_layout=slab)
     return x_hat, w_hat, xc, xs, wc, ws
 
 
@@ -138,20 +139,38 @@ def test_mx_forward_fullsize_gate(F, O):
     check_layer(F, O, X, W, Y, w.sub_block, "perturbed", "fullsize gate", rows=rows)
 
 
-def test_block_major_scales_are_the_transpose(F):
-    announce("block-major scale bytes")
+def test_gemm_layouts_are_permutations(F):
+    """Block-major scale bytes are the transpose of the row-major ones, K-slab codes the row-major codes
+    rearranged, for every call that writes them."""
+    announce("block-major scale bytes and K-slab codes")
     g = torch.Generator().manual_seed(9)
     X = torch.randn(300, 640, generator=g).to(torch.bfloat16).cuda()
     W = (torch.randn(72, 640, generator=g) * 0.02).to(torch.bfloat16).cuda()
-    bm = F.SCALES_BLOCK_MAJOR
+    bm, slab = F.SCALES_BLOCK_MAJOR, F.CODES_K_SLAB
     for fmt in (0, 1):
         _, c0, s0, _ = F.fakequant_fwd(X, fmt, 8, want_codes=True, want_scale_bytes=True)
         _, c1, s1, _ = F.fakequant_fwd(X, fmt, 8, want_codes=True, want_scale_bytes=True, scale_layout=bm)
         assert torch.equal(c0, c1) and torch.equal(s0.t().contiguous(), s1), f"activation fmt {fmt}"
+        _, c2, _, _ = F.fakequant_fwd(X, fmt, 8, want_codes=True, code_layout=slab)
+        assert torch.equal(to_k_slabs(c0), c2), f"activation K-slabs fmt {fmt}"
         s, c, a = F.scales_init(W, fmt, 8)
         _, w0, t0, _ = F.fakequant_fwd(W, fmt, 8, s, c, a, want_codes=True, want_scale_bytes=True)
         _, w1, t1, _ = F.fakequant_fwd(W, fmt, 8, s, c, a, want_codes=True, want_scale_bytes=True, scale_layout=bm)
         assert torch.equal(w0, w1) and torch.equal(t0.t().contiguous(), t1), f"weight fmt {fmt}"
+        _, w2, _, _ = F.fakequant_fwd(W, fmt, 8, s, c, a, want_codes=True, code_layout=slab)
+        assert torch.equal(to_k_slabs(w0), w2), f"weight K-slabs fmt {fmt}"
         p0, e0 = F.export_packed(W, fmt, 8, s, c, a)
         p1, e1 = F.export_packed(W, fmt, 8, s, c, a, scale_layout=bm)
         assert torch.equal(p0, p1) and torch.equal(e0.t().contiguous(), e1), f"export fmt {fmt}"
+        p2, _ = F.export_packed(W, fmt, 8, s, c, a, code_layout=slab)
+        assert torch.equal(to_k_slabs(p0), p2), f"export K-slabs fmt {fmt}"
+        g2 = [dict(W=W, s_fp=s, c=c, alpha=a, codes=torch.empty_like(p2))]
+        F.fakequant_weights(g2, fmt, 8, code_layout=slab)
+        assert torch.equal(g2[0]["codes"], p2), f"grouped K-slabs fmt {fmt}"
+        # fp32 inputs take the one-chunk-per-thread kernels
+        _, c3, _, _ = F.fakequant_fwd(X.float(), fmt, 8, want_codes=True, want_x_hat=False, code_layout=slab)
+        assert torch.equal(c3, c2), f"fp32 activation K-slabs fmt {fmt}"
+        _, w3, _, _ = F.fakequant_fwd(W.float(), fmt, 8, s, c, a, want_codes=True, want_x_hat=False,
+                                      code_layout=slab)
+        _, w4, _, _ = F.fakequant_fwd(W.float(), fmt, 8, s, c, a, want_codes=True, want_x_hat=False)
+        assert torch.equal(to_k_slabs(w4), w3), f"fp32 weight K-slabs fmt {fmt}"

@@ -112,20 +112,20 @@ def full_size_layers(F, workload, perturb):
 
 
 def test_group_equals_per_layer_export_hidden8192(F):
-    """The benchmark's packed step: every linear of the hidden-8192 MXFP4 block in one launch, block-major
-    bytes, against one export call per linear (whole tensors, on the device)."""
+    """The benchmark's packed step: every linear of the hidden-8192 MXFP4 block in one launch, K-slab codes
+    and block-major bytes, against one export call per linear (whole tensors, on the device)."""
     for perturb in (False, True):
         w, layers = full_size_layers(F, "block8192_mxfp4", perturb)
         announce(f"weight group vs per-layer export, block8192_mxfp4, perturbed={perturb}")
         group, ref = [], []
         for lin, l in layers:
             N, K = l["W"].shape
-            g = dict(l, codes=torch.empty(N, K // 2, dtype=torch.uint8, device="cuda"),
+            g = dict(l, codes=torch.empty(*F.codes_shape(N, K, F.CODES_K_SLAB), dtype=torch.uint8, device="cuda"),
                      scale_bytes=torch.empty(K // 32, N, dtype=torch.uint8, device="cuda"))
             group.append(g)
             ref.append(F.export_packed(l["W"], w.fmt, w.sub_block, l["s_fp"], l["c"], l["alpha"],
-                                       scale_layout=F.SCALES_BLOCK_MAJOR))
-        F.fakequant_weights(group, w.fmt, w.sub_block, scale_layout=F.SCALES_BLOCK_MAJOR)
+                                       scale_layout=F.SCALES_BLOCK_MAJOR, code_layout=F.CODES_K_SLAB))
+        F.fakequant_weights(group, w.fmt, w.sub_block, scale_layout=F.SCALES_BLOCK_MAJOR, code_layout=F.CODES_K_SLAB)
         torch.cuda.synchronize()
         for (lin, _), g, (codes, sbytes) in zip(layers, group, ref):
             assert torch.equal(g["codes"], codes), f"codes {lin.name}"

@@ -23,7 +23,7 @@ def F():
 
 
 def operands(F, M, N, K, seed):
-    """Packed MXFP4 codes + block-major E8M0 bytes of a seeded X [M][K] and W [N][K], and Y_ref."""
+    """Packed MXFP4 codes (W in K-slabs) + block-major E8M0 bytes of a seeded X [M][K] and W [N][K], and Y_ref."""
     g = torch.Generator(device="cuda").manual_seed(seed)
     X = torch.randn(M, K, device="cuda", generator=g).to(torch.bfloat16)
     W = (torch.randn(N, K, device="cuda", generator=g) * 0.02).to(torch.bfloat16)
@@ -32,7 +32,7 @@ def operands(F, M, N, K, seed):
     _, xc, xs, _ = F.fakequant_fwd(X, MX, 8, want_codes=True, want_scale_bytes=True, want_x_hat=False,
                                    scale_layout=bm)
     _, wc, ws, _ = F.fakequant_fwd(W, MX, 8, want_codes=True, want_scale_bytes=True, want_x_hat=False,
-                                   scale_layout=bm)
+                                   scale_layout=bm, code_layout=F.CODES_K_SLAB)
     return xc, xs, wc, ws, Y
 
 
@@ -76,9 +76,9 @@ def test_noalloc_matches_the_workspace_forward_twice(F):
 
 
 def test_noalloc_refuses_sizes_beyond_the_scratch(F):
-    xc = torch.empty(65536, 64, dtype=torch.uint8, device="cuda")
+    xc = torch.empty(65536, 64, dtype=torch.uint8, device="cuda")  # K = 128
     xs = torch.empty(4, 65536, dtype=torch.uint8, device="cuda")
-    wc = torch.empty(20480, 64, dtype=torch.uint8, device="cuda")
+    wc = torch.empty(1, 20480, 64, dtype=torch.uint8, device="cuda")  # K-slabs
     ws = torch.empty(4, 20480, dtype=torch.uint8, device="cuda")
     Y = torch.empty(1, dtype=torch.bfloat16, device="cuda")  # never read: the size check comes first
     dy = torch.empty(1, dtype=torch.bfloat16, device="cuda")
