@@ -5,7 +5,8 @@ nothing (outputs and workspaces come from the caller), so a caller can capture a
 and replay it. Checked on the fp32 layer (VALU kernels), on a bf16 MXFP4 layer with bf16 operands
 (MFMA kernels) and with packed operands (FP4-MFMA forward, backward from packed activations): the
 step captured with torch.cuda.graph, then three replays, each after eager work of the program's own
-and a synchronisation, each compared with the eager step on loss, dY and both gradients.
+and a synchronisation, each compared with the eager step on loss, dY and both gradients. The weight
+pass goes through the grouped call (focus_fakequant_weights), as the benchmark's step does.
 """
 import pytest
 import torch
@@ -44,7 +45,8 @@ def layer_step(F, w, lin, packed):
 
         def step():
             F.fakequant_fwd(X, fmt, sb, ws=ws_fq, want_x_hat=False, codes_out=xc, scales_out=xs, scale_layout=bm)
-            F.export_packed(W, fmt, sb, s, c, a, ws=ws_fq, out=(wc, wsb), scale_layout=bm, code_layout=F.CODES_K_SLAB)
+            F.fakequant_weights([dict(W=W, s_fp=s, c=c, alpha=a, codes=wc, scale_bytes=wsb)], fmt, sb, ws=ws_fq,
+                                scale_layout=bm, code_layout=F.CODES_K_SLAB)
             F.recon_gemm_fwd_mxfp4(xc, xs, wc, wsb, Y, ws=ws_fwd, out=out["dY"], loss=out["loss"])
             F.recon_gemm_bwd_mxfp4(out["dY"], xc, xs, W, sb, s, c, ws=ws_bwd, out=(out["gs"], out["gc"]))
     else:
@@ -52,7 +54,7 @@ def layer_step(F, w, lin, packed):
 
         def step():
             F.fakequant_fwd(X, fmt, sb, ws=ws_fq, out=xh)
-            F.fakequant_fwd(W, fmt, sb, s, c, a, ws=ws_fq, out=wh)
+            F.fakequant_weights([dict(W=W, s_fp=s, c=c, alpha=a, W_hat=wh)], fmt, sb, ws=ws_fq)
             F.recon_gemm_fwd(xh, wh, Y, ws=ws_fwd, out=out["dY"], loss=out["loss"])
             F.recon_gemm_bwd(out["dY"], xh, W, fmt, sb, s, c, a, ws=ws_bwd, out=(out["gs"], out["gc"]))
     return step, out, X
