@@ -452,7 +452,7 @@ def main():
     result["export"] = opt["export"]
     big = max(w.linears, key=lambda l: l.N * l.K)
     result["attainable"] = attainable(torch, fq_GBps=fq_bytes / (fq_ms * 1e-3) / 1e9,
-                                      layer=(M, big.N, big.K) if esz == 2 else None)
+                                      layer=(M, big.N, big.K) if esz == 2 else None, mx=mx_possible)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens, args.cpu_sample_rows)
     print(json.dumps(result), flush=True)
@@ -621,11 +621,13 @@ def cpu_model():
     return "unknown"
 
 
-def attainable(torch, fq_GBps, layer=None):
+def attainable(torch, fq_GBps, layer=None, mx=False):
     """Measured attainable rates on this GPU as secondary denominators (not the product's code): a
     1 GiB device copy, a large bf16 library GEMM (torch.mm, 8192^3, random data) and, for `layer`
     = (M, N, K), the library GEMM on that layer's forward ([M][K] x [K][N]) and backward
-    ([K][M] x [M][N]) shapes, plain products without the fused epilogues."""
+    ([K][M] x [M][N]) shapes, plain products without the fused epilogues; with `mx`, also the
+    library's block-scaled MXFP4 GEMM on the forward shape (torch._scaled_mm on E2M1 operands with
+    E8M0 scales per 32, bf16 out; null where this torch build does not offer it)."""
     src = torch.randn(1 << 28, device="cuda").to(torch.bfloat16)
     dst = torch.empty_like(src)
     a = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
@@ -656,6 +658,31 @@ def attainable(torch, fq_GBps, layer=None):
     if layer:
         out["library_layer_gemm"] = {"shape_MNK": list(layer), "fwd_TFLOPs": round(res["layer_fwd"] / 1e12, 1),
                                      "bwd_TFLOPs": round(res["layer_bwd"] / 1e12, 1)}
+        del xf, wf, xb, yb
+    if layer and mx:
+        out["library_layer_gemm"]["fwd_mxfp4_TFLOPs"] = None
+        try:
+            M, N, K = layer
+            u8 = dict(dtype=torch.uint8, device="cuda")
+            a4 = torch.randint(0, 256, (M, K // 2), **u8).view(torch.float4_e2m1fn_x2)
+            b4 = torch.randint(0, 256, (N, K // 2), **u8).view(torch.float4_e2m1fn_x2)
+            sa = torch.randint(118, 124, (M, K // 32), **u8).view(torch.float8_e8m0fnu)
+            sb = torch.randint(118, 124, (N, K // 32), **u8).view(torch.float8_e8m0fnu)
+            fn = lambda: torch._scaled_mm(a4, b4.t(), sa, sb, out_dtype=torch.bfloat16)
+            fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(5):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            tf = 2 * M * N * K / (e0.elapsed_time(e1) / 5 * 1e-3) / 1e12
+            out["library_layer_gemm"]["fwd_mxfp4_TFLOPs"] = round(tf, 1)
+            out["library_layer_gemm"]["fwd_mxfp4_frac"] = round(tf / PEAK_FP4_TFLOPS, 4)
+            del a4, b4, sa, sb
+        except (RuntimeError, AttributeError, TypeError) as e:  # no MX path in this torch build
+            out["library_layer_gemm"]["fwd_mxfp4_error"] = str(e)[:200]
     return out
 
 
