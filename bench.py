@@ -37,6 +37,8 @@ def parse():
     p.add_argument("--summarize-mfma", metavar="DIR",
                    help="write the MFMA-utilisation summary from the rocprofv3 --pmc output directory of a "
                         "--steps 1 --warmup 0 --copy-calibration run with the counters of PMC_MFMA and exit")
+    p.add_argument("--summarize-memory", metavar="DIR",
+                   help="write profiles/gemm_memory_<workload>.md from a rocprofv3 --pmc run of PMC_MEM")
     p.add_argument("--summarize-stalls", metavar="DIR",
                    help="write the wave-cycle breakdown of the GEMMs from the rocprofv3 --pmc output directory of a "
                         "--steps 1 --warmup 0 run with the counters of PMC_STALL and exit")
@@ -128,7 +130,8 @@ def traffic_from_profile(kernel: str, src_hash: str, path):
 
 def main():
     args = parse()
-    if args.summarize_trace or args.summarize_counters or args.summarize_mfma or args.summarize_stalls:
+    if (args.summarize_trace or args.summarize_counters or args.summarize_mfma or args.summarize_stalls
+            or args.summarize_memory):
         if args.summarize_trace:
             summarize_trace(args.summarize_trace, args.workload)
         if args.summarize_counters:
@@ -137,6 +140,8 @@ def main():
             summarize_mfma(args.summarize_mfma, args.workload)
         if args.summarize_stalls:
             summarize_stalls(args.summarize_stalls, args.workload)
+        if args.summarize_memory:
+            summarize_memory(args.summarize_memory, args.workload)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the data-parallel path across GPUs is not built "
@@ -763,6 +768,12 @@ PMC_STALL = ("SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_WAIT_INST_LDS SQ_AC
 STALL_CMD = ("rocprofv3 --pmc {c} -d OUT/prof_stall -o run --output-format csv -- "
              "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --step-only{wl}")
 
+# the GEMMs' memory side (2 TCC, 2 TA, 4 TCP and 1 GRBM counters, one pass)
+PMC_MEM = ("TCC_HIT_sum TCC_MISS_sum TA_BUSY_avr TA_ADDR_STALLED_BY_TC_CYCLES_sum TCP_PENDING_STALL_CYCLES_sum "
+           "TCP_TCC_READ_REQ_sum TCP_TCC_READ_REQ_LATENCY_sum TCP_TOTAL_CACHE_ACCESSES_sum GRBM_GUI_ACTIVE")
+MEM_CMD = ("rocprofv3 --pmc {c} -d OUT/prof_mem -o run --output-format csv -- "
+           "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --step-only{wl}")
+
 
 def wl_arg(workload):
     """The --workload argument of a profiling command (none for the default workload)."""
@@ -933,6 +944,48 @@ def summarize_mfma(pmc_dir, workload, out_dir=None):
             md.append(f"| `{k}` | {lin.N}x{lin.K} | {v['ns'] / 1e3:.0f} | {util:.1f}% | {ghz:.2f} | "
                       f"{mops / alg:.3f} | {tf:.0f} | {frac:.3f} | {frac * 2.4 / ghz if ghz else 0:.3f} | {100 * lds:.1f}% |")
     out = os.path.join(out_dir or os.path.join(REPO, "profiles"), f"mfma_util_{workload}.md")
+    with open(out, "w") as f:
+        f.write("\n".join(md) + "\n")
+    print(out)
+
+
+def summarize_memory(pmc_dir, workload, out_dir=None):
+    """The GEMMs' memory side per launch: L2 hit rate, how busy the texture-address units are, how
+    long their address path waits on the L1 and the L1 on L2 data, and the L1->L2 read latency."""
+    import csv
+
+    from paper_2608_01847_amd import synth
+    w = synth.WORKLOADS[workload]
+    vals = {}
+    for r in csv.DictReader(open(os.path.join(pmc_dir, "run_counter_collection.csv"))):
+        d = vals.setdefault((int(r["Dispatch_Id"]), r["Kernel_Name"]), {})
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+        d["ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    cus = 256  # one texture-address unit (TA) and one L1 (TCP) per CU
+    md = [f"# Memory side of the reconstruction GEMMs ({workload}, {w.M:,} tokens)\n",
+          "Command (from the repository root on one MI355X; OUT is any output directory):\n",
+          "    " + MEM_CMD.format(c=PMC_MEM, wl=wl_arg(workload)) + "\n",
+          "Per launch (one linear layer; the first launches of each kernel, the default step's). `L2 hit` = TCC_HIT / "
+          "(TCC_HIT + TCC_MISS); `TA busy` = TA_BUSY_avr / GRBM_GUI_ACTIVE (share of GPU-busy cycles in which a "
+          "CU's texture-address unit works); `TA waits on L1` = TA_ADDR_STALLED_BY_TC_CYCLES_sum / (256 GRBM_GUI_ACTIVE); "
+          "`L1 waits on L2` = TCP_PENDING_STALL_CYCLES_sum / (256 GRBM_GUI_ACTIVE); `L1->L2 latency` = "
+          "TCP_TCC_READ_REQ_LATENCY_sum / TCP_TCC_READ_REQ_sum (cycles per read request); `L1 reads / KB` = L1->L2 "
+          "read requests per KB of the launch's algorithmic operand bytes (each operand read once), i.e. how often "
+          f"the tiles re-fetch operands from L2. Source hash of the kernels: `{kernel_source_hash()}`.\n",
+          "| Kernel | Layer (N x K) | us | L2 hit | TA busy | TA waits on L1 | L1 waits on L2 | L1->L2 latency | "
+          "L1 reads / KB |", "|---|---|---|---|---|---|---|---|---|"]
+    for k, pre in GEMM_KERNELS.items():
+        runs = [v for (disp, name), v in sorted(vals.items()) if name.startswith(pre)][:len(w.linears)]
+        for v, lin in zip(runs, w.linears):
+            gui = max(v.get("GRBM_GUI_ACTIVE", 0.0), 1.0)
+            hit, miss = v.get("TCC_HIT_sum", 0.0), v.get("TCC_MISS_sum", 0.0)
+            req = max(v.get("TCP_TCC_READ_REQ_sum", 0.0), 1.0)
+            op_bytes = algorithmic_bytes(k, w.M, lin.N, lin.K, w.sub_block, w.fmt)
+            md.append(f"| `{k}` | {lin.N}x{lin.K} | {v['ns'] / 1e3:.0f} | {hit / max(hit + miss, 1.0):.3f} | "
+                      f"{v.get('TA_BUSY_avr', 0.0) / gui:.3f} | {v.get('TA_ADDR_STALLED_BY_TC_CYCLES_sum', 0.0) / (cus * gui):.3f} | "
+                      f"{v.get('TCP_PENDING_STALL_CYCLES_sum', 0.0) / (cus * gui):.3f} | "
+                      f"{v.get('TCP_TCC_READ_REQ_LATENCY_sum', 0.0) / req:.0f} | {req / (op_bytes / 1024):.2f} |")
+    out = os.path.join(out_dir or os.path.join(REPO, "profiles"), f"gemm_memory_{workload}.md")
     with open(out, "w") as f:
         f.write("\n".join(md) + "\n")
     print(out)

@@ -179,3 +179,24 @@ def test_stall_summary_row(tmp_path):
     cells = [c.strip() for c in row.strip("|").split("|")]
     assert cells[2] == "500"
     assert cells[3:7] == ["17.0%", "34.3%", "0.0%", "12.5%"]
+
+
+def test_memory_summary_row(tmp_path):
+    from paper_2608_01847_amd import synth
+    w = synth.WORKLOADS["block2560_mxfp4"]
+    lin = w.linears[0]
+    gui = 1.0e6
+    op_kb = bench.algorithmic_bytes("bwd_mfma_mx_kernel", w.M, lin.N, lin.K, w.sub_block, w.fmt) / 1024
+    rows = [(40, BWD_MX, "TCC_HIT_sum", 900.0, 5.0e5), (40, BWD_MX, "TCC_MISS_sum", 100.0, 5.0e5),
+            (40, BWD_MX, "TA_BUSY_avr", 0.6 * gui, 5.0e5), (40, BWD_MX, "GRBM_GUI_ACTIVE", gui, 5.0e5),
+            (40, BWD_MX, "TA_ADDR_STALLED_BY_TC_CYCLES_sum", 0.1 * 256 * gui, 5.0e5),
+            (40, BWD_MX, "TCP_PENDING_STALL_CYCLES_sum", 0.2 * 256 * gui, 5.0e5),
+            (40, BWD_MX, "TCP_TCC_READ_REQ_sum", 2.0 * op_kb, 5.0e5),
+            (40, BWD_MX, "TCP_TCC_READ_REQ_LATENCY_sum", 2.0 * op_kb * 700, 5.0e5)]
+    write_counter_csv(tmp_path / "mem", rows)
+    bench.summarize_memory(str(tmp_path / "mem"), "block2560_mxfp4", out_dir=str(tmp_path))
+    text = (tmp_path / "gemm_memory_block2560_mxfp4.md").read_text()
+    row = next(l for l in text.splitlines() if l.startswith("| `bwd_mfma_mx_kernel`"))
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    assert cells[1] == f"{lin.N}x{lin.K}" and cells[2] == "500"
+    assert cells[3:9] == ["0.900", "0.600", "0.100", "0.200", "700", "2.00"]
