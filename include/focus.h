@@ -273,9 +273,10 @@ typedef struct {
 /* Weight fake quantisation (Sec. 3.2 Eq. 4, Sec. 3.3 Eq. 6-7, Sec. 3.4 Eq. 8) of up to
  * FOCUS_MAX_WEIGHT_LAYERS linear layers under one q, e.g. all the linears of the decoder block being
  * calibrated. Each layer's W_hat, codes and scale bytes are bit for bit those that focus_fakequant_fwd
- * in weight mode writes for it (with W_hat NULL: those of focus_export_packed, Fig. 3(d)); bf16
- * weights go out in one launch for the whole group, so small layers cost no launch and tail latency
- * of their own (fp32 weights: one launch per layer).
+ * in weight mode writes for it (with W_hat NULL: those of focus_export_packed, Fig. 3(d)), in
+ * q->code_layout and q->scale_layout; bf16 weights go out in one launch for the whole group, so small
+ * layers cost no launch and tail latency of their own (fp32 weights, or a group of more than 2^23
+ * 64 x 256 tiles: one launch per layer, same results).
  *   layers: HOST array of n_layers entries, read during the call (the tensors stay device memory
  *     owned by the caller); every layer is checked as focus_fakequant_fwd checks a weight-mode call
  *     (W_hat and codes both NULL is FOCUS_ERR_NULL), and one failed check launches nothing.
