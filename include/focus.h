@@ -171,7 +171,9 @@ focus_status focus_fakequant_bwd(const focus_qconfig *q, const float *G, int64_t
  *   Y_ref == NULL: plain GEMM, Y_hat is written to dY [M][N] (op_dtype).
  *   Y_ref != NULL ([M][N], op_dtype): D = Y_hat - Y_ref, dY = fl(2 D / (M N)) (op_dtype),
  *     *loss_out (device double) = sum(D^2) / (M N) and, if col_sq_opt != NULL, col_sq_opt[n]
- *     (device double [N]) = sum over tokens of D[t][n]^2. */
+ *     (device double [N]) = sum over tokens of D[t][n]^2.
+ *   With M == 0 or N == 0 nothing is launched and nothing is written: dY, *loss_out and col_sq_opt
+ *   keep their contents (a mean over no elements is undefined). */
 focus_status focus_recon_gemm_fwd(const void *X_hat, const void *W_hat, int op_dtype,
                                   int64_t M, int64_t N, int64_t K, const void *Y_ref, void *dY,
                                   double *loss_out, double *col_sq_opt,

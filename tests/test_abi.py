@@ -118,6 +118,17 @@ def test_argument_checks(L, cpu_only):
                                   None) == focus.ERR_NULL  # MSE mode needs loss_out
     assert L.focus_recon_gemm_fwd(BOGUS, BOGUS, 3, 8, 8, 32, None, BOGUS, None, None, BOGUS, 1 << 30,
                                   None) == focus.ERR_DTYPE
+    # no tokens or no output features: nothing is launched and nothing is written (the loss, a mean over
+    # no elements, keeps whatever the caller's buffer held); the workspace is still checked
+    loss = ctypes.c_double(-7.0)
+    for M, N in ((0, 8), (8, 0)):
+        assert L.focus_recon_gemm_fwd(BOGUS, BOGUS, 1, M, N, 32, BOGUS, BOGUS, ctypes.byref(loss), None, BOGUS,
+                                      1 << 30, None) == focus.OK
+        assert L.focus_recon_gemm_fwd_mxfp4(BOGUS, BOGUS, BOGUS, BOGUS, M, N, 128, BOGUS, BOGUS, ctypes.byref(loss),
+                                            None, BOGUS, 1 << 30, None) == focus.OK
+    assert loss.value == -7.0
+    assert L.focus_recon_gemm_fwd(BOGUS, BOGUS, 1, 0, 8, 32, BOGUS, BOGUS, ctypes.byref(loss), None, BOGUS, 8,
+                                  None) == focus.ERR_WORKSPACE
     # forward GEMM from packed MXFP4 operands
     mxf = L.focus_recon_gemm_fwd_mxfp4
     assert mxf(BOGUS, BOGUS, BOGUS, BOGUS, 8, 8, 64, None, BOGUS, None, None, BOGUS, 1 << 30,
