@@ -121,7 +121,8 @@ size_t focus_workspace_size(int call, const focus_qconfig *q, int64_t M, int64_t
  *   MXFP4: s_fp[n][i] = fl32(max_{block i}|w| / 6)              ([N][K/32] fp32)
  *   NVFP4: alpha = fl32(max|W| / 2688) (1 if W is all zero), written to *alpha_out (device fp32);
  *          s_fp[n][i] = Delta_fp = fl32(max_{block i}|w| / fl32(alpha * 6))   ([N][K/16] fp32)
- *   c [N][K/sub_block] fp32 is set to 1 (Sec. 3.3, Sec. 3.4). alpha_out may be NULL for MXFP4. */
+ *   c [N][K/sub_block] fp32 is set to 1 (Sec. 3.3, Sec. 3.4). alpha_out may be NULL for MXFP4.
+ *   With N == 0 or K == 0 nothing is launched and nothing is written (*alpha_out included). */
 focus_status focus_scales_init(const focus_qconfig *q, const void *W, int w_dtype, int64_t N, int64_t K,
                                float *s_fp, float *c, float *alpha_out,
                                void *ws, size_t ws_bytes, focus_stream stream);
@@ -320,7 +321,8 @@ focus_status focus_fakequant_act_bwd(const focus_qconfig *q, const void *X, int 
  *   p_t = softmax(Z_teacher[row, I]),  p_s = softmax(Z_student[row, I])
  *   loss = (1/T) sum_rows sum_{i in I} p_t[i] (log p_t[i] - log p_s[i])      -> *loss_out (device fp64)
  *   dZ_student[row, i] = (p_s[i] - p_t[i]) / T for i in I, 0 elsewhere       (dtype, written in full)
- * dtype FOCUS_BF16 or FOCUS_F32 for all three arrays (element-aligned). k >= 1, 1 <= V <= 2^31.
+ * dtype FOCUS_BF16 or FOCUS_F32 for all three arrays (element-aligned). k >= 1 (else FOCUS_ERR_CONFIG);
+ * T >= 1 and 1 <= V <= 2^31 (else FOCUS_ERR_SHAPE).
  * The logits must be finite: a NaN or infinity raises the domain flag (results unspecified). ws:
  * focus_workspace_size(FOCUS_CALL_KL_TOP, NULL, T, V, 0) bytes. Deterministic (fixed-order sums). */
 focus_status focus_kl_top(const void *Z_student, const void *Z_teacher, int dtype, int64_t T, int64_t V, int32_t k,

@@ -202,6 +202,15 @@ def test_argument_checks(L, cpu_only):
     assert adam(good, ws_bytes=8) == focus.ERR_WORKSPACE
     assert focus.workspace_size(focus.CALL_ADAMW, focus.qconfig(focus.MXFP4, 8)) == 256
     assert L.focus_check_flags(None, None) == focus.ERR_WORKSPACE
+    # KL-Top: k >= 1, at least one token row and 1 <= V <= 2^31
+    def kl(T=4, V=64, k=8, ptr=BOGUS):
+        return L.focus_kl_top(ptr, BOGUS, 1, T, V, k, BOGUS, BOGUS, BOGUS, 1 << 30, None)
+    assert kl(k=0) == focus.ERR_CONFIG
+    assert kl(T=0) == focus.ERR_SHAPE
+    assert kl(V=0) == focus.ERR_SHAPE
+    assert kl(V=(1 << 31) + 1, T=1) == focus.ERR_SHAPE
+    assert kl(ptr=None) == focus.ERR_NULL
+    assert kl(ptr=ctypes.c_void_p((1 << 20) + 1)) == focus.ERR_SHAPE  # not element-aligned (bf16)
 
 
 def test_grouped_weight_argument_checks(L, cpu_only):
