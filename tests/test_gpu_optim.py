@@ -4,6 +4,8 @@ rate) against the CPU oracle.
   * focus_adamw_step on ragged lengths (1 to 2^20 + 3 elements), linear and log2 domain, with and
     without weight decay, five chained steps from the same inputs: parameter and both moments
     within 1e-5 (fp32 arithmetic against float64);
+  * the benchmark's largest optimizer tensor (29.4 M coefficients), sampled elements after three
+    chained steps on the whole tensor, within 1e-5;
   * the log2 domain's guard: non-positive or non-finite parameters raise the domain flag and stay
     unchanged, the rest are updated;
   * the calibration step of calib.BlockCalibrator, teacher-forced: at each of three steps the GPU
@@ -66,6 +68,33 @@ def test_adamw_kernel(F, OO, n, log2, wd):
         assert_close(host_f32(p), po, TOL, f"param t={t}")
         assert_close(host_f32(m), mo, TOL, f"exp_avg t={t}")
         assert_close(host_f32(v), vo, TOL, f"exp_avg_sq t={t}")
+    assert F.check_flags(ws) == F.OK
+
+
+def test_adamw_fullsize_sampled(F, OO):
+    """The largest tensor the benchmark steps: the coefficients of the hidden-8192 block's gate_proj
+    (28,672 x 1,024 = 29.4 M, sub-blocks of 8) in the log2 domain at the paper's MXFP4 rate, three
+    chained steps on the whole tensor; parameter and moments of sampled elements (the first, the last
+    and 4,096 seeded ones) within 1e-5 of the oracle's element-wise steps."""
+    n = 28672 * (8192 // 8)
+    announce(f"adamw full size n={n} log2")
+    rng = np.random.default_rng(17)
+    idx = np.unique(np.concatenate([[0, n - 1], rng.choice(n, 4096, replace=False)])).astype(np.int64)
+    di = torch.from_numpy(idx).cuda()
+    g = torch.Generator(device="cuda").manual_seed(19)
+    p = torch.exp2(torch.randn(n, generator=g, device="cuda") * 0.1)  # coefficients near 1
+    m, v = torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda")
+    lr = f32(5e-2)
+    ws = F.workspace(256)
+    po, mo, vo = host_f32(p.index_select(0, di)).astype(np.float64), np.zeros(len(idx)), np.zeros(len(idx))
+    for t in range(1, 4):
+        grad = torch.randn(n, generator=g, device="cuda") * 1e-4
+        F.adamw_step(p, grad, m, v, t, lr, log2_domain=True, ws=ws)
+        po, mo, vo = OO.adamw(po, host_f32(grad.index_select(0, di)), mo, vo, t, lr, B1, B2, EPS, log2_domain=True)
+        torch.cuda.synchronize()
+        assert_close(host_f32(p.index_select(0, di)), po, TOL, f"param t={t}")
+        assert_close(host_f32(m.index_select(0, di)), mo, TOL, f"exp_avg t={t}")
+        assert_close(host_f32(v.index_select(0, di)), vo, TOL, f"exp_avg_sq t={t}")
     assert F.check_flags(ws) == F.OK
 
 
