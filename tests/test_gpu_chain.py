@@ -7,7 +7,8 @@ straight-through backward of the activation fake quantisation and the KL-Top los
     floor rule and NVFP4: clipped elements), bf16 and fp32;
   * focus_kl_top: loss within 1e-5, dZ within 1e-5 (fp32) / 2e-2 (bf16 output), zero exactly off the
     teacher's top-k set, for k = 1000 of ragged vocabularies, k = 1, k >= V, bf16 logits with many
-    ties (index-order tie rule), deterministic from run to run;
+    ties (index-order tie rule), deterministic from run to run; rows long enough for the
+    sample-select path, with ties at the threshold, and rows whose gathered lists overflow;
   * the top layer of a stack trained on KL-Top: loss, grad_s, grad_c and dX through KL-Top, the
     fused backward driven by dZ, dX_hat and the activation backward (fp32 1e-5; bf16 2e-2);
   * one epoch of the synthetic two-linear stack trained end to end on KL-Top lowers the held-out
@@ -81,6 +82,12 @@ def test_activation_backward_bitexact(F, C, fmt, floor, dt):
 
 
 def logits(rng, T, V, ties=False):
+    if ties == "equal":  # every logit equal: the gathered lists overflow and the passes decide
+        return np.full((T, V), 1.5)
+    if ties == "spikes":  # the largest logits only where the sample does not look (every 32nd from 1)
+        z = rng.normal(size=(T, V))
+        z[:, 1::32] += 50.0
+        return z
     if ties:  # multiples of 1/4 in about [-12, 12]: exact in bf16, and many equal values per row
         return np.round(rng.normal(size=(T, V)) * 12.0) / 4.0
     return rng.normal(size=(T, V)) * 3.0
@@ -89,7 +96,13 @@ def logits(rng, T, V, ties=False):
 @pytest.mark.parametrize("T,V,k,dt,ties", [(64, 1007, 1000, torch.float32, False), (32, 32000, 1000, torch.float32, False),
                                            (32, 32000, 1000, torch.bfloat16, False), (48, 5000, 1000, torch.bfloat16, True),
                                            (16, 700, 1, torch.float32, False), (16, 700, 900, torch.bfloat16, False),
-                                           (8, 4099, 4099, torch.float32, False)])
+                                           (8, 4099, 4099, torch.float32, False),
+                                           # rows of 32,768 or more take the sample-select path: plain,
+                                           # hundreds of ties at the threshold (the index-order cut), k = 1,
+                                           # and two rows whose gathered lists overflow (the passes decide)
+                                           (6, 40000, 1000, torch.float32, False), (4, 65536, 1000, torch.bfloat16, True),
+                                           (4, 65536, 1, torch.bfloat16, False), (3, 65536, 1000, torch.bfloat16, "equal"),
+                                           (3, 98304, 1000, torch.float32, "spikes")])
 def test_kl_top(F, C, T, V, k, dt, ties):
     announce(f"kl_top T={T} V={V} k={k} dt={dt} ties={ties}")
     rng = np.random.default_rng(T * 7 + V + k)
@@ -103,7 +116,7 @@ def test_kl_top(F, C, T, V, k, dt, ties):
     assert_close(host_f32(dZ), dZo, 1e-5 if dt == torch.float32 else 2e-2, "dZ")
     got_set = host_f32(dZ) != 0
     assert not np.any(got_set & (dZo == 0)), "dZ nonzero off the teacher's top-k set"
-    if ties:
+    if ties is True:
         assert (np.diff(np.sort(host_f32(Zt), axis=1), axis=1) == 0).sum() > T * 100  # ties are present
     assert loss.item() == loss2.item() and torch.equal(dZ, dZ2)
 
