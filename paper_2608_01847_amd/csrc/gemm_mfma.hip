@@ -244,6 +244,14 @@ __device__ __forceinline__ void tr_wait(Frags &f) {
                    "+v"(f.b[2]), "+v"(f.b[3]));
 }
 
+// The same for a set whose 16 reads were followed by other LDS operations: a wave's LDS operations
+// complete in order, so once at most 15 are in flight the set has landed.
+__device__ __forceinline__ void tr_wait15(Frags &f) {
+    asm volatile("s_waitcnt lgkmcnt(15)"
+                 : "+v"(f.a[0]), "+v"(f.a[1]), "+v"(f.a[2]), "+v"(f.a[3]), "+v"(f.b[0]), "+v"(f.b[1]),
+                   "+v"(f.b[2]), "+v"(f.b[3]));
+}
+
 // Workgroups are dealt to the 8 XCDs round-robin (id % 8), each XCD with its own L2. Renumbering
 // so that XCD x runs a contiguous block of tiles keeps tiles that share operand panels in one L2.
 __device__ __forceinline__ uint32_t xcd_tile(uint32_t id, uint32_t count) {
@@ -433,58 +441,99 @@ fwd_mfma_kernel(const void *__restrict__ X, const void *__restrict__ W, const ui
     // Before the barrier of step kt, this thread's loads of slots up to kt + 1 have landed (only
     // slots kt + 2 .. kt + S - 2 may still be in flight); after it, everyone's have, so the first
     // fragments of step kt + 1 can be read while step kt's MFMAs run, and stage (kt - 1) % S,
-    // last read in step kt - 1, can be refilled with slot kt + S - 1. A bare s_barrier:
+    // whose fragments every wave read during step kt - 2 and used in step kt - 1, can be refilled
+    // with slot kt + S - 1. A bare s_barrier:
     // __syncthreads would also wait for the loads still in flight.
     FOCUS_WAIT_VMCNT(kLoads * (S - 3));
     asm volatile("s_barrier" ::: "memory");
-    Frags f, g;
+    // Fragments are read a whole step ahead, in three sets: step kt's two halves use sets X and Y,
+    // both read during step kt - 1; after the barrier the free set Z takes step kt + 1's first half
+    // (and MX its scales), and X, once its MFMAs are issued, step kt + 1's second half. Read half a
+    // step ahead (two sets), the MFMAs waited for their fragments: three sets are 2-6% faster on the
+    // hidden-8192 layers, bit-identical. The sets rotate with a period of three steps.
+    Frags f, g, h;
     uint32_t sa[4], sb[4], na[4], nb[4];
     load_frags_fwd(f, smem, smem + kFwdOpBytes, 0, wm, wn, lane);
+    load_frags_fwd(g, smem, smem + kFwdOpBytes, 1, wm, wn, lane);
     if constexpr (MX) load_scales(smem, na, nb);
     // One step (sc = kt % S). The loads of slot kt + S - 1 go out spread over the step's 32 MFMAs:
     // one after every fourth (operand loads 0-3 in the first half, 4-7 in the second; MX's scale
     // loads after the fourth MFMA of each half). Issued closer together they fill the texture
     // unit's queue, and a wave stalled on a full queue issues no MFMA (loads after every second
     // MFMA of the first half only: 4-7% slower). The scheduling barriers keep the compiler from
-    // regrouping them. Stage (kt - 1) % S, which they fill, was last read in step kt - 1.
+    // regrouping them. Stage (kt - 1) % S, which they fill, was last read in step kt - 2.
     auto issue_at = [&](lds_char *st, int64_t kt, int li, auto y_slot) {
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (decltype(y_slot)::value) issue_y(st, kt + S - 1, li);
         else issue_op(st, kt + S - 1, li);
         __builtin_amdgcn_sched_barrier(0);
     };
-    auto step = [&](int64_t kt, int sc, auto y_slot) {
+    auto step = [&](int64_t kt, int sc, auto y_slot, Frags &X, Frags &Y, Frags &Z) {
         FOCUS_WAIT_VMCNT(kLoads * (S - 3));
         asm volatile("s_barrier" ::: "memory");
         const int sn = sc == S - 1 ? 0 : sc + 1, sl = sc == 0 ? S - 1 : sc - 1;
-        const char *As = smem + sc * kStage, *Bs = As + kFwdOpBytes;
         const char *An = smem + sn * kStage, *Bn = An + kFwdOpBytes;
         lds_char *st = stage(sl);
         if constexpr (MX) {
 #pragma unroll
             for (int i = 0; i < 4; i++) sa[i] = na[i], sb[i] = nb[i];
         }
-        load_frags_fwd(g, As, Bs, 1, wm, wn, lane);
-        static_for<16>([&](auto idx) {
-            constexpr int i = idx / 4, jj = idx % 4;
-            mfma(std::integral_constant<int, i>{}, std::integral_constant<int, jj>{}, f, sa, sb, std::integral_constant<int, 0>{});
-            if constexpr (idx % 4 == 1) issue_at(st, kt, idx / 4, y_slot);
-            if constexpr (MX && idx == 3) issue_at(st, kt, 8, y_slot);
-        });
-        load_frags_fwd(f, An, Bn, 0, wm, wn, lane);
+        load_frags_fwd(Z, An, Bn, 0, wm, wn, lane);
         if constexpr (MX) load_scales(An, na, nb);
         static_for<16>([&](auto idx) {
             constexpr int i = idx / 4, jj = idx % 4;
-            mfma(std::integral_constant<int, i>{}, std::integral_constant<int, jj>{}, g, sa, sb, std::integral_constant<int, 1>{});
+            mfma(std::integral_constant<int, i>{}, std::integral_constant<int, jj>{}, X, sa, sb, std::integral_constant<int, 0>{});
+            if constexpr (idx % 4 == 1) issue_at(st, kt, idx / 4, y_slot);
+            if constexpr (MX && idx == 3) issue_at(st, kt, 8, y_slot);
+        });
+        load_frags_fwd(X, An, Bn, 1, wm, wn, lane);
+        static_for<16>([&](auto idx) {
+            constexpr int i = idx / 4, jj = idx % 4;
+            mfma(std::integral_constant<int, i>{}, std::integral_constant<int, jj>{}, Y, sa, sb, std::integral_constant<int, 1>{});
             if constexpr (idx % 4 == 1) issue_at(st, kt, 4 + idx / 4, y_slot);
             if constexpr (MX && idx == 3) issue_at(st, kt, 9, y_slot);
         });
     };
+    auto nxt = [](int sc) { return sc == S - 1 ? 0 : sc + 1; };
     const int64_t n_op = nk > S - 1 ? nk - (S - 1) : 0;  // steps whose slot kt + S - 1 is an operand step
     int64_t kt = 0;
     int sc = 0;
-    for (; kt < n_op; kt++, sc = sc == S - 1 ? 0 : sc + 1) step(kt, sc, std::false_type{});
-    for (; kt < nk; kt++, sc = sc == S - 1 ? 0 : sc + 1) step(kt, sc, std::true_type{});
+    for (; kt + 3 <= n_op; kt += 3) {
+        step(kt, sc, std::false_type{}, f, g, h);
+        sc = nxt(sc);
+        step(kt + 1, sc, std::false_type{}, h, f, g);
+        sc = nxt(sc);
+        step(kt + 2, sc, std::false_type{}, g, h, f);
+        sc = nxt(sc);
+    }
+    // the last operand steps, then the sets renamed once so that the Y_ref steps (at most S - 1)
+    // start from the loop's rotation and run as straight-line code (a rotation chosen at run time
+    // in each of them made the compiler spill)
+    if (kt < n_op) {
+        step(kt, sc, std::false_type{}, f, g, h);
+        sc = nxt(sc);
+        kt++;
+    }
+    if (kt < n_op) {
+        step(kt, sc, std::false_type{}, h, f, g);
+        sc = nxt(sc);
+        kt++;
+        Frags t = f;  // (g, h, f) becomes (f, g, h)
+        f = g, g = h, h = t;
+    } else if (n_op % 3 == 1) {
+        Frags t = f;  // (h, f, g) becomes (f, g, h)
+        f = h, h = g, g = t;
+    }
+    static_for<S - 1>([&](auto r) {
+        if (kt < nk) {
+            constexpr int q = decltype(r)::value % 3;
+            if constexpr (q == 0) step(kt, sc, std::true_type{}, f, g, h);
+            else if constexpr (q == 1) step(kt, sc, std::true_type{}, h, f, g);
+            else step(kt, sc, std::true_type{}, g, h, f);
+            sc = nxt(sc);
+            kt++;
+        }
+    });
     // quarters not yet issued (S == 4: the last one) go into stages whose steps every wave is done with
     if constexpr (S < 5) {
         asm volatile("s_barrier" ::: "memory");
@@ -811,22 +860,27 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
     const uint32_t lds0 = lds_addr(smem);
     FOCUS_WAIT_VMCNT(8);
     asm volatile("s_barrier" ::: "memory");
-    Frags f, g;
+    // Fragments are read a whole step ahead in three rotating sets, as in bwd_mfma_mx_kernel: step
+    // kt multiplies sets P and Q, filled during step kt - 1, and refills R and then P with step
+    // kt + 1's halves.
+    Frags f, g, h;
     load_frags_tr<0>(f, lds0, a_off, b_off);
-    for (int64_t kt = 0; kt < nk; kt++) {
-        FOCUS_WAIT_VMCNT(8);
-        asm volatile("s_barrier" ::: "memory");
-        const uint32_t cur = lds0 + (uint32_t)(kt & 3) * kBwdStageBytes;
+    load_frags_tr<1>(g, lds0, a_off, b_off);
+    auto step = [&](int64_t kt, Frags &P, Frags &Q, Frags &R) {
         const uint32_t nxt = lds0 + (uint32_t)((kt + 1) & 3) * kBwdStageBytes;
         const int64_t t0 = t_begin + (kt + 3) * kBwdStep;
         const __amdgpu_buffer_rsrc_t ra = BwdDma::step_rsrc(X, K, t0, t_end), rb = BwdDma::step_rsrc(dY, N, t0, t_end);
         lds_char *st = lsm + (int)((kt + 3) & 3) * kBwdStageBytes;
-        tr_wait(f);  // f (read during the previous step's second half) has landed
-        load_frags_tr<1>(g, cur, a_off, b_off);
+        // slot kt + 1 and this thread's reads of P have landed (only reads of Q may be in flight);
+        // after the barrier everyone's have, and stage (kt - 1) % 4 is free for slot kt + 3
+        FOCUS_WAIT_VMCNT(8);
+        tr_wait15(P);
+        asm volatile("s_barrier" ::: "memory");
+        load_frags_tr<0>(R, nxt, a_off, b_off);
         // the 8 loads of slot kt + 3 go out one after every second MFMA (see the forward kernel)
         static_for<16>([&](auto idx) {
             constexpr int i = idx / 4, jj = idx % 4;
-            acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[jj], acc[i][jj], 0, 0, 0);
+            acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(P.a[i], P.b[jj], acc[i][jj], 0, 0, 0);
             if constexpr (idx % 2 == 1) {
                 __builtin_amdgcn_sched_barrier(0);
                 if constexpr (idx / 2 < 4) pa.issue_one(ra, st, wave_u, idx / 2);
@@ -834,10 +888,18 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
                 __builtin_amdgcn_sched_barrier(0);
             }
         });
-        tr_wait(g);  // read before the first half's MFMAs, long landed
-        load_frags_tr<0>(f, nxt, a_off, b_off);
-        mma_frags(g, acc);
+        tr_wait15(Q);  // read during step kt - 1
+        load_frags_tr<1>(P, nxt, a_off, b_off);
+        mma_frags(Q, acc);
+    };
+    int64_t kt = 0;
+    for (; kt + 3 <= nk; kt += 3) {
+        step(kt, f, g, h);
+        step(kt + 1, h, f, g);
+        step(kt + 2, g, h, f);
     }
+    if (kt < nk) step(kt, f, g, h);
+    if (kt + 1 < nk) step(kt + 1, h, f, g);
     tr_wait(f);  // no read may still be in flight when the workgroup ends
     // the empty slots' zero writes must land before the workgroup's LDS is handed on
     FOCUS_WAIT_VMCNT(0);
@@ -857,8 +919,8 @@ bwd_mfma_kernel(const uint16_t *__restrict__ dY, const uint16_t *__restrict__ X,
 // wave so that every thread issues the same number of loads). Two steps after a slot's loads are
 // issued, each thread converts one token's 32 codes of one block (16 bytes, one scale) into 32 bf16
 // with the scaled FP4 conversion and writes them into one of three bf16 A stages, in the layout the
-// transposing fragment reads expect. Step kt issues slot kt + 4, converts slot kt + 2 and multiplies
-// step kt: 5 DMA stages + 3 A stages = 153 KB of LDS.
+// transposing fragment reads expect. Step kt issues slot kt + 4, converts slot kt + 2, reads the
+// fragments of step kt + 1 and multiplies step kt: 5 DMA stages + 3 A stages = 153 KB of LDS.
 constexpr int kMxDmaStages = 5;
 constexpr int kMxCodeOff = kBwdOpBytes;            // codes after the dY tile
 constexpr int kMxScaleOff = kMxCodeOff + 32 * 128; // then 4 per-wave copies of the scale bytes
@@ -1065,28 +1127,36 @@ bwd_mfma_mx_kernel(const uint16_t *__restrict__ dY, const uint8_t *__restrict__ 
     auto next_a = [](uint32_t o) {
         return o == kMxAOff + (kMxAStages - 1) * kBwdOpBytes ? (uint32_t)kMxAOff : o + kBwdOpBytes;
     };
-    int64_t t_is = t_begin + 4 * kBwdStep;  // first token of slot kt + 4
-    Frags f, g;
+    // Fragments are read a whole step ahead, in three sets: step kt's two k16 halves use sets X and
+    // Y, both filled during step kt - 1; after the barrier the free set Z takes step kt + 1's first
+    // half, and X, once its MFMAs are issued, step kt + 1's second half. Read only half a step ahead
+    // (two sets), the waits for the fragments stalled the matrix units: three sets are 5-7% faster
+    // on the hidden-8192 layers, bit-identical. The sets rotate with a period of three steps, so the
+    // loop is unrolled three times.
+    Frags f, g, h;
     frags(std::integral_constant<int, 0>{}, f, a_addr(0), d_addr(0));
-    for (int64_t kt = 0; kt < nk; kt++, t_is += kBwdStep) {
-        const MxSlot sl = slot_at(t_is);
+    frags(std::integral_constant<int, 1>{}, g, a_addr(0), d_addr(0));
+    auto step = [&](int64_t kt, Frags &X, Frags &Y, Frags &Z) {
+        const MxSlot sl = slot_at(t_begin + (kt + 4) * kBwdStep);
         lds_char *st = lsm + o_is;
         const uint32_t cds = lds0 + o_cv, cas = lds0 + a_cv;
+        const uint32_t a_nx = lds0 + next_a(a_cur), o_nx = lds0 + next_d(o_cur);
         // this thread's codes and scale bytes of slot kt + 2 and all of slot kt + 1 have landed (slot
-        // kt + 3 and the dY loads of slot kt + 2 may be in flight); after the barrier everyone's
-        // have, and every wave is done with step kt - 1's stages
+        // kt + 3 and the dY loads of slot kt + 2 may be in flight), and so have its reads of X and
+        // its conversion writes of step kt - 1 (only reads of Y may be in flight); after the barrier
+        // everyone's have, and every wave is done with step kt - 1's stages
         FOCUS_WAIT_VMCNT(kMxLoads + 4);
+        tr_wait15(X);
         asm volatile("s_barrier" ::: "memory");
-        tr_wait(f);
-        // the conversion's two reads go first, then the 16 fragment reads of the second half: LDS
-        // operations complete in order, so lgkmcnt(15) means the first two have
+        // the conversion's two reads go first, then the 16 fragment reads of step kt + 1's first
+        // half: lgkmcnt(15) then means that the first two have landed
         u32x4_t w = ds_read_b128<0>(cds + cv_code);
         uint32_t sb = ds_read_u8<0>(cds + cv_scale);
-        frags(std::integral_constant<int, 1>{}, g, lds0 + a_cur, lds0 + o_cur);
+        frags(std::integral_constant<int, 0>{}, Z, a_nx, o_nx);
         float sc = 0.0f;
         static_for<16>([&](auto idx) {
             constexpr int i = idx / 4, jj = idx % 4;
-            acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[jj], acc[i][jj], 0, 0, 0);
+            acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(X.a[i], X.b[jj], acc[i][jj], 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
             // slot kt + 4: one load after every second MFMA; the conversion of slot kt + 2 after
             // MFMAs 4, 6, 8, 10 (one 16-byte chunk each), starting with the wait for its reads
@@ -1101,12 +1171,20 @@ bwd_mfma_mx_kernel(const uint16_t *__restrict__ dY, const uint8_t *__restrict__ 
             }
             __builtin_amdgcn_sched_barrier(0);
         });
+        tr_wait15(Y);  // read during step kt - 1
+        frags(std::integral_constant<int, 1>{}, X, a_nx, o_nx);
+        mma_frags(Y, acc);
         o_cur = next_d(o_cur), o_cv = next_d(o_cv), o_is = next_d(o_is);
         a_cur = next_a(a_cur), a_cv = next_a(a_cv);
-        tr_wait(g);  // also covers the conversion's writes, before the barrier that publishes them
-        frags(std::integral_constant<int, 0>{}, f, lds0 + a_cur, lds0 + o_cur);  // step kt + 1's stages
-        mma_frags(g, acc);
+    };
+    int64_t kt = 0;
+    for (; kt + 3 <= nk; kt += 3) {
+        step(kt, f, g, h);
+        step(kt + 1, h, f, g);
+        step(kt + 2, g, h, f);
     }
+    if (kt < nk) step(kt, f, g, h);
+    if (kt + 1 < nk) step(kt + 1, h, f, g);
     tr_wait(f);  // no read may still be in flight when the workgroup ends
     FOCUS_WAIT_VMCNT(0);
     ste_epilogue<kFmtMX, WDT>(acc, k0, n0, split, N, K, W, s_fp, c, sb_log2, nullptr, ste_clip, e8m0_floor, part_s,
