@@ -95,13 +95,15 @@ __device__ __forceinline__ uint32_t block_scan(uint32_t v, uint32_t *buf) {
 // largest logits, ties at the k-th value in index order) and the same per-element formulas; the sums
 // run in a fixed order in each, so every result is deterministic.
 //  * Sample-select, when the k largest are a small part of a long row: the r-th largest of 3,072
-//    evenly spaced teacher keys, r with a binomial margin of 3 standard deviations over the expected
-//    count, lies below the k-th largest key almost always (10 rows of 8,192 miss at k = 1,000 of
-//    151,936). One pass over both rows writes a zero dZ for every element and gathers those at or
+//    teacher keys, r with a binomial margin of 3 standard deviations over the expected count, lies
+//    below the k-th largest key almost always (10 rows of 8,192 miss at k = 1,000 of 151,936 on
+//    independent logits). The sample is 384 evenly spaced runs of 8 adjacent keys: keys spaced
+//    singly touched nearly every memory line of the row, an extra read of it (2.9 -> 2.3 ms). A
+//    sample that misleads (logits correlated along the row) costs time only, never a result. One pass over both rows writes a zero dZ for every element and gathers those at or
 //    above that key (about 1.8 k) into per-wave LDS lists in index order; the k-th largest key, the
 //    tie cut (up to kTieMax ties at it), the softmax statistics and the KL terms then come from LDS,
 //    and the gathered elements get their final dZ. Two reads of each row instead of seven: 8,192 x
-//    151,936 bf16 logits 7.3 -> 2.9 ms.
+//    151,936 bf16 logits 7.3 -> 2.3 ms.
 //  * The passes below whenever the gathered set misses the k-th largest key, overflows the lists or
 //    holds too many ties, or the row is short or k large: a radix select of the k-th largest teacher key (8-bit digits from
 //    the top, LDS histograms); if fewer ties at that key are admitted than exist, the index of the
@@ -229,11 +231,12 @@ kl_top_kernel(const void *__restrict__ Zs, const void *__restrict__ Zt, int64_t 
     const double kexp = (double)k * kSample / (double)V;  // expected sampled keys at or above the k-th
     const int r = (int)ceil(kexp) + (int)ceil(3.0 * sqrt(kexp)) + 2;
     if (!all && V >= kSampleMinV && r <= kSample / 4 && (double)r * (double)V / kSample <= 0.65 * kCand) {
-        // ---- the sample: keys of elements floor(j V / kSample), its r-th largest the gather bound ----
+        // ---- the sample: 8 adjacent keys from each of kSample / 8 evenly spaced elements (rows of at
+        // least kSampleMinV keep the runs apart), its r-th largest the gather bound ----
         uint32_t sk[kSample / 256];
 #pragma unroll
         for (int u = 0; u < kSample / 256; u++)
-            sk[u] = logit_key<IN>(load_logit<IN>(zt, (int64_t)(t + 256 * u) * V / kSample));
+            sk[u] = logit_key<IN>(load_logit<IN>(zt, (int64_t)((t + 256 * u) >> 3) * V / (kSample / 8) + ((t + 256 * u) & 7)));
 #pragma unroll
         for (int u = 0; u < kSample / 256; u++) cand_a[t + 256 * u] = sk[u];
         __syncthreads();

@@ -84,9 +84,9 @@ def test_activation_backward_bitexact(F, C, fmt, floor, dt):
 def logits(rng, T, V, ties=False):
     if ties == "equal":  # every logit equal: the gathered lists overflow and the passes decide
         return np.full((T, V), 1.5)
-    if ties == "spikes":  # the largest logits only where the sample does not look (every 32nd from 1)
-        z = rng.normal(size=(T, V))
-        z[:, 1::32] += 50.0
+    if ties == "spikes":  # the largest logits only where the sample does not look: every 32nd from 16
+        z = rng.normal(size=(T, V))  # (at 98,304 logits the sampled runs are elements 256 j .. 256 j + 7)
+        z[:, 16::32] += 50.0
         return z
     if ties:  # multiples of 1/4 in about [-12, 12]: exact in bf16, and many equal values per row
         return np.round(rng.normal(size=(T, V)) * 12.0) / 4.0
