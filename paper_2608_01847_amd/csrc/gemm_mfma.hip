@@ -7,6 +7,8 @@
 //   forward : 32 of K per step (128 for packed MXFP4 operands) in 5 (4) stages;
 //   backward: 32 tokens per step in 4 stages; with packed MXFP4 X_hat, 5 stages of dY, codes and
 //             scale bytes, whose codes are converted to bf16 into 3 further stages.
+// The fragments of each half-step (16 of the reduction) are read from LDS one whole step before
+// their MFMAs, into one of three register sets that rotate over a three-step unrolled loop.
 //
 // MFMA operand layout (32x32x16): lane l holds 8 consecutive reduction values of row l % 32 of A
 // (resp. column l % 32 of B), starting at reduction index 8 (l / 32). Accumulator register r of
