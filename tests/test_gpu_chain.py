@@ -97,9 +97,11 @@ def logits(rng, T, V, ties=False):
                                            (32, 32000, 1000, torch.bfloat16, False), (48, 5000, 1000, torch.bfloat16, True),
                                            (16, 700, 1, torch.float32, False), (16, 700, 900, torch.bfloat16, False),
                                            (8, 4099, 4099, torch.float32, False),
-                                           # rows of 32,768 or more take the sample-select path: plain,
-                                           # hundreds of ties at the threshold (the index-order cut), k = 1,
-                                           # and two rows whose gathered lists overflow (the passes decide)
+                                           # rows of 32,768 or more take the sample-select path: plain (at
+                                           # the shortest such row the sampled runs of 8 lie closest), hundreds
+                                           # of ties at the threshold (the index-order cut), k = 1, and two rows
+                                           # whose gathered lists overflow (the passes decide)
+                                           (5, 32768, 1000, torch.bfloat16, False),
                                            (6, 40000, 1000, torch.float32, False), (4, 65536, 1000, torch.bfloat16, True),
                                            (4, 65536, 1, torch.bfloat16, False), (3, 65536, 1000, torch.bfloat16, "equal"),
                                            (3, 98304, 1000, torch.float32, "spikes")])
