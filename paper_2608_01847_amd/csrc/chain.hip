@@ -59,6 +59,13 @@ __device__ __forceinline__ void store_logit(void *p, int64_t i, float v) {
     else reinterpret_cast<float *>(p)[i] = v;
 }
 
+// the same with the non-temporal cache policy (dZ is written once and not read back here)
+template <int IN>
+__device__ __forceinline__ void store_logit_nt(void *p, int64_t i, float v) {
+    if (IN == kBF16) __builtin_nontemporal_store((uint16_t)f32_to_bf16_bits(v), reinterpret_cast<uint16_t *>(p) + i);
+    else __builtin_nontemporal_store(v, reinterpret_cast<float *>(p) + i);
+}
+
 // Logits of elements base + t + 256 u (u = 0 .. kTrips - 1) of a row: a thread's next kTrips elements
 // in its usual order, loaded before any is used so that kTrips loads are in flight at once (the passes
 // are bound by the latency of rows that no longer fit the caches: 16 in flight took the 8192 x 151936
@@ -102,8 +109,9 @@ __device__ __forceinline__ uint32_t block_scan(uint32_t v, uint32_t *buf) {
 //    sample that misleads (logits correlated along the row) costs time only, never a result. One pass over both rows writes a zero dZ for every element and gathers those at or
 //    above that key (about 1.8 k) into per-wave LDS lists in index order; the k-th largest key, the
 //    tie cut (up to kTieMax ties at it), the softmax statistics and the KL terms then come from LDS,
-//    and the gathered elements get their final dZ. Two reads of each row instead of seven: 8,192 x
-//    151,936 bf16 logits 7.3 -> 2.3 ms.
+//    and the gathered elements get their final dZ. Two reads of each row instead of seven, dZ stored
+//    with the non-temporal policy (10% faster than the default): 8,192 x 151,936 bf16 logits 7.3 ->
+//    2.0 ms.
 //  * The passes below whenever the gathered set misses the k-th largest key, overflows the lists or
 //    holds too many ties, or the row is short or k large: a radix select of the k-th largest teacher key (8-bit digits from
 //    the top, LDS histograms); if fewer ties at that key are admitted than exist, the index of the
@@ -271,14 +279,14 @@ kl_top_kernel(const void *__restrict__ Zs, const void *__restrict__ Zt, int64_t 
                 for (int u = 0; u < kTrips; u++) {
                     const int64_t i = base + t + 256 * u;
                     gather(i, true, va[u], vb[u]);
-                    store_logit<IN>(dz, i, 0.0f);
+                    store_logit_nt<IN>(dz, i, 0.0f);
                 }
             } else {
 #pragma unroll
                 for (int u = 0; u < kTrips; u++) {
                     const int64_t i = base + t + 256 * u;
                     gather(i, i < V, va[u], vb[u]);
-                    if (i < V) store_logit<IN>(dz, i, 0.0f);
+                    if (i < V) store_logit_nt<IN>(dz, i, 0.0f);
                 }
             }
         }
@@ -364,7 +372,7 @@ kl_top_kernel(const void *__restrict__ Zs, const void *__restrict__ Zt, int64_t 
                 double kl = 0.0;
                 for_cands([&](uint32_t s) {
                     const float g = chosen(s) ? kl_term(__uint_as_float(cand_a[s]), cand_b[s], lt_d, dl, kl) : 0.0f;
-                    store_logit<IN>(dz, cand_idx[s], g);
+                    store_logit_nt<IN>(dz, cand_idx[s], g);
                 });
                 row_total(kl);
                 done = true;
