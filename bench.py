@@ -42,6 +42,10 @@ def parse():
     p.add_argument("--summarize-stalls", metavar="DIR",
                    help="write the wave-cycle breakdown of the GEMMs from the rocprofv3 --pmc output directory of a "
                         "--steps 1 --warmup 0 run with the counters of PMC_STALL and exit")
+    p.add_argument("--summarize-extras", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="write profiles/hbm_traffic_extras_<workload>.md (the chaining and optimizer kernels) from "
+                        "two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of a full --steps 1 --warmup 0 "
+                        "--copy-calibration run and exit")
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
@@ -131,7 +135,9 @@ def traffic_from_profile(kernel: str, src_hash: str, path):
 def main():
     args = parse()
     if (args.summarize_trace or args.summarize_counters or args.summarize_mfma or args.summarize_stalls
-            or args.summarize_memory):
+            or args.summarize_memory or args.summarize_extras):
+        if args.summarize_extras:
+            summarize_extras(*args.summarize_extras, args.workload)
         if args.summarize_trace:
             summarize_trace(args.summarize_trace, args.workload)
         if args.summarize_counters:
@@ -593,10 +599,19 @@ def chain_costs(torch, F, layers, acts, x_hat, fmt, sb, M, ws, rnd, reps=3):
                        "GBps": round(T * V * 6 / (res["kl_top"] * 1e-3) / 1e9, 1)}}
 
 
+def under_profiler():
+    """Whether rocprofv3 runs this process: its tool library is preloaded and its settings are in the
+    environment."""
+    return "rocprof" in os.environ.get("LD_PRELOAD", "") or any(k.startswith("ROCPROF") for k in os.environ)
+
+
 def gpu_clocks():
     """The GPU's clocks as rocm-smi reports them (current levels of sclk, mclk, fclk, socclk), or why
-    they could not be read."""
+    they could not be read. Under rocprofv3 no child program is started: the profiler has initialised
+    the GPU in this process before it began, and a child that execs after such a start is refused."""
     import subprocess
+    if under_profiler():
+        return {"skipped": "under rocprofv3"}
     try:
         r = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True, timeout=30)
         data = json.loads(r.stdout)
@@ -894,6 +909,74 @@ def summarize_counters(fetch_dir, write_dir, workload, out_dir=None):
     with open(os.path.join(out_dir, f"traffic_{workload}.json"), "w") as f:
         json.dump(data, f, indent=1)
     out = os.path.join(out_dir, f"hbm_traffic_{workload}.md")
+    with open(out, "w") as f:
+        f.write("\n".join(md) + "\n")
+    print(out)
+
+
+EXTRA_KERNELS = {"transpose_kernel": "transpose_kernel<", "fq_act_bwd_kernel": "fq_act_bwd_kernel<",
+                 "kl_top_kernel": "kl_top_kernel<", "adamw_kernel": "adamw_kernel"}
+EXTRAS_CMD = ("rocprofv3 --pmc {c} -d OUT/prof_extras_{d} -o run --output-format csv -- "
+              "python3 -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --copy-calibration{wl}")
+
+
+def extra_launches(kernel, w):
+    """One call's launches of a kernel outside the step, in order, with their algorithmic bytes: the
+    transposes of dX (every linear's bf16 W_hat read and written once), the activation straight-through
+    backward (every bf16 block input: X and dX_hat read, dX written), KL-Top (8,192 x 151,936 bf16 logits:
+    both rows read, dZ written) and AdamW (S_fp, then c, of every linear: p, g, m, v read, p, m, v written,
+    28 B per fp32 parameter). The bench repeats each call, so a position's launches are pooled."""
+    if kernel == "transpose_kernel":
+        return [(f"{l.name} {l.N}x{l.K}", 4 * l.N * l.K) for l in w.linears]
+    if kernel == "fq_act_bwd_kernel":
+        return [(f"{src} {w.M}x{K}", 6 * w.M * K) for src, K in w.inputs.items()]
+    if kernel == "kl_top_kernel":
+        return [("8192 x 151936 bf16, k = 1000", 8192 * 151936 * 6)]
+    out = []
+    for l in w.linears:
+        out.append((f"{l.name} S_fp {l.N}x{l.K // w.block}", 28 * l.N * (l.K // w.block)))
+        out.append((f"{l.name} c {l.N}x{l.K // w.sub_block}", 28 * l.N * (l.K // w.sub_block)))
+    return out
+
+
+def summarize_extras(fetch_dir, write_dir, workload, out_dir=None):
+    """HBM-side bytes of the calls outside the step (chaining, AdamW) against their algorithmic bytes:
+    for each launch position of a call, the median over the bench's repetitions of that call."""
+    import csv
+    import statistics
+
+    from paper_2608_01847_amd import synth
+    w = synth.WORKLOADS[workload]
+    got = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = [r for r in csv.DictReader(open(os.path.join(d, "run_counter_collection.csv")))
+                if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        copy = next(r for r in rows if "copyBuffer" in r["Kernel_Name"])
+        scale = (1 << 30) / (float(copy["Counter_Value"]) * 1024)
+        per = {}
+        for k, pat in EXTRA_KERNELS.items():
+            vals = [float(r["Counter_Value"]) * 1024 * scale for r in rows if pat in r["Kernel_Name"]]
+            n = len(extra_launches(k, w))
+            per[k] = [statistics.median(vals[i::n]) for i in range(n)] if len(vals) >= n else []
+        got[counter] = (scale, per)
+    md = [f"# HBM-side traffic of the chaining and optimizer kernels ({workload}, {w.M:,} tokens)\n",
+          "Commands (one counter per run, from the repository root on one MI355X; OUT is any output directory):\n",
+          "    " + EXTRAS_CMD.format(c="FETCH_SIZE", d="fetch", wl=wl_arg(workload)),
+          "    " + EXTRAS_CMD.format(c="WRITE_SIZE", d="write", wl=wl_arg(workload)) + "\n",
+          f"Each counter scaled by what it reads for the untimed 1 GiB device copy of the same run (FETCH_SIZE "
+          f"x{got['FETCH_SIZE'][0]:.3f}, WRITE_SIZE x{got['WRITE_SIZE'][0]:.3f}); per launch position of a call, the "
+          f"median over the bench's repetitions of the call. Algorithmic bytes: every input read and every output "
+          f"written once (bf16 tensors; AdamW 28 B per fp32 parameter). Source hash of the kernels: "
+          f"`{kernel_source_hash()}`.\n",
+          "| Kernel | Tensor | fetched MB | written MB | algorithmic MB | ratio |", "|---|---|---|---|---|---|"]
+    fetch, write = got["FETCH_SIZE"][1], got["WRITE_SIZE"][1]
+    for k in EXTRA_KERNELS:
+        if not fetch[k] or not write[k]:
+            continue
+        for (label, alg), f, wr in zip(extra_launches(k, w), fetch[k], write[k]):
+            md.append(f"| `{k}` | {label} | {f / 1e6:.1f} | {wr / 1e6:.1f} | {alg / 1e6:.1f} | {(f + wr) / alg:.2f} |")
+    out = os.path.join(out_dir or os.path.join(REPO, "profiles"), f"hbm_traffic_extras_{workload}.md")
     with open(out, "w") as f:
         f.write("\n".join(md) + "\n")
     print(out)

@@ -134,6 +134,55 @@ def test_counter_summary_maps_fakequant_launches(tmp_path):
     assert sum(l.startswith("| `fq_act_mx_kernel`") for l in text.splitlines()) == 4
 
 
+ADAMW = "focus::adamw_kernel(float*, float const*)"
+KLTOP = "void focus::(anonymous namespace)::kl_top_kernel<1>(void const*)"
+
+
+def test_extras_summary_pools_each_launch_position(tmp_path):
+    from paper_2608_01847_amd import synth
+    w = synth.WORKLOADS["block2560_mxfp4"]
+    n = 2 * len(w.linears)  # AdamW launches per call: S_fp, then c, of every linear
+    # three calls of AdamW: position j reads 10 j + 5 KiB in the middle call, +/- 1 in the others;
+    # KL-Top twice, 2000 and 4000 KiB fetched (median 3000)
+    fetch = [(1, COPY, "FETCH_SIZE", 524288.0, 10)]
+    for call, d in enumerate((-1.0, 0.0, 1.0)):
+        fetch += [(100 + call * n + j, ADAMW, "FETCH_SIZE", 10.0 * j + 5 + d, 10) for j in range(n)]
+    fetch += [(500, KLTOP, "FETCH_SIZE", 2000.0, 10), (501, KLTOP, "FETCH_SIZE", 4000.0, 10)]
+    write = [(1, COPY, "WRITE_SIZE", 1048576.0, 10)]
+    for call in range(3):
+        write += [(100 + call * n + j, ADAMW, "WRITE_SIZE", 7.0, 10) for j in range(n)]
+    write += [(500, KLTOP, "WRITE_SIZE", 100.0, 10), (501, KLTOP, "WRITE_SIZE", 100.0, 10)]
+    write_counter_csv(tmp_path / "f", fetch)
+    write_counter_csv(tmp_path / "w", write)
+    bench.summarize_extras(str(tmp_path / "f"), str(tmp_path / "w"), "block2560_mxfp4", out_dir=str(tmp_path))
+    rows = [l for l in (tmp_path / "hbm_traffic_extras_block2560_mxfp4.md").read_text().splitlines()
+            if l.startswith("| `")]
+    adam = [l for l in rows if l.startswith("| `adamw_kernel`")]
+    assert len(adam) == n
+    # position 3 (k_proj's c): fetched (10 * 3 + 5) KiB x 2, written 7 KiB x 1
+    lin = w.linears[1]
+    cells = [c.strip() for c in adam[3].split("|")]
+    assert cells[2] == f"{lin.name} c {lin.N}x{lin.K // w.sub_block}"
+    assert float(cells[3]) == pytest.approx(35 * 1024 * 2 / 1e6, abs=0.05)
+    assert float(cells[4]) == pytest.approx(7 * 1024 / 1e6, abs=0.05)
+    assert float(cells[5]) == pytest.approx(28 * lin.N * (lin.K // w.sub_block) / 1e6, abs=0.05)
+    kl = [l for l in rows if l.startswith("| `kl_top_kernel`")]
+    assert len(kl) == 1 and float(kl[0].split("|")[3]) == pytest.approx(3000 * 1024 * 2 / 1e6, abs=0.05)
+    assert not any(l.startswith("| `transpose_kernel`") for l in rows)  # no launches, no rows
+
+
+def test_no_child_program_under_the_profiler(monkeypatch):
+    def refuse(*a, **k):
+        raise AssertionError("a child program was started under the profiler")
+    monkeypatch.setattr(subprocess, "run", refuse)
+    monkeypatch.setenv("ROCPROFILER_LIBRARY_CTOR", "1")
+    assert bench.under_profiler()
+    assert bench.gpu_clocks() == {"skipped": "under rocprofv3"}
+    monkeypatch.delenv("ROCPROFILER_LIBRARY_CTOR")
+    monkeypatch.setenv("LD_PRELOAD", "/opt/rocm/lib/rocprofiler-sdk/librocprofiler-sdk-tool.so")
+    assert bench.under_profiler()
+
+
 def test_mfma_summary_row(tmp_path):
     from paper_2608_01847_amd import synth
     w = synth.WORKLOADS["block2560_mxfp4"]
